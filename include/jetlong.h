@@ -1,0 +1,163 @@
+/*
+ * jetlong.h -- C ABI of libjetlong.so: fused causal bifocal-RoPE attention
+ * (Jet-Long, arXiv 2607.07740) for AMD Instinct MI355X (gfx950).
+ *
+ * The method (Sec. 3, Eq. (1)): a query at position q attends to a key at
+ * position k <= q with the score
+ *     <R(q) x_q, R(k) x_k>            if q - k <= w_local   (local view)
+ *     <R(f(q)) x_q, R(f(k)) x_k>      if q - k >  w_local   (remote view)
+ * where R(p) is the RoPE rotation to position p, f(x) = floor(x / G) (Eq. (3))
+ * and G = max(1, ceil(L / w_pretrained)) (Eq. (2)) for the current length L.
+ * The remote rotation is applied on the fly to raw (pre-RoPE) Q/K as the
+ * correction rotation of Sec. 3.2 (Eqs. (5)-(6)); no rotated copy of K is ever
+ * written.  Local and remote partial softmax states are merged by the
+ * max-shifted, linear-space rule of Sec. 3.3, Eq. (7).
+ *
+ * Conventions shared by every entry point:
+ *  - Tensors are DEVICE pointers to contiguous row-major storage; "bf16" is
+ *    IEEE bfloat16 stored as 16-bit words.  Every tensor pointer must be
+ *    16-byte aligned.  The caller owns all tensors and workspaces.
+ *  - RoPE uses the rotate-half pairing (element i with i + head_dim/2) and
+ *    frequencies omega_i = rope_theta^(-2i/head_dim); positions are 0-based;
+ *    the softmax scale is 1/sqrt(head_dim).
+ *  - Grouped-query attention: query head h reads kv head h / (Hq / Hkv).
+ *  - head_dim must be 128 (other values return JL_ERR_UNSUPPORTED).
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream).  Arguments are validated on the host before anything is
+ *    launched; on any error nothing is written and nothing is launched.
+ *  - Thread safety: calls may come from several host threads; the library's
+ *    only shared state (a per-device cache of cos/sin tables) is guarded by a
+ *    mutex.  Calls that share output buffers must be ordered by the caller.
+ *  - Status codes are returned; no exception crosses the ABI and nothing
+ *    aborts.  jl_last_error() gives a human-readable detail for the calling
+ *    thread's most recent failure.
+ */
+#ifndef JETLONG_H
+#define JETLONG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  JL_OK = 0,
+  JL_ERR_INVALID_ARG = 1, /* bad shape, pointer, alignment or window value      */
+  JL_ERR_UNSUPPORTED = 2, /* valid but not built (head_dim != 128, GQA group)   */
+  JL_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required         */
+  JL_ERR_HIP = 4          /* HIP runtime error (launch, allocation, no device)  */
+};
+
+/* Name of a status code ("JL_OK", ...); never NULL. */
+const char* jl_status_string(int status);
+
+/* Detail message of the calling thread's last failed call ("" if none). */
+const char* jl_last_error(void);
+
+/* ABI version: major * 10000 + minor * 100 + patch. */
+int jl_version(void);
+
+/*
+ * Group size of Sec. 3.1, Eq. (2), computed on the host:
+ * G = max(1, ceil(L / w_pretrained)).  Returns -1 if L < 1 or w_pretrained < 1.
+ */
+int64_t jl_group_size(int64_t L, int64_t w_pretrained);
+
+/*
+ * Bifocal prefill (Sec. 3, Eq. (1); merge of Sec. 3.3, Eq. (7)).
+ *   q   bf16 [B, L, Hq, head_dim]   raw (pre-RoPE) queries, position = row index
+ *   k   bf16 [B, L, Hkv, head_dim]  raw (pre-RoPE) keys
+ *   v   bf16 [B, L, Hkv, head_dim]
+ *   o   bf16 [B, L, Hq, head_dim]   output (written)
+ *   lse fp32 [B, Hq, L] or NULL     natural-log softmax normaliser per row
+ * One G for the whole call, from this call's L (all B sequences share L).
+ * w_pretrained >= 1, w_local >= 0; keys with q - k <= w_local use the base
+ * rotation, older keys the remote one.  When G == 1 the output equals
+ * jl_rope_attention bit for bit (the method reduces to the base model).
+ * Requires Hq % Hkv == 0 and 128 % (Hq / Hkv) == 0.
+ */
+int jl_bifocal_prefill(const void* q, const void* k, const void* v, void* o, float* lse, int B,
+                       int Hq, int Hkv, int L, int head_dim, double rope_theta, int w_pretrained,
+                       int w_local, void* stream);
+
+/*
+ * Vanilla causal RoPE attention with the same tiling and in-register RoPE of
+ * raw Q/K at base positions: the base model of Sec. 3 and the denominator of
+ * the overhead measurements.  Arguments as in jl_bifocal_prefill.
+ */
+int jl_rope_attention(const void* q, const void* k, const void* v, void* o, float* lse, int B,
+                      int Hq, int Hkv, int L, int head_dim, double rope_theta, void* stream);
+
+/*
+ * Bytes of device workspace the decode entry points need for this shape
+ * (split-K partial softmax states).  Returns 0 for invalid arguments.
+ */
+size_t jl_decode_workspace_bytes(int B, int Hq, int Hkv, int max_len, int head_dim);
+
+/*
+ * Bifocal single-query decode on a raw KV cache (Sec. 3.2, Eqs. (4)-(6)).
+ *   q        bf16 [B, Hq, head_dim]           raw new queries; the query of
+ *                                              sequence b sits at position
+ *                                              kv_lens[b] - 1
+ *   k_cache  bf16 [B, max_len, Hkv, head_dim] raw (pre-RoPE) keys, the new
+ *                                              token already appended
+ *   v_cache  bf16 [B, max_len, Hkv, head_dim]
+ *   kv_lens  int32 [B] DEVICE array, 1 <= kv_lens[b] <= max_len; positions
+ *            at or past kv_lens[b] are never read
+ *   o        bf16 [B, Hq, head_dim] output (written)
+ *   workspace, workspace_bytes: device scratch of at least
+ *            jl_decode_workspace_bytes(B, Hq, Hkv, max_len, head_dim) bytes,
+ *            16-byte aligned; its contents on entry do not matter.
+ * G is taken per sequence from L = kv_lens[b] on the device, so one cache
+ * serves every length and G change without being rewritten.
+ * Requires Hq % Hkv == 0 and Hq / Hkv <= 8.
+ */
+int jl_bifocal_decode(const void* q, const void* k_cache, const void* v_cache,
+                      const int32_t* kv_lens, int max_len, void* o, int B, int Hq, int Hkv,
+                      int head_dim, double rope_theta, int w_pretrained, int w_local,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Vanilla RoPE decode with the same kernels (base rotation for every key). */
+int jl_rope_attention_decode(const void* q, const void* k_cache, const void* v_cache,
+                             const int32_t* kv_lens, int max_len, void* o, int B, int Hq,
+                             int Hkv, int head_dim, double rope_theta, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
+/*
+ * Debug view of the schedule as the device computes it (Eqs. (2), (3), (5)),
+ * for bit-exact tests.  All pointers are device pointers.
+ *   lengths    int32 [n_lengths]              sequence lengths L (>= 1)
+ *   positions  int32 [n_positions]            positions x (>= 0)
+ *   group_out  int32 [n_lengths]              G(L)
+ *   remote_out int32 [n_lengths, n_positions] f(x) = floor(x / G(L))
+ *   offset_out int32 [n_lengths, n_positions] Delta(x) = f(x) - x
+ */
+int jl_debug_schedule(const int32_t* lengths, int n_lengths, const int32_t* positions,
+                      int n_positions, int w_pretrained, int32_t* group_out, int32_t* remote_out,
+                      int32_t* offset_out, void* stream);
+
+/* Tile classes written by jl_debug_prefill_tiles. */
+enum { JL_TILE_SKIP = 0, JL_TILE_LOCAL = 1, JL_TILE_REMOTE = 2, JL_TILE_MIXED = 3 };
+
+/*
+ * Debug view of the prefill kernel's tile classification (Eq. (1)'s window
+ * boundary at tile granularity), computed on the device with the kernel's own
+ * block sizes.  Writes int8 classes_out[n_qblocks, n_ktiles] (device) and the
+ * block geometry to the host ints *block_q, *block_k, *n_qblocks, *n_ktiles.
+ * classes_len is the capacity of classes_out in elements.
+ */
+int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_out,
+                           int64_t classes_len, int* block_q, int* block_k, int* n_qblocks,
+                           int* n_ktiles, void* stream);
+
+/* Frees the library-owned cos/sin tables on every device (they are rebuilt
+ * on demand).  Must not race with running calls. */
+void jl_release_caches(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JETLONG_H */

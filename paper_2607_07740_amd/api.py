@@ -1,0 +1,216 @@
+"""Thin ctypes binding of libjetlong.so (C ABI in include/jetlong.h).
+
+Argument marshalling only: every step of the attention runs in the library's
+HIP kernels.  PyTorch supplies device memory and the current stream.  If the
+library is not built this module raises -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libjetlong.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "jetlong.h")
+
+JL_OK, JL_ERR_INVALID_ARG, JL_ERR_UNSUPPORTED, JL_ERR_WORKSPACE, JL_ERR_HIP = range(5)
+TILE_SKIP, TILE_LOCAL, TILE_REMOTE, TILE_MIXED = range(4)
+
+_lib = None
+
+
+class JetLongError(RuntimeError):
+    def __init__(self, status: int, name: str, detail: str):
+        super().__init__("%s (%d): %s" % (name, status, detail))
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load libjetlong.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libjetlong.so is not built (run __graft_entry__.build()); "
+                               "the HIP library is the only implementation")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, dbl, sz = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double,
+                                 ctypes.c_size_t)
+        L.jl_status_string.restype = ctypes.c_char_p
+        L.jl_status_string.argtypes = [i32]
+        L.jl_last_error.restype = ctypes.c_char_p
+        L.jl_last_error.argtypes = []
+        L.jl_version.restype = i32
+        L.jl_version.argtypes = []
+        L.jl_group_size.restype = i64
+        L.jl_group_size.argtypes = [i64, i64]
+        L.jl_bifocal_prefill.restype = i32
+        L.jl_bifocal_prefill.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl, i32,
+                                         i32, vp]
+        L.jl_rope_attention.restype = i32
+        L.jl_rope_attention.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl, vp]
+        L.jl_decode_workspace_bytes.restype = sz
+        L.jl_decode_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
+        L.jl_bifocal_decode.restype = i32
+        L.jl_bifocal_decode.argtypes = [vp, vp, vp, vp, i32, vp, i32, i32, i32, i32, dbl, i32, i32,
+                                        vp, sz, vp]
+        L.jl_rope_attention_decode.restype = i32
+        L.jl_rope_attention_decode.argtypes = [vp, vp, vp, vp, i32, vp, i32, i32, i32, i32, dbl,
+                                               vp, sz, vp]
+        L.jl_debug_schedule.restype = i32
+        L.jl_debug_schedule.argtypes = [vp, i32, vp, i32, i32, vp, vp, vp, vp]
+        L.jl_debug_prefill_tiles.restype = i32
+        L.jl_debug_prefill_tiles.argtypes = [i32, i32, i32, i32, vp, i64,
+                                             ctypes.POINTER(i32), ctypes.POINTER(i32),
+                                             ctypes.POINTER(i32), ctypes.POINTER(i32), vp]
+        L.jl_release_caches.restype = None
+        L.jl_release_caches.argtypes = []
+        _lib = L
+    return _lib
+
+
+def declared_functions() -> list:
+    """Function names declared in include/jetlong.h."""
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(jl_[a-z0-9_]+)\s*\(", src)))
+
+
+def _check(status: int) -> None:
+    if status != JL_OK:
+        L = lib()
+        raise JetLongError(status, L.jl_status_string(status).decode(),
+                           L.jl_last_error().decode())
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t, name, dtype=None):
+    import torch
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError("%s must be a CUDA (HIP) tensor" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def group_size(L: int, w_pretrained: int) -> int:
+    return int(lib().jl_group_size(L, w_pretrained))
+
+
+def _prefill(bifocal, q, k, v, w_pretrained, w_local, rope_theta, out, lse, want_lse, stream):
+    import torch
+    B, L, Hq, D = q.shape
+    Hkv = k.shape[2]
+    if k.shape != (B, L, Hkv, D) or v.shape != k.shape:
+        raise ValueError("k and v must be [B, L, Hkv, D] matching q [B, L, Hq, D]")
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, L), dtype=torch.float32, device=q.device)
+    args = [_dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
+            _dev(v, "v", torch.bfloat16), _dev(out, "out", torch.bfloat16),
+            _dev(lse, "lse", torch.float32) if lse is not None else None, B, Hq, Hkv, L, D,
+            float(rope_theta)]
+    if bifocal:
+        _check(lib().jl_bifocal_prefill(*args, int(w_pretrained), int(w_local), _stream(stream)))
+    else:
+        _check(lib().jl_rope_attention(*args, _stream(stream)))
+    return (out, lse) if want_lse else out
+
+
+def bifocal_prefill(q, k, v, *, w_pretrained: int, w_local: int, rope_theta: float = 1e6,
+                    out=None, lse=None, want_lse: bool = False, stream=None):
+    """jl_bifocal_prefill: q [B, L, Hq, 128], k/v [B, L, Hkv, 128] raw bf16 -> out bf16."""
+    return _prefill(True, q, k, v, w_pretrained, w_local, rope_theta, out, lse,
+                    want_lse or lse is not None, stream)
+
+
+def rope_attention(q, k, v, *, rope_theta: float = 1e6, out=None, lse=None,
+                   want_lse: bool = False, stream=None):
+    """jl_rope_attention: vanilla causal RoPE attention with the same kernel."""
+    return _prefill(False, q, k, v, 1, 0, rope_theta, out, lse, want_lse or lse is not None,
+                    stream)
+
+
+def decode_workspace_bytes(B: int, Hq: int, Hkv: int, max_len: int, head_dim: int = 128) -> int:
+    return int(lib().jl_decode_workspace_bytes(B, Hq, Hkv, max_len, head_dim))
+
+
+def _decode(bifocal, q, k_cache, v_cache, kv_lens, w_pretrained, w_local, rope_theta, out,
+            workspace, stream):
+    import torch
+    B, Hq, D = q.shape
+    _, max_len, Hkv, _ = k_cache.shape
+    if k_cache.shape != (B, max_len, Hkv, D) or v_cache.shape != k_cache.shape:
+        raise ValueError("caches must be [B, max_len, Hkv, D]")
+    if kv_lens.shape != (B,):
+        raise ValueError("kv_lens must be [B]")
+    if out is None:
+        out = torch.empty_like(q)
+    need = decode_workspace_bytes(B, Hq, Hkv, max_len, D)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    args = [_dev(q, "q", torch.bfloat16), _dev(k_cache, "k_cache", torch.bfloat16),
+            _dev(v_cache, "v_cache", torch.bfloat16), _dev(kv_lens, "kv_lens", torch.int32),
+            max_len, _dev(out, "out", torch.bfloat16), B, Hq, Hkv, D, float(rope_theta)]
+    ws = [_dev(workspace, "workspace"), workspace.numel() * workspace.element_size()]
+    if bifocal:
+        _check(lib().jl_bifocal_decode(*args, int(w_pretrained), int(w_local), *ws,
+                                       _stream(stream)))
+    else:
+        _check(lib().jl_rope_attention_decode(*args, *ws, _stream(stream)))
+    return out
+
+
+def bifocal_decode(q, k_cache, v_cache, kv_lens, *, w_pretrained: int, w_local: int,
+                   rope_theta: float = 1e6, out=None, workspace=None, stream=None):
+    """jl_bifocal_decode: q [B, Hq, 128] raw, caches [B, max_len, Hkv, 128] raw, kv_lens int32."""
+    return _decode(True, q, k_cache, v_cache, kv_lens, w_pretrained, w_local, rope_theta, out,
+                   workspace, stream)
+
+
+def rope_attention_decode(q, k_cache, v_cache, kv_lens, *, rope_theta: float = 1e6, out=None,
+                          workspace=None, stream=None):
+    """jl_rope_attention_decode: vanilla RoPE decode with the same kernels."""
+    return _decode(False, q, k_cache, v_cache, kv_lens, 1, 0, rope_theta, out, workspace, stream)
+
+
+def debug_schedule(lengths, positions, w_pretrained: int, stream=None):
+    """jl_debug_schedule: device-computed G(L), f(x), Delta(x) (int32 CUDA tensors)."""
+    import torch
+    nl, npos = lengths.numel(), positions.numel()
+    g = torch.empty(nl, dtype=torch.int32, device=lengths.device)
+    f = torch.empty((nl, npos), dtype=torch.int32, device=lengths.device)
+    dlt = torch.empty((nl, npos), dtype=torch.int32, device=lengths.device)
+    _check(lib().jl_debug_schedule(_dev(lengths, "lengths", torch.int32), nl,
+                                   _dev(positions, "positions", torch.int32), npos,
+                                   int(w_pretrained), _dev(g, "g"), _dev(f, "f"), _dev(dlt, "d"),
+                                   _stream(stream)))
+    return g, f, dlt
+
+
+def debug_prefill_tiles(L: int, Hq: int, Hkv: int, w_local: int, device="cuda", stream=None):
+    """jl_debug_prefill_tiles: (classes int8 [n_qblocks, n_ktiles], block_q, block_k)."""
+    import torch
+    bq, bk, nq, nk = (ctypes.c_int(), ctypes.c_int(), ctypes.c_int(), ctypes.c_int())
+    # first call with no buffer reports the geometry
+    lib().jl_debug_prefill_tiles(L, Hq, Hkv, w_local, None, 0, ctypes.byref(bq),
+                                 ctypes.byref(bk), ctypes.byref(nq), ctypes.byref(nk), None)
+    if nq.value <= 0:
+        _check(JL_ERR_INVALID_ARG)
+    out = torch.empty((nq.value, nk.value), dtype=torch.int8, device=device)
+    _check(lib().jl_debug_prefill_tiles(L, Hq, Hkv, w_local, _dev(out, "classes"), out.numel(),
+                                        ctypes.byref(bq), ctypes.byref(bk), ctypes.byref(nq),
+                                        ctypes.byref(nk), _stream(stream)))
+    return out, bq.value, bk.value
+
+
+def release_caches() -> None:
+    lib().jl_release_caches()

@@ -1,0 +1,75 @@
+// aux.hip -- RoPE cos/sin tables and the debug views of the device schedule.
+#include "jl_device.h"
+
+namespace jl {
+
+struct Omega {
+  double w[kHalf];  // omega_i = theta^(-2i/d), computed on the host in fp64
+};
+
+// table[p][i] = (cos(p * omega_i), sin(p * omega_i)): the angle and its
+// trigonometric functions are evaluated in fp64 and rounded once to fp32
+// (positions reach ~1.3e5, where an fp32 angle would be off by ~1e-2 rad).
+__global__ void build_table_kernel(float2* table, int n_pos, Omega om) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)n_pos * kHalf) return;
+  const int p = (int)(idx >> 6);
+  const int i = (int)(idx & 63);
+  double s, c;
+  sincos((double)p * om.w[i], &s, &c);
+  table[idx] = make_float2((float)c, (float)s);
+}
+
+hipError_t launch_build_table(float2* table, int n_pos, const double* omega, hipStream_t stream) {
+  Omega om;
+  for (int i = 0; i < kHalf; ++i) om.w[i] = omega[i];
+  const long long n = (long long)n_pos * kHalf;
+  const unsigned blocks = (unsigned)((n + 255) / 256);
+  hipLaunchKernelGGL(build_table_kernel, dim3(blocks), dim3(256), 0, stream, table, n_pos, om);
+  return hipGetLastError();
+}
+
+__global__ void debug_schedule_kernel(const int32_t* lengths, int nl, const int32_t* positions,
+                                      int np, int w, int32_t* gout, int32_t* fout,
+                                      int32_t* dout) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)nl * np) return;
+  const int li = (int)(idx / np);
+  const int pi = (int)(idx - (long long)li * np);
+  const int G = group_size(lengths[li], w);
+  const int x = positions[pi];
+  fout[idx] = remote_pos(x, G);
+  dout[idx] = pos_offset(x, G);
+  if (pi == 0) gout[li] = G;
+}
+
+hipError_t launch_debug_schedule(const int32_t* lengths, int nl, const int32_t* positions, int np,
+                                 int w, int32_t* gout, int32_t* fout, int32_t* dout,
+                                 hipStream_t stream) {
+  const long long n = (long long)nl * np;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(debug_schedule_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                     stream, lengths, nl, positions, np, w, gout, fout, dout);
+  return hipGetLastError();
+}
+
+__global__ void debug_tiles_kernel(int L, int BQ, int BK, int w0, int nqb, int nkt, int8_t* out) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)nqb * nkt) return;
+  const int qb = (int)(idx / nkt);
+  const int kt = (int)(idx - (long long)qb * nkt);
+  const int q0 = qb * BQ, q1 = min(q0 + BQ, L) - 1;
+  const int k0 = kt * BK, k1 = min(k0 + BK, L) - 1;
+  out[idx] = (int8_t)tile_class(q0, q1, k0, k1, w0);
+}
+
+hipError_t launch_debug_tiles(int L, int BQ, int BK, int w0, int nqb, int nkt, int8_t* out,
+                              hipStream_t stream) {
+  const long long n = (long long)nqb * nkt;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(debug_tiles_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
+                     L, BQ, BK, w0, nqb, nkt, out);
+  return hipGetLastError();
+}
+
+}  // namespace jl

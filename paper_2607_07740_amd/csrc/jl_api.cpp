@@ -1,0 +1,306 @@
+// jl_api.cpp -- host side of libjetlong.so: the C ABI declared in
+// include/jetlong.h.  Validates every argument before anything is launched,
+// owns the per-device cache of RoPE cos/sin tables, and dispatches the
+// gfx950 kernels.  See the header for the contract of each entry point.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/jetlong.h"
+
+namespace jl {
+// kernels (prefill.hip, decode.hip, aux.hip)
+hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                          uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
+                          int L, int G, int w0, hipStream_t stream);
+int prefill_block_q(int g);
+int prefill_block_k();
+size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len);
+hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                         const int32_t* kv_lens, int max_len, uint16_t* o, const float2* table,
+                         int B, int Hq, int Hkv, int w_pre, int w0, float* ws,
+                         hipStream_t stream);
+hipError_t launch_build_table(float2* table, int n_pos, const double* omega, hipStream_t stream);
+hipError_t launch_debug_schedule(const int32_t* lengths, int nl, const int32_t* positions, int np,
+                                 int w, int32_t* gout, int32_t* fout, int32_t* dout,
+                                 hipStream_t stream);
+hipError_t launch_debug_tiles(int L, int BQ, int BK, int w0, int nqb, int nkt, int8_t* out,
+                              hipStream_t stream);
+}  // namespace jl
+
+namespace {
+
+constexpr int kHeadDim = 128;
+thread_local std::string t_detail;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  t_detail = buf;
+  return status;
+}
+
+int ok() {
+  t_detail.clear();
+  return JL_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(JL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+bool aligned4(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 3) == 0; }
+
+// ------------------------------------------------------------ table cache
+struct TableEntry {
+  int device;
+  double theta;
+  int cap;  // positions held
+  float2* ptr;
+};
+std::mutex g_mu;
+std::vector<TableEntry> g_tables;
+std::vector<std::pair<int, float2*>> g_retired;  // superseded tables, freed by jl_release_caches
+
+// Returns a device table covering positions [0, n_pos) for the current device.
+int get_table(double theta, int n_pos, hipStream_t stream, const float2** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_mu);
+  TableEntry* found = nullptr;
+  for (auto& t : g_tables)
+    if (t.device == dev && t.theta == theta) found = &t;
+  if (found && found->cap >= n_pos) {
+    *out = found->ptr;
+    return JL_OK;
+  }
+  long long cap = 4096;
+  while (cap < n_pos) cap *= 2;
+  if (found && cap < 2LL * found->cap) cap = 2LL * found->cap;
+  if (cap > (1LL << 30) / 64) cap = n_pos;  // keep the element count in range
+  float2* p = nullptr;
+  e = hipMalloc(&p, (size_t)cap * 64 * sizeof(float2));
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc(rope table)");
+  double omega[64];
+  for (int i = 0; i < 64; ++i) omega[i] = std::pow(theta, -2.0 * i / (double)kHeadDim);
+  e = jl::launch_build_table(p, (int)cap, omega, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);  // usable from any stream afterwards
+  if (e != hipSuccess) {
+    (void)hipFree(p);
+    return hip_fail(e, "building rope table");
+  }
+  if (found) {
+    g_retired.emplace_back(found->device, found->ptr);
+    found->ptr = p;
+    found->cap = (int)cap;
+  } else {
+    g_tables.push_back(TableEntry{dev, theta, (int)cap, p});
+  }
+  *out = p;
+  return JL_OK;
+}
+
+int check_common(int B, int Hq, int Hkv, int head_dim, double theta) {
+  if (B < 1 || Hq < 1 || Hkv < 1)
+    return fail(JL_ERR_INVALID_ARG, "B, Hq, Hkv must be >= 1 (got %d, %d, %d)", B, Hq, Hkv);
+  if (Hq % Hkv != 0)
+    return fail(JL_ERR_INVALID_ARG, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
+  if (head_dim < 2 || head_dim % 2 != 0)
+    return fail(JL_ERR_INVALID_ARG, "head_dim must be even and >= 2 (got %d)", head_dim);
+  if (head_dim != kHeadDim)
+    return fail(JL_ERR_UNSUPPORTED, "head_dim %d not built (only 128)", head_dim);
+  if (!(theta > 0.0) || !std::isfinite(theta))
+    return fail(JL_ERR_INVALID_ARG, "rope_theta must be finite and > 0");
+  return JL_OK;
+}
+
+int prefill_common(bool bifocal, const void* q, const void* k, const void* v, void* o, float* lse,
+                   int B, int Hq, int Hkv, int L, int head_dim, double theta, int w_pre, int w0,
+                   void* stream) {
+  int st = check_common(B, Hq, Hkv, head_dim, theta);
+  if (st != JL_OK) return st;
+  if (L < 1) return fail(JL_ERR_INVALID_ARG, "L must be >= 1 (got %d)", L);
+  if (bifocal && w_pre < 1)
+    return fail(JL_ERR_INVALID_ARG, "w_pretrained must be >= 1 (got %d)", w_pre);
+  if (bifocal && w0 < 0) return fail(JL_ERR_INVALID_ARG, "w_local must be >= 0 (got %d)", w0);
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+    return fail(JL_ERR_INVALID_ARG, "q, k, v, o must be non-null and 16-byte aligned");
+  if (lse != nullptr && !aligned4(lse)) return fail(JL_ERR_INVALID_ARG, "lse must be 4-byte aligned");
+  const int g = Hq / Hkv;
+  if (128 % g != 0)
+    return fail(JL_ERR_UNSUPPORTED, "GQA group Hq/Hkv = %d must divide 128", g);
+  const long long nqb = (L + (128 / g) - 1) / (128 / g);
+  if (nqb * B * Hkv > 0x7fffffffLL) return fail(JL_ERR_INVALID_ARG, "problem too large");
+  const int G = bifocal ? (int)jl_group_size(L, w_pre) : 1;
+  const float2* table = nullptr;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  st = get_table(theta, L, s, &table);
+  if (st != JL_OK) return st;
+  // G == 1: f is the identity and the method is the base model (Sec. 3), so
+  // the bifocal entry runs the vanilla kernel and matches it bit for bit.
+  const bool use_bifocal = bifocal && G > 1;
+  hipError_t e = jl::launch_prefill(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,
+                                    (const uint16_t*)v, (uint16_t*)o, lse, table, B, Hq, Hkv, L,
+                                    G, w0, s);
+  if (e != hipSuccess) return hip_fail(e, "prefill launch");
+  return ok();
+}
+
+int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
+                  const int32_t* kv_lens, int max_len, void* o, int B, int Hq, int Hkv,
+                  int head_dim, double theta, int w_pre, int w0, void* ws, size_t ws_bytes,
+                  void* stream) {
+  int st = check_common(B, Hq, Hkv, head_dim, theta);
+  if (st != JL_OK) return st;
+  if (max_len < 1) return fail(JL_ERR_INVALID_ARG, "max_len must be >= 1 (got %d)", max_len);
+  if (bifocal && w_pre < 1)
+    return fail(JL_ERR_INVALID_ARG, "w_pretrained must be >= 1 (got %d)", w_pre);
+  if (bifocal && w0 < 0) return fail(JL_ERR_INVALID_ARG, "w_local must be >= 0 (got %d)", w0);
+  if (!aligned16(q) || !aligned16(kc) || !aligned16(vc) || !aligned16(o))
+    return fail(JL_ERR_INVALID_ARG, "q, k_cache, v_cache, o must be non-null and 16-byte aligned");
+  if (!aligned4(kv_lens)) return fail(JL_ERR_INVALID_ARG, "kv_lens must be non-null and aligned");
+  if (Hq / Hkv > 8) return fail(JL_ERR_UNSUPPORTED, "decode GQA group %d > 8", Hq / Hkv);
+  const size_t need = jl::decode_workspace_bytes(B, Hq, Hkv, max_len);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(JL_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  if (!aligned16(ws)) return fail(JL_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+  const float2* table = nullptr;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  st = get_table(theta, max_len, s, &table);
+  if (st != JL_OK) return st;
+  hipError_t e = jl::launch_decode(bifocal, (const uint16_t*)q, (const uint16_t*)kc,
+                                   (const uint16_t*)vc, kv_lens, max_len, (uint16_t*)o, table, B,
+                                   Hq, Hkv, w_pre, w0, (float*)ws, s);
+  if (e != hipSuccess) return hip_fail(e, "decode launch");
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* jl_status_string(int status) {
+  switch (status) {
+    case JL_OK: return "JL_OK";
+    case JL_ERR_INVALID_ARG: return "JL_ERR_INVALID_ARG";
+    case JL_ERR_UNSUPPORTED: return "JL_ERR_UNSUPPORTED";
+    case JL_ERR_WORKSPACE: return "JL_ERR_WORKSPACE";
+    case JL_ERR_HIP: return "JL_ERR_HIP";
+    default: return "JL_ERR_UNKNOWN";
+  }
+}
+
+const char* jl_last_error(void) { return t_detail.c_str(); }
+
+int jl_version(void) { return 100; }
+
+int64_t jl_group_size(int64_t L, int64_t w_pretrained) {
+  if (L < 1 || w_pretrained < 1) return -1;
+  if (L <= w_pretrained) return 1;
+  return (L + w_pretrained - 1) / w_pretrained;
+}
+
+int jl_bifocal_prefill(const void* q, const void* k, const void* v, void* o, float* lse, int B,
+                       int Hq, int Hkv, int L, int head_dim, double rope_theta, int w_pretrained,
+                       int w_local, void* stream) {
+  return prefill_common(true, q, k, v, o, lse, B, Hq, Hkv, L, head_dim, rope_theta, w_pretrained,
+                        w_local, stream);
+}
+
+int jl_rope_attention(const void* q, const void* k, const void* v, void* o, float* lse, int B,
+                      int Hq, int Hkv, int L, int head_dim, double rope_theta, void* stream) {
+  return prefill_common(false, q, k, v, o, lse, B, Hq, Hkv, L, head_dim, rope_theta, 1, 0,
+                        stream);
+}
+
+size_t jl_decode_workspace_bytes(int B, int Hq, int Hkv, int max_len, int head_dim) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || max_len < 1 || head_dim != kHeadDim) return 0;
+  return jl::decode_workspace_bytes(B, Hq, Hkv, max_len);
+}
+
+int jl_bifocal_decode(const void* q, const void* k_cache, const void* v_cache,
+                      const int32_t* kv_lens, int max_len, void* o, int B, int Hq, int Hkv,
+                      int head_dim, double rope_theta, int w_pretrained, int w_local,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_common(true, q, k_cache, v_cache, kv_lens, max_len, o, B, Hq, Hkv, head_dim,
+                       rope_theta, w_pretrained, w_local, workspace, workspace_bytes, stream);
+}
+
+int jl_rope_attention_decode(const void* q, const void* k_cache, const void* v_cache,
+                             const int32_t* kv_lens, int max_len, void* o, int B, int Hq,
+                             int Hkv, int head_dim, double rope_theta, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  return decode_common(false, q, k_cache, v_cache, kv_lens, max_len, o, B, Hq, Hkv, head_dim,
+                       rope_theta, 1, 0, workspace, workspace_bytes, stream);
+}
+
+int jl_debug_schedule(const int32_t* lengths, int n_lengths, const int32_t* positions,
+                      int n_positions, int w_pretrained, int32_t* group_out, int32_t* remote_out,
+                      int32_t* offset_out, void* stream) {
+  if (n_lengths < 0 || n_positions < 0)
+    return fail(JL_ERR_INVALID_ARG, "counts must be >= 0");
+  if (w_pretrained < 1) return fail(JL_ERR_INVALID_ARG, "w_pretrained must be >= 1");
+  if (n_lengths > 0 && n_positions > 0) {
+    if (!aligned4(lengths) || !aligned4(positions) || !aligned4(group_out) ||
+        !aligned4(remote_out) || !aligned4(offset_out))
+      return fail(JL_ERR_INVALID_ARG, "null or misaligned pointer");
+    if ((long long)n_lengths * n_positions > 0x7fffffffLL)
+      return fail(JL_ERR_INVALID_ARG, "problem too large");
+  }
+  hipError_t e = jl::launch_debug_schedule(lengths, n_lengths, positions, n_positions,
+                                           w_pretrained, group_out, remote_out, offset_out,
+                                           reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "debug schedule launch");
+  return ok();
+}
+
+int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_out,
+                           int64_t classes_len, int* block_q, int* block_k, int* n_qblocks,
+                           int* n_ktiles, void* stream) {
+  if (L < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || w_local < 0)
+    return fail(JL_ERR_INVALID_ARG, "invalid L, Hq, Hkv or w_local");
+  if (128 % (Hq / Hkv) != 0) return fail(JL_ERR_UNSUPPORTED, "GQA group must divide 128");
+  if (!block_q || !block_k || !n_qblocks || !n_ktiles)
+    return fail(JL_ERR_INVALID_ARG, "null geometry pointer");
+  const int BQ = jl::prefill_block_q(Hq / Hkv), BK = jl::prefill_block_k();
+  const int nqb = (L + BQ - 1) / BQ, nkt = (L + BK - 1) / BK;
+  *block_q = BQ;
+  *block_k = BK;
+  *n_qblocks = nqb;
+  *n_ktiles = nkt;
+  if (classes_out == nullptr || classes_len < (int64_t)nqb * nkt)
+    return fail(JL_ERR_INVALID_ARG, "classes_out needs %lld elements",
+                (long long)nqb * nkt);
+  hipError_t e = jl::launch_debug_tiles(L, BQ, BK, w_local, nqb, nkt, classes_out,
+                                        reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "debug tiles launch");
+  return ok();
+}
+
+void jl_release_caches(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  int cur = 0;
+  const bool have_cur = hipGetDevice(&cur) == hipSuccess;
+  for (auto& t : g_tables) {
+    if (hipSetDevice(t.device) == hipSuccess) (void)hipFree(t.ptr);
+  }
+  for (auto& r : g_retired) {
+    if (hipSetDevice(r.first) == hipSuccess) (void)hipFree(r.second);
+  }
+  g_tables.clear();
+  g_retired.clear();
+  if (have_cur) (void)hipSetDevice(cur);
+}
+
+}  // extern "C"

@@ -1,0 +1,107 @@
+// jl_device.h -- device-side building blocks shared by the gfx950 kernels:
+// the integer schedule of Jet-Long (arXiv 2607.07740, Sec. 3.1 Eqs. (2)-(3),
+// Sec. 3.2 Eq. (5)), the tile classification of Eq. (1)'s window boundary, and
+// small wave-level helpers (bf16 packing, lane exchange, transposing LDS read).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace jl {
+
+constexpr int kHeadDim = 128;
+constexpr int kHalf = 64;  // rotate-half partner offset and number of RoPE frequencies
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- schedule
+// Eq. (2): G = max(1, ceil(L / w)).  Integer ceiling, no floating point.
+__host__ __device__ inline int group_size(int L, int w) {
+  if (L <= w) return 1;
+  return (int)(((int64_t)L + w - 1) / w);
+}
+// Eq. (3): f(x) = floor(x / G) for x >= 0 (truncating division is the floor).
+__host__ __device__ inline int remote_pos(int x, int G) { return (int)((unsigned)x / (unsigned)G); }
+// Eq. (5): Delta(x) = f(x) - x.
+__host__ __device__ inline int pos_offset(int x, int G) { return remote_pos(x, G) - x; }
+
+// Tile classes over a query block [q0, q1] x key tile [k0, k1] (inclusive,
+// already clipped to the sequence).  Eq. (1): a causal pair is local iff
+// q - k <= w0 and remote iff q - k > w0.  A class names the set of element
+// classes present among the tile's causal pairs.
+enum TileClass : int { kSkip = 0, kLocal = 1, kRemote = 2, kMixed = 3 };
+
+__host__ __device__ inline int tile_class(int q0, int q1, int k0, int k1, int w0) {
+  if (k0 > q1) return kSkip;           // no causal pair
+  if (q1 - k0 <= w0) return kLocal;    // the widest pair is inside the band
+  if (q0 - k1 > w0) return kRemote;    // the narrowest pair is outside it
+  return kMixed;
+}
+
+// ------------------------------------------------------------ wave helpers
+__device__ inline float bf16_lo(unsigned w) { return __uint_as_float(w << 16); }
+__device__ inline float bf16_hi(unsigned w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Unpack 8 bf16 (one 16-byte vector) to fp32.
+__device__ inline void unpack8(const u32x4 v, float* f) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    f[2 * j] = bf16_lo(v[j]);
+    f[2 * j + 1] = bf16_hi(v[j]);
+  }
+}
+
+// Pack 8 fp32 to bf16 with round-to-nearest-even (hardware conversion).
+__device__ inline bf16x8 pack8(const float* f) {
+  f32x8 t;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) t[j] = f[j];
+  return __builtin_convertvector(t, bf16x8);
+}
+
+// Exchange a 16-byte vector with the lane 8 positions away inside its 16-lane
+// row (lane i <-> lane i ^ 8), via DPP row rotation.
+__device__ inline u32x4 swap_half_row(u32x4 v) {
+  u32x4 r;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    r[j] = (unsigned)__builtin_amdgcn_update_dpp((int)0, (int)v[j], 0x128 /* row_ror:8 */, 0xf,
+                                                 0xf, false);
+  return r;
+}
+
+__device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Transposing LDS read (gfx950 ds_read_b64_tr_b16).  Inside each 16-lane group
+// lane j supplies the address of 4 consecutive 16-bit elements; lane i receives
+// element i of each of the 4 lane quads.  With lane j pointing at
+// M[r0 + j/4][c0 + 4*(j%4)], lane i receives M[r0 + s][c0 + i] for s = 0..3:
+// one column of a 4 x 16 block of a row-major matrix.
+__device__ inline i16x4 lds_read_tr4(const void* lds_ptr) {
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_i16x4*)(__attribute__((address_space(3))) void*)(lds_ptr));
+}
+
+__device__ inline bf16x8 concat_tr(i16x4 a, i16x4 b) {
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  i16x8 r = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return __builtin_bit_cast(bf16x8, r);
+}
+
+__device__ inline f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ inline u32x4 load16(const void* p) { return *(const u32x4*)p; }
+
+}  // namespace jl

@@ -1,0 +1,120 @@
+"""The C ABI without a GPU: symbols, status strings, host schedule, argument checks.
+
+Every invalid call below must be rejected on the host before anything touches
+the HIP runtime, so these run on a machine without a GPU.  Fake device
+addresses are never dereferenced because validation fails first.
+"""
+import ctypes
+
+import pytest
+
+from oracle import oracle as O
+from paper_2607_07740_amd import api
+
+pytestmark = pytest.mark.filterwarnings("ignore::DeprecationWarning")
+
+P = ctypes.c_void_p
+A = P(0x1000)  # aligned fake device address
+A2 = P(0x2000)
+MIS = P(0x1002)  # misaligned
+
+
+def test_library_exports_every_declared_symbol():
+    L = api.lib()
+    names = api.declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings_and_version():
+    L = api.lib()
+    for code, name in [(0, "JL_OK"), (1, "JL_ERR_INVALID_ARG"), (2, "JL_ERR_UNSUPPORTED"),
+                       (3, "JL_ERR_WORKSPACE"), (4, "JL_ERR_HIP")]:
+        assert L.jl_status_string(code).decode() == name
+    assert L.jl_status_string(99).decode() == "JL_ERR_UNKNOWN"
+    assert L.jl_version() >= 100
+
+
+def test_host_group_size_matches_oracle():
+    for w in (1, 2, 3, 7, 512, 32768):
+        for Lx in list(range(1, 3 * w + 2, max(1, w // 7))) + [131072, 2 ** 31 - 1]:
+            assert api.group_size(Lx, w) == O.group_size(Lx, w), (Lx, w)
+    assert api.group_size(0, 5) == -1 and api.group_size(5, 0) == -1
+
+
+def _prefill(q=A, k=A, v=A, o=A, lse=None, B=1, Hq=4, Hkv=2, L=64, d=128, theta=1e6, w=16,
+             w0=4):
+    return api.lib().jl_bifocal_prefill(q, k, v, o, lse, B, Hq, Hkv, L, d, theta, w, w0, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Hq=3, Hkv=2), api.JL_ERR_INVALID_ARG),
+    (dict(B=0), api.JL_ERR_INVALID_ARG),
+    (dict(Hkv=0), api.JL_ERR_INVALID_ARG),
+    (dict(L=0), api.JL_ERR_INVALID_ARG),
+    (dict(d=64), api.JL_ERR_UNSUPPORTED),
+    (dict(d=127), api.JL_ERR_INVALID_ARG),
+    (dict(theta=0.0), api.JL_ERR_INVALID_ARG),
+    (dict(theta=float("nan")), api.JL_ERR_INVALID_ARG),
+    (dict(w=0), api.JL_ERR_INVALID_ARG),
+    (dict(w0=-1), api.JL_ERR_INVALID_ARG),
+    (dict(q=None), api.JL_ERR_INVALID_ARG),
+    (dict(k=MIS), api.JL_ERR_INVALID_ARG),
+    (dict(o=None), api.JL_ERR_INVALID_ARG),
+    (dict(lse=P(0x1001)), api.JL_ERR_INVALID_ARG),
+    (dict(Hq=6, Hkv=2), api.JL_ERR_UNSUPPORTED),  # GQA group 3 does not divide 128
+])
+def test_prefill_rejects_before_launch(kw, code):
+    assert _prefill(**kw) == code
+    assert api.lib().jl_last_error().decode() != ""
+
+
+def test_rope_attention_rejects_before_launch():
+    L = api.lib()
+    assert L.jl_rope_attention(A, A, A, A, None, 1, 4, 2, 0, 128, 1e6, None) == api.JL_ERR_INVALID_ARG
+    assert L.jl_rope_attention(A, A, A, A, None, 1, 4, 2, 8, 96, 1e6, None) == api.JL_ERR_UNSUPPORTED
+
+
+def _decode(q=A, kc=A, vc=A, lens=A2, max_len=1024, o=A, B=2, Hq=8, Hkv=2, d=128, theta=1e6,
+            w=256, w0=16, ws=A, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = api.decode_workspace_bytes(B, Hq, Hkv, max_len) if Hkv and Hq % max(Hkv, 1) == 0 else 0
+    return api.lib().jl_bifocal_decode(q, kc, vc, lens, max_len, o, B, Hq, Hkv, d, theta, w, w0,
+                                       ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(max_len=0), api.JL_ERR_INVALID_ARG),
+    (dict(Hq=7, Hkv=2), api.JL_ERR_INVALID_ARG),
+    (dict(d=256), api.JL_ERR_UNSUPPORTED),
+    (dict(Hq=32, Hkv=2), api.JL_ERR_UNSUPPORTED),  # group 16 > 8
+    (dict(w=0), api.JL_ERR_INVALID_ARG),
+    (dict(w0=-5), api.JL_ERR_INVALID_ARG),
+    (dict(lens=None), api.JL_ERR_INVALID_ARG),
+    (dict(q=MIS), api.JL_ERR_INVALID_ARG),
+    (dict(ws=None), api.JL_ERR_WORKSPACE),
+    (dict(ws_bytes=16), api.JL_ERR_WORKSPACE),
+])
+def test_decode_rejects_before_launch(kw, code):
+    assert _decode(**kw) == code
+
+
+def test_workspace_size_is_positive_and_monotone():
+    a = api.decode_workspace_bytes(1, 32, 8, 131072)
+    b = api.decode_workspace_bytes(8, 32, 8, 131072)
+    assert 0 < a <= b
+    assert api.decode_workspace_bytes(1, 32, 8, 0) == 0
+    assert api.decode_workspace_bytes(1, 32, 8, 1024, 64) == 0
+
+
+def test_debug_entry_points_reject_bad_arguments():
+    L = api.lib()
+    assert L.jl_debug_schedule(A, 4, A, 4, 0, A, A, A, None) == api.JL_ERR_INVALID_ARG
+    assert L.jl_debug_schedule(A, -1, A, 4, 8, A, A, A, None) == api.JL_ERR_INVALID_ARG
+    bq, bk, nq, nk = (ctypes.c_int(), ctypes.c_int(), ctypes.c_int(), ctypes.c_int())
+    rc = L.jl_debug_prefill_tiles(2048, 2, 1, 128, None, 0, ctypes.byref(bq), ctypes.byref(bk),
+                                  ctypes.byref(nq), ctypes.byref(nk), None)
+    assert rc == api.JL_ERR_INVALID_ARG  # no buffer, but the geometry is reported
+    assert (bq.value, bk.value) == (64, 64)
+    assert (nq.value, nk.value) == (32, 32)

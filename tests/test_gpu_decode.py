@@ -1,0 +1,92 @@
+"""Decode parity on a raw cache: the HIP kernels through the C ABI against the oracle."""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2607_07740_amd import api, synth
+from parity_util import assert_close, say, to_dev, to_f64
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _run(bifocal, q, kc, vc, lens, w, w0, theta=1e6, ws_fill=float("nan")):
+    qd, kd, vd = to_dev(q), to_dev(kc), to_dev(vc)
+    ld = torch.from_numpy(np.asarray(lens, dtype=np.int32)).cuda()
+    out = torch.full_like(qd, float("nan"))
+    B, Hq, _ = q.shape
+    Hkv, max_len = kc.shape[2], kc.shape[1]
+    nbytes = api.decode_workspace_bytes(B, Hq, Hkv, max_len)
+    ws = torch.full((nbytes // 4,), ws_fill, dtype=torch.float32, device="cuda")
+    if bifocal:
+        api.bifocal_decode(qd, kd, vd, ld, w_pretrained=w, w_local=w0, rope_theta=theta, out=out,
+                           workspace=ws)
+    else:
+        api.rope_attention_decode(qd, kd, vd, ld, rope_theta=theta, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    return out
+
+
+def test_decode_4b_128k_full():
+    w = synth.WORKLOADS["qwen3_4b_decode_128k"]
+    say("generating decode 4b 128k")
+    q, kc, vc, lens = synth.make_inputs(w)
+    for bif in (True, False):
+        say("decode bifocal=%s B=%d Hq=%d Hkv=%d kv_len=%d" % (bif, w.B, w.Hq, w.Hkv, lens[0]))
+        out = _run(bif, q, kc, vc, lens, w.w_pretrained, w.w_local)
+        want, _, _ = O.decode(q, kc, vc, lens, theta=w.theta, w_pretrained=w.w_pretrained,
+                              w_local=w.w_local, bifocal=bif)
+        assert_close(to_f64(out), want, what="decode 128k bifocal=%s" % bif)
+
+
+def test_decode_ragged_batch_with_nan_tails():
+    w = synth.WORKLOADS["qwen3_4b_decode_b8_ragged"]
+    say("generating decode ragged B=8")
+    q, kc, vc, lens = synth.make_inputs(w)
+    say("decode ragged lens", list(lens))
+    out = _run(True, q, kc, vc, lens, w.w_pretrained, w.w_local)
+    want, _, _ = O.decode(q, kc, vc, lens, theta=w.theta, w_pretrained=w.w_pretrained,
+                          w_local=w.w_local)
+    assert_close(to_f64(out), want, what="decode ragged")
+
+
+@pytest.mark.parametrize("g", [1, 2, 4, 8])
+def test_decode_small_shapes_and_g_transitions(g):
+    """One untouched raw cache decoded at lengths across G changes (Sec. 3.2)."""
+    Hkv, w_pre, w0 = 2, 96, 20
+    max_len = 4 * w_pre + 5
+    lens = [1, 2, w0, w0 + 1, w0 + 2, w_pre, w_pre + 1, 2 * w_pre, 2 * w_pre + 1, 3 * w_pre + 7,
+            max_len]
+    B = len(lens)
+    q, kc, vc, lens = synth.decode_inputs(B, g * Hkv, Hkv, max_len, lens, seed=g, nan_tail=True,
+                                          outlier_channels=8)
+    say("decode small g=%d lens=%s" % (g, list(lens)))
+    out = _run(True, q, kc, vc, lens, w_pre, w0)
+    want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    assert_close(to_f64(out), want, what="decode small g=%d" % g)
+    van = _run(False, q, kc, vc, lens, w_pre, w0)
+    want_v, _, _ = O.decode(q, kc, vc, lens, theta=1e6, bifocal=False)
+    assert_close(to_f64(van), want_v, what="vanilla decode small g=%d" % g)
+
+
+def test_decode_matches_prefill_last_row():
+    Hq, Hkv, L, w_pre, w0 = 8, 2, 777, 200, 50
+    qa, ka, va = synth.prefill_inputs(1, Hq, Hkv, L, 128, seed=77)
+    say("prefill for decode comparison L=%d" % L)
+    qd, kd, vd = to_dev(qa), to_dev(ka), to_dev(va)
+    pre = api.bifocal_prefill(qd, kd, vd, w_pretrained=w_pre, w_local=w0)
+    say("decode at the last position")
+    dec = _run(True, qa[:, L - 1].copy(), ka, va, [L], w_pre, w0)
+    a = to_f64(pre[:, L - 1])
+    b = to_f64(dec)
+    assert_close(b, a, max_abs=2e-2, mean_abs=2e-3, what="decode vs prefill last row")
+
+
+def test_decode_deterministic_and_workspace_contents_irrelevant():
+    Hq, Hkv, max_len = 16, 4, 5000
+    lens = [4999, 1234, 5000]
+    q, kc, vc, lens = synth.decode_inputs(3, Hq, Hkv, max_len, lens, seed=5)
+    say("decode determinism")
+    a = _run(True, q, kc, vc, lens, 1024, 100, ws_fill=float("nan"))
+    b = _run(True, q, kc, vc, lens, 1024, 100, ws_fill=0.0)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))

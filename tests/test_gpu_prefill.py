@@ -1,0 +1,115 @@
+"""Prefill parity: the HIP kernels through the C ABI against the fp64 oracle."""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2607_07740_amd import api, synth
+from parity_util import assert_close, rows_for, sample_positions, say, to_dev, to_f64
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _run(bifocal, q, k, v, w, w0, theta=1e6, want_lse=False):
+    qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)
+    out = torch.full_like(qd, float("nan"))  # poison: every element must be written
+    lse = None
+    if want_lse:
+        lse = torch.full((q.shape[0], q.shape[2], q.shape[1]), float("nan"), device="cuda")
+    if bifocal:
+        api.bifocal_prefill(qd, kd, vd, w_pretrained=w, w_local=w0, rope_theta=theta, out=out,
+                            lse=lse)
+    else:
+        api.rope_attention(qd, kd, vd, rope_theta=theta, out=out, lse=lse)
+    torch.cuda.synchronize()
+    return (out, lse) if want_lse else out
+
+
+def test_tiny_workload_full_tensor():
+    w = synth.WORKLOADS["tiny_prefill"]
+    q, k, v = synth.make_inputs(w)
+    say("tiny bifocal prefill", q.shape, "G=%d" % api.group_size(w.L, w.w_pretrained))
+    out, lse = _run(True, q, k, v, w.w_pretrained, w.w_local, want_lse=True)
+    want, want_lse = O.prefill(q, k, v, theta=w.theta, w_pretrained=w.w_pretrained,
+                               w_local=w.w_local)
+    assert_close(to_f64(out), want, what="tiny bifocal")
+    # LSE error budget: fp32 scores from bf16 operands, ~1e-2 in the logit at |s| ~ 10
+    assert_close(lse.cpu().numpy(), want_lse, max_abs=5e-2, mean_abs=5e-3, what="tiny lse")
+
+
+def test_tiny_workload_vanilla_full_tensor():
+    w = synth.WORKLOADS["tiny_prefill"]
+    q, k, v = synth.make_inputs(w)
+    say("tiny vanilla prefill", q.shape)
+    out = _run(False, q, k, v, 0, 0)
+    want, _ = O.prefill(q, k, v, theta=w.theta, bifocal=False)
+    assert_close(to_f64(out), want, what="tiny vanilla")
+
+
+@pytest.mark.parametrize("L,g,w_pre,w0", [
+    (1, 1, 1, 0), (2, 2, 1, 0), (63, 4, 16, 5), (65, 2, 20, 0), (127, 8, 40, 1),
+    (129, 1, 32, 64), (300, 2, 64, 63), (300, 4, 70, 100), (517, 2, 100, 128), (640, 8, 128, 65),
+    (200, 2, 300, 10),  # G == 1: must equal vanilla
+])
+def test_ragged_shapes_full_tensor(L, g, w_pre, w0):
+    B, Hkv = 2, 2
+    q, k, v = synth.prefill_inputs(B, g * Hkv, Hkv, L, 128, seed=L + g, outlier_channels=8)
+    say("ragged prefill L=%d g=%d w_pre=%d w0=%d" % (L, g, w_pre, w0))
+    out, lse = _run(True, q, k, v, w_pre, w0, want_lse=True)
+    want, want_lse = O.prefill(q, k, v, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    assert_close(to_f64(out), want, what="ragged L=%d g=%d" % (L, g))
+    assert_close(lse.cpu().numpy(), want_lse, max_abs=5e-2, mean_abs=5e-3, what="lse")
+    if api.group_size(L, w_pre) == 1:
+        van = _run(False, q, k, v, 0, 0)
+        assert torch.equal(out.view(torch.int16), van.view(torch.int16))
+
+
+def test_deterministic_and_theta_variants():
+    q, k, v = synth.prefill_inputs(1, 4, 2, 333, 128, seed=41)
+    for theta in (1e4, 5e5):
+        say("prefill theta=%g" % theta)
+        a = _run(True, q, k, v, 100, 17, theta=theta)
+        b = _run(True, q, k, v, 100, 17, theta=theta)
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+        want, _ = O.prefill(q, k, v, theta=theta, w_pretrained=100, w_local=17)
+        assert_close(to_f64(a), want, what="theta=%g" % theta)
+
+
+def _sampled_parity(name, n_random):
+    w = synth.WORKLOADS[name]
+    say("generating", name)
+    q, k, v = synth.make_inputs(w)
+    G = api.group_size(w.L, w.w_pretrained)
+    say("%s bifocal prefill B=%d Hq=%d Hkv=%d L=%d G=%d" % (name, w.B, w.Hq, w.Hkv, w.L, G))
+    out = _run(True, q, k, v, w.w_pretrained, w.w_local)
+    block_q = 128 // (w.Hq // w.Hkv)
+    pos = sample_positions(w.L, w.w_local, w.w_pretrained, G, block_q, n_random)
+    rows = rows_for(w.B, w.Hq, pos)
+    say("oracle rows", len(rows))
+    want, nthreads = O.prefill_rows(q, k, v, rows, theta=w.theta, w_pretrained=w.w_pretrained,
+                                    w_local=w.w_local)
+    o = out.float().cpu().numpy()
+    got = o[rows[:, 0], rows[:, 2], rows[:, 1]].astype(np.float64)
+    assert_close(got, want, what=name)
+    assert np.isfinite(o).all()
+    return q, k, v, out
+
+
+def test_within_window_equals_vanilla_and_oracle():
+    q, k, v, out = _sampled_parity("qwen3_1p7b_within_32k", 32)
+    w = synth.WORKLOADS["qwen3_1p7b_within_32k"]
+    say("within-window vanilla prefill")
+    van = _run(False, q, k, v, 0, 0)
+    assert torch.equal(out.view(torch.int16), van.view(torch.int16))
+
+
+def test_long_1p7b_128k_sampled_rows():
+    _sampled_parity("qwen3_1p7b_prefill_128k", 24)
+
+
+def test_long_8b_128k_sampled_rows():
+    _sampled_parity("qwen3_8b_prefill_128k", 16)
+
+
+def test_long_8b_64k_sampled_rows():
+    _sampled_parity("qwen3_8b_prefill_64k", 16)
