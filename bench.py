@@ -1,0 +1,264 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused bifocal-RoPE attention hot path on one MI355X.
+
+One step = one bifocal prefill of a Qwen3-8B-like attention layer at
+L = 131072 (B=1, Hq=32, Hkv=8, d=128, G=4, w0=4096) followed by one bifocal
+decode of a Qwen3-4B-like layer against a 131072-token raw KV cache.  Inputs
+are synthetic and seeded (paper_2607_07740_amd.synth) and resident in HBM
+before timing starts.  Prints ONE JSON line.
+
+  value       prefill TFLOP/s (algorithmic: 4 d B Hq L(L+1)/2 per call)
+  roofline    prefill kernel vs dense bf16 MFMA peak (HIP events, launch stream)
+  decode_*    decode us per call (split + reduce) and HBM GB/s vs 8 TB/s
+  overhead_*  bifocal / same-build vanilla RoPE attention - 1
+  cpu_baseline  the fp64 oracle on a bounded row sample, on the host cores
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "bifocal prefill TFLOP/s & MFMA util at 128K; decode us/token and HBM GB/s at 128K"
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBPS = 8000.0     # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "prefill_traffic_qwen3_8b_128k.txt")
+KERNEL_SOURCES = ["paper_2607_07740_amd/csrc/prefill.hip", "paper_2607_07740_amd/csrc/jl_device.h"]
+
+
+def _kernel_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def _traffic_from_profile():
+    """HBM bytes per prefill launch from the committed rocprofv3 counter summary,
+    or None when it is missing or was taken on a different kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.lstrip().startswith("#"):
+            key, val = line.split(":", 1)
+            vals[key.strip()] = val.strip()
+    if vals.get("kernel_source_sha256") != _kernel_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def _dev(bits, torch, np):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def cpu_baseline(q, k, v, w, target_s: float):
+    """Time the oracle (as it stands) on a seeded sample of prefill rows."""
+    import numpy as np
+    from oracle import oracle as O
+    rng = np.random.default_rng(1234)
+    g = w.Hq // w.Hkv
+
+    def rows_of(n):
+        pos = rng.integers(0, w.L, size=n)
+        return np.stack([np.zeros(n, np.int64), rng.integers(0, g, size=n),  # kv head 0's group
+                         pos], axis=1).astype(np.int64)
+
+    def run(rows):
+        t0 = time.perf_counter()
+        _, thr = O.prefill_rows(q, k, v, rows, theta=w.theta, w_pretrained=w.w_pretrained,
+                                w_local=w.w_local)
+        return time.perf_counter() - t0, thr
+
+    # two probes separate the per-call cost (rotating the kv head's keys) from
+    # the per-row cost, so the timed sample lands near target_s
+    t_a, _ = run(rows_of(16))
+    t_b, _ = run(rows_of(256))
+    per_row = max((t_b - t_a) / 240.0, 1e-5)
+    fixed = max(t_a - 16 * per_row, 0.0)
+    n = int(max(16, min(200000, (target_s - fixed) / per_row)))
+    rows = rows_of(n)
+    dt, threads = run(rows)
+    flops = float(np.sum(4.0 * w.d * (rows[:, 2] + 1)))
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": "%d rows (b=0, heads of kv head 0, uniform positions) of %s, %.1f s wall, "
+                      "includes rotating that kv head's keys" % (n, w.name, dt)}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--prefill", default="qwen3_8b_prefill_128k")
+    ap.add_argument("--decode", default="qwen3_4b_decode_128k")
+    ap.add_argument("--overhead-reps", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (each GPU would take "
+              "its own kv heads with no exchange); run with --gpus 1", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2607_07740_amd import api, synth
+
+    torch.cuda.set_device(0)
+    wp = synth.WORKLOADS[args.prefill]
+    wd = synth.WORKLOADS[args.decode]
+    assert wp.kind == "prefill" and wd.kind == "decode"
+
+    # ---- inputs resident in HBM
+    qh, kh, vh = synth.make_inputs(wp)
+    q, k, v = _dev(qh, torch, np), _dev(kh, torch, np), _dev(vh, torch, np)
+    out = torch.empty_like(q)
+    dq, dk, dv, lens = synth.make_inputs(wd)
+    dqd = _dev(dq, torch, np)
+    caches = [(_dev(dk, torch, np), _dev(dv, torch, np))]
+    # a second cache with the same contents, alternated so consecutive decode
+    # calls cannot be served from the 256 MB Infinity Cache
+    caches.append((caches[0][0].clone(), caches[0][1].clone()))
+    lens_d = torch.from_numpy(lens).cuda()
+    dout = torch.empty_like(dqd)
+    ws = torch.empty(api.decode_workspace_bytes(wd.B, wd.Hq, wd.Hkv, wd.L), dtype=torch.uint8,
+                     device="cuda")
+    del dk, dv
+
+    stream = torch.cuda.current_stream()
+
+    def prefill(bifocal=True):
+        if bifocal:
+            api.bifocal_prefill(q, k, v, w_pretrained=wp.w_pretrained, w_local=wp.w_local,
+                                rope_theta=wp.theta, out=out, stream=stream)
+        else:
+            api.rope_attention(q, k, v, rope_theta=wp.theta, out=out, stream=stream)
+
+    def decode(i, bifocal=True):
+        kc, vc = caches[i % 2]
+        if bifocal:
+            api.bifocal_decode(dqd, kc, vc, lens_d, w_pretrained=wd.w_pretrained,
+                               w_local=wd.w_local, rope_theta=wd.theta, out=dout, workspace=ws,
+                               stream=stream)
+        else:
+            api.rope_attention_decode(dqd, kc, vc, lens_d, rope_theta=wd.theta, out=dout,
+                                      workspace=ws, stream=stream)
+
+    for i in range(args.warmup):
+        prefill()
+        decode(i)
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        e = ev[i]
+        e[0].record(stream)
+        prefill()
+        e[1].record(stream)
+        e[2].record(stream)
+        decode(i)
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    pre_ms = [e[0].elapsed_time(e[1]) for e in ev]
+    dec_ms = [e[2].elapsed_time(e[3]) for e in ev]
+    pre_avg = sum(pre_ms) / len(pre_ms)
+    dec_avg = sum(dec_ms) / len(dec_ms)
+
+    flops = 4.0 * wp.d * wp.B * wp.Hq * wp.L * (wp.L + 1) / 2.0
+    tflops = flops / (pre_avg * 1e-3) / 1e12
+    kv_bytes = 2.0 * float(np.sum(lens)) * wd.Hkv * wd.d * 2.0
+    io_bytes = 2.0 * wd.B * wd.Hq * wd.d * 2.0
+    dec_gbps = (kv_bytes + io_bytes) / (dec_avg * 1e-3) / 1e9
+
+    # ---- overhead against the same-build vanilla kernel, interleaved
+    def timed(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b)
+
+    pb, pv, db_, dv_ = [], [], [], []
+    for r in range(args.overhead_reps):
+        pv.append(timed(lambda: prefill(False)))
+        pb.append(timed(lambda: prefill(True)))
+    for r in range(20):
+        dv_.append(timed(lambda: decode(r, False)))
+        db_.append(timed(lambda: decode(r, True)))
+    med = lambda x: sorted(x)[len(x) // 2]
+
+    traffic = _traffic_from_profile()
+    line = {
+        "metric": METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s + %s" % (wp.name, wd.name),
+            "prefill": {"B": wp.B, "Hq": wp.Hq, "Hkv": wp.Hkv, "L": wp.L, "head_dim": wp.d,
+                        "w_pretrained": wp.w_pretrained, "w_local": wp.w_local,
+                        "rope_theta": wp.theta,
+                        "G": api.group_size(wp.L, wp.w_pretrained)},
+            "decode": {"B": wd.B, "Hq": wd.Hq, "Hkv": wd.Hkv, "kv_lens": [int(x) for x in lens],
+                       "head_dim": wd.d, "w_pretrained": wd.w_pretrained,
+                       "w_local": wd.w_local, "rope_theta": wd.theta},
+        },
+        "prefill_ms": round(pre_avg, 3),
+        "prefill_mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "decode_us": round(dec_avg * 1e3, 2),
+        "decode_GBps": round(dec_gbps, 1),
+        "decode_hbm_frac": round(dec_gbps / PEAK_HBM_GBPS, 4),
+        "overhead_prefill_vs_vanilla": round(med(pb) / med(pv) - 1.0, 4),
+        "overhead_decode_vs_vanilla": round(med(db_) / med(dv_) - 1.0, 4),
+        "vanilla_prefill_ms": round(med(pv), 3),
+        "vanilla_decode_us": round(med(dv_) * 1e3, 2),
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "prefill_kernel<bifocal>",
+            "achieved": round(tflops, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+        },
+        "decode_roofline": {
+            "bound": "hbm", "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(dec_gbps / PEAK_HBM_GBPS, 4),
+        },
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(qh, kh, vh, wp, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -76,7 +76,7 @@ int64_t jl_group_size(int64_t L, int64_t w_pretrained);
  * w_pretrained >= 1, w_local >= 0; keys with q - k <= w_local use the base
  * rotation, older keys the remote one.  When G == 1 the output equals
  * jl_rope_attention bit for bit (the method reduces to the base model).
- * Requires Hq % Hkv == 0 and 128 % (Hq / Hkv) == 0.
+ * Requires Hq % Hkv == 0 and 256 % (Hq / Hkv) == 0.
  */
 int jl_bifocal_prefill(const void* q, const void* k, const void* v, void* o, float* lse, int B,
                        int Hq, int Hkv, int L, int head_dim, double rope_theta, int w_pretrained,

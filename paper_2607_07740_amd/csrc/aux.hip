@@ -37,9 +37,10 @@ __global__ void debug_schedule_kernel(const int32_t* lengths, int nl, const int3
   const int li = (int)(idx / np);
   const int pi = (int)(idx - (long long)li * np);
   const int G = group_size(lengths[li], w);
+  const FastDiv gd = make_fastdiv((uint32_t)G);
   const int x = positions[pi];
-  fout[idx] = remote_pos(x, G);
-  dout[idx] = pos_offset(x, G);
+  fout[idx] = remote_pos(x, gd);
+  dout[idx] = pos_offset(x, gd);
   if (pi == 0) gout[li] = G;
 }
 
@@ -59,8 +60,7 @@ __global__ void debug_tiles_kernel(int L, int BQ, int BK, int w0, int nqb, int n
   const int qb = (int)(idx / nkt);
   const int kt = (int)(idx - (long long)qb * nkt);
   const int q0 = qb * BQ, q1 = min(q0 + BQ, L) - 1;
-  const int k0 = kt * BK, k1 = min(k0 + BK, L) - 1;
-  out[idx] = (int8_t)tile_class(q0, q1, k0, k1, w0);
+  out[idx] = (int8_t)tile_class(visit_ranges(q0, q1, w0, BK), kt);
 }
 
 hipError_t launch_debug_tiles(int L, int BQ, int BK, int w0, int nqb, int nkt, int8_t* out,

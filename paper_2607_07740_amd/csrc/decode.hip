@@ -83,6 +83,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(DecodeArgs a)
   if (c0 >= kv_len) return;  // uniform over the workgroup
   const int c1 = min(c0 + a.chunk, kv_len);
   const int G = BIFOCAL ? group_size(kv_len, a.w_pre) : 1;
+  const FastDiv gdiv = make_fastdiv((uint32_t)G);
   const int qpos = kv_len - 1;
 
   // ---- query operand: column col = (view, head) with view = col / 8
@@ -93,7 +94,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(DecodeArgs a)
   bf16x8 qop[4];
   if (col_on) {
     const uint16_t* qrow = a.q + ((size_t)b * a.Hq + kvh * a.g + hj) * kHeadDim;
-    const int pos = view ? remote_pos(qpos, G) : qpos;
+    const int pos = view ? remote_pos(qpos, gdiv) : qpos;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       const int d = 32 * s + 8 * g4;
@@ -138,7 +139,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(DecodeArgs a)
       const bool kval = key < c1;
       const int keyc = kval ? key : c1 - 1;
       int pos = keyc;
-      if (BIFOCAL && qpos - keyc > a.w0) pos = remote_pos(keyc, G);
+      if (BIFOCAL && qpos - keyc > a.w0) pos = remote_pos(keyc, gdiv);
       const uint16_t* krow = kbase + (size_t)keyc * kv_row;
 #pragma unroll
       for (int s = 0; s < 2; ++s) {

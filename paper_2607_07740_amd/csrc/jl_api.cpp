@@ -19,6 +19,7 @@ namespace jl {
 hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                           uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
                           int L, int G, int w0, hipStream_t stream);
+int prefill_rows_per_block();
 int prefill_block_q(int g);
 int prefill_block_k();
 size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len);
@@ -138,9 +139,10 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
     return fail(JL_ERR_INVALID_ARG, "q, k, v, o must be non-null and 16-byte aligned");
   if (lse != nullptr && !aligned4(lse)) return fail(JL_ERR_INVALID_ARG, "lse must be 4-byte aligned");
   const int g = Hq / Hkv;
-  if (128 % g != 0)
-    return fail(JL_ERR_UNSUPPORTED, "GQA group Hq/Hkv = %d must divide 128", g);
-  const long long nqb = (L + (128 / g) - 1) / (128 / g);
+  const int rows = jl::prefill_rows_per_block();
+  if (rows % g != 0)
+    return fail(JL_ERR_UNSUPPORTED, "GQA group Hq/Hkv = %d must divide %d", g, rows);
+  const long long nqb = (L + (rows / g) - 1) / (rows / g);
   if (nqb * B * Hkv > 0x7fffffffLL) return fail(JL_ERR_INVALID_ARG, "problem too large");
   const int G = bifocal ? (int)jl_group_size(L, w_pre) : 1;
   const float2* table = nullptr;
@@ -270,7 +272,8 @@ int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_
                            int* n_ktiles, void* stream) {
   if (L < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || w_local < 0)
     return fail(JL_ERR_INVALID_ARG, "invalid L, Hq, Hkv or w_local");
-  if (128 % (Hq / Hkv) != 0) return fail(JL_ERR_UNSUPPORTED, "GQA group must divide 128");
+  if (jl::prefill_rows_per_block() % (Hq / Hkv) != 0)
+    return fail(JL_ERR_UNSUPPORTED, "GQA group must divide the block's rows");
   if (!block_q || !block_k || !n_qblocks || !n_ktiles)
     return fail(JL_ERR_INVALID_ARG, "null geometry pointer");
   const int BQ = jl::prefill_block_q(Hq / Hkv), BK = jl::prefill_block_k();

@@ -26,22 +26,62 @@ __host__ __device__ inline int group_size(int L, int w) {
   if (L <= w) return 1;
   return (int)(((int64_t)L + w - 1) / w);
 }
-// Eq. (3): f(x) = floor(x / G) for x >= 0 (truncating division is the floor).
-__host__ __device__ inline int remote_pos(int x, int G) { return (int)((unsigned)x / (unsigned)G); }
-// Eq. (5): Delta(x) = f(x) - x.
-__host__ __device__ inline int pos_offset(int x, int G) { return remote_pos(x, G) - x; }
+// Division by the run-time constant G without a divide instruction
+// (Granlund-Montgomery, round-up multiplier with the add-and-shift fix-up):
+// with l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1,
+//   t = mulhi(m, x),  x / d = (t + ((x - t) >> 1)) >> (l - 1)
+// exactly, for every 32-bit unsigned x and d >= 2 (d = 1 is the identity).
+struct FastDiv {
+  uint32_t m, l, d;
+};
 
-// Tile classes over a query block [q0, q1] x key tile [k0, k1] (inclusive,
-// already clipped to the sequence).  Eq. (1): a causal pair is local iff
-// q - k <= w0 and remote iff q - k > w0.  A class names the set of element
-// classes present among the tile's causal pairs.
+__host__ __device__ inline FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f;
+  f.d = d;
+  f.m = 0;
+  f.l = 0;
+  if (d <= 1) return f;
+  uint32_t l = 0;
+  while ((1u << l) < d) ++l;
+  f.m = (uint32_t)(((((uint64_t)1 << l) - d) << 32) / d + 1);
+  f.l = l;
+  return f;
+}
+
+__host__ __device__ inline uint32_t fastdiv(uint32_t x, FastDiv f) {
+  if (f.d <= 1) return x;
+  const uint32_t t = (uint32_t)(((uint64_t)f.m * x) >> 32);
+  return (t + ((x - t) >> 1)) >> (f.l - 1);
+}
+
+// Eq. (3): f(x) = floor(x / G) for x >= 0 (truncating division is the floor).
+__host__ __device__ inline int remote_pos(int x, FastDiv G) { return (int)fastdiv((uint32_t)x, G); }
+// Eq. (5): Delta(x) = f(x) - x.
+__host__ __device__ inline int pos_offset(int x, FastDiv G) { return remote_pos(x, G) - x; }
+
+// Key tiles a query block [q0, q1] visits (Eq. (1): a causal pair is local
+// iff q - k <= w0, remote iff q - k > w0).  Tiles are BK keys wide.
+//   n_kt  tiles up to the block's last query (all others hold no causal pair)
+//   n_r   tiles [0, n_r) hold at least one remote pair: k0 < q1 - w0
+//   kt_l  tiles [kt_l, n_kt) hold at least one band pair: k0 + BK - 1 >= q0 - w0
+struct VisitRanges {
+  int n_kt, n_r, kt_l;
+};
+
+__host__ __device__ inline VisitRanges visit_ranges(int q0, int q1, int w0, int BK) {
+  VisitRanges r;
+  r.n_kt = q1 / BK + 1;
+  r.n_r = q1 - w0 > 0 ? (q1 - w0 + BK - 1) / BK : 0;
+  r.kt_l = q0 - w0 > 0 ? (q0 - w0) / BK : 0;
+  return r;
+}
+
+// Tile classes: the set of element classes among a tile's causal pairs.
 enum TileClass : int { kSkip = 0, kLocal = 1, kRemote = 2, kMixed = 3 };
 
-__host__ __device__ inline int tile_class(int q0, int q1, int k0, int k1, int w0) {
-  if (k0 > q1) return kSkip;           // no causal pair
-  if (q1 - k0 <= w0) return kLocal;    // the widest pair is inside the band
-  if (q0 - k1 > w0) return kRemote;    // the narrowest pair is outside it
-  return kMixed;
+__host__ __device__ inline int tile_class(const VisitRanges& r, int kt) {
+  if (kt >= r.n_kt) return kSkip;
+  return (kt >= r.kt_l ? kLocal : 0) | (kt < r.n_r ? kRemote : 0);
 }
 
 // ------------------------------------------------------------ wave helpers
