@@ -103,7 +103,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--prefill", default="qwen3_8b_prefill_128k")
     ap.add_argument("--decode", default="qwen3_4b_decode_128k")
-    ap.add_argument("--overhead-reps", type=int, default=3)
+    ap.add_argument("--overhead-reps", type=int, default=3,
+                    help="interleaved vanilla/bifocal prefill pairs for the overhead figure")
+    ap.add_argument("--decode-reps", type=int, default=20,
+                    help="interleaved vanilla/bifocal decode pairs for the overhead figure")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -202,10 +205,10 @@ def main() -> int:
     for r in range(args.overhead_reps):
         pv.append(timed(lambda: prefill(False)))
         pb.append(timed(lambda: prefill(True)))
-    for r in range(20):
+    for r in range(args.decode_reps):
         dv_.append(timed(lambda: decode(r, False)))
         db_.append(timed(lambda: decode(r, True)))
-    med = lambda x: sorted(x)[len(x) // 2]
+    med = lambda x: sorted(x)[len(x) // 2] if x else float("nan")
 
     traffic = _traffic_from_profile()
     line = {

@@ -36,6 +36,7 @@
 //   m moves (and O, l are rescaled) only when a tile's scores exceed it by more
 //   than 2^8, which keeps every exponent <= 2^8 without a per-tile rescale.
 #include <climits>
+#include <type_traits>
 
 #include "jl_device.h"
 
@@ -44,8 +45,10 @@ namespace jl {
 constexpr int kPfThreads = 512;
 constexpr int kPfRows = 256;   // query rows per workgroup, 32 per wave
 constexpr int kPfBK = 64;      // keys per tile
-constexpr int kKStride = 136;  // bf16 per K row in LDS (272 B: conflict-free 16-byte row reads)
-constexpr int kVStride = 144;  // bf16 per V row in LDS (288 B: conflict-free transposing reads)
+constexpr int kKStride = 136;  // bf16 per K row in LDS (272 B = 68 dwords: 16 rows read at one
+                               // column hit 16 disjoint 4-bank groups)
+constexpr int kVStride = 160;  // bf16 per V row in LDS (320 B = 80 dwords: the 4 rows x 64 B of a
+                               // transposing read land on disjoint quarters of the 64 banks)
 constexpr int kKBuf = kPfBK * kKStride;
 constexpr int kVBuf = kPfBK * kVStride;
 constexpr float kRescaleLog2 = 8.f;
@@ -151,28 +154,23 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   const uint16_t* kbase = a.k + ((size_t)b * L * a.Hkv + kvh) * kHeadDim + 8 * st_c;
   const uint16_t* vbase = a.v + ((size_t)b * L * a.Hkv + kvh) * kHeadDim + 8 * st_c;
 
-  // raw K/V rows of visit j (issued before the current tile's compute)
-  auto issue_kv = [&](int j, Stage& st) {
-    const int key = (j < n_r ? j : kt_l + (j - n_r)) * kPfBK + st_key;
-    st.klo = st.khi = st.vlo = st.vhi = u32x4{0, 0, 0, 0};
-    if (key < L) {
-      const uint16_t* kr = kbase + (size_t)key * kv_row;
-      const uint16_t* vr = vbase + (size_t)key * kv_row;
-      st.klo = load16(kr);
-      st.khi = load16(kr + kHalf);
-      st.vlo = load16(vr);
-      st.vhi = load16(vr + kHalf);
-    }
-  };
-  // cos/sin row of visit j's key at the view's position (issued once the
-  // current tile's scores are consumed, so it reuses their registers)
-  auto issue_cs = [&](int j, Stage& st) {
+  // raw K/V rows and the cos/sin row of visit j at its view's position; keys
+  // past the sequence read row L-1 and are zeroed (only the last tile has any)
+  auto issue = [&](int j, Stage& st) {
     const bool remote = j < n_r;
-    const int key = min((remote ? j : kt_l + (j - n_r)) * kPfBK + st_key, L - 1);
+    const int k0 = (remote ? j : kt_l + (j - n_r)) * kPfBK;
+    const int key = min(k0 + st_key, L - 1);
+    const uint16_t* kr = kbase + (size_t)key * kv_row;
+    const uint16_t* vr = vbase + (size_t)key * kv_row;
+    st.klo = load16(kr);
+    st.khi = load16(kr + kHalf);
+    st.vlo = load16(vr);
+    st.vhi = load16(vr + kHalf);
     const int pos = remote ? remote_pos(key, a.gdiv) : key;
     const float4* c4 = (const float4*)(a.table + (size_t)pos * kHalf + 8 * st_c);
 #pragma unroll
     for (int t = 0; t < 4; ++t) st.cs[t] = c4[t];
+    if (k0 + kPfBK > L && k0 + st_key >= L) st.vlo = st.vhi = u32x4{0, 0, 0, 0};
   };
   // rotate the chunk pair and store K and V rows
   auto commit = [&](int buf, const Stage& st) {
@@ -207,8 +205,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   float l_run = 0.f;
 
   Stage st;
-  issue_kv(0, st);
-  issue_cs(0, st);
+  issue(0, st);
   commit(0, st);
   __syncthreads();
 
@@ -216,14 +213,14 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   const int i16 = lane & 15;
   const int kap_hi = g16 >> 1;
 
-  for (int j = 0; j < n_steps; ++j) {
-    const bool remote = j < n_r;
+  // one visit: scores of tile j in one view, online softmax, PV; the next
+  // visit's rows are loaded meanwhile and staged into the other buffer
+  auto step = [&](int j, auto remote_tag) {
+    constexpr bool remote = decltype(remote_tag)::value;
     const int k0 = (remote ? j : kt_l + (j - n_r)) * kPfBK;
     const int buf = j & 1;
-    if (j + 1 < n_steps) issue_kv(j + 1, st);  // in flight during this step's compute
-    if (BIFOCAL && j == n_r && n_r > 0)      // switch to the base-rotated query operand
-      load_q_operand(qrow, hl32, a.table, qp, a.q_scale, qop);
-
+    if (j + 1 < n_steps) issue(j + 1, st);  // in flight during the QK products
+    __builtin_amdgcn_sched_barrier(0);
     // ---- S^T - m for 2 blocks of 32 keys
     const float c_init = m_ref == -INFINITY ? 0.f : -m_ref;
     f32x16 sc[2];
@@ -236,6 +233,12 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
       for (int s = 0; s < 8; ++s) sc[kb] = mfma32(*(const bf16x8*)(krow + 16 * s), qop[s], sc[kb]);
     }
+
+    // stage the next visit into the other buffer now, so its registers are free
+    // before the softmax and the PV products
+    __builtin_amdgcn_sched_barrier(0);
+    if (j + 1 < n_steps) commit(buf ^ 1, st);
+    __builtin_amdgcn_sched_barrier(0);
 
     // ---- element masks where the tile is not wholly inside this view
     const bool need_mask = remote ? !(q0 - (k0 + kPfBK - 1) > w0)
@@ -252,6 +255,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       }
     }
 
+    __builtin_amdgcn_sched_barrier(0);
     // ---- online softmax with a lazily moved reference maximum
     float mt = -INFINITY;
 #pragma unroll
@@ -299,7 +303,6 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       l_run += psum;
     }
 
-    if (j + 1 < n_steps) issue_cs(j + 1, st);
 
     // ---- O^T += V^T P^T.  k-step ks covers 16 keys; the P^T operand's k index
     // kappa holds key 8 ((kappa % 8) / 4) + 4 (kappa / 8) + kappa % 4 of the
@@ -318,9 +321,12 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       }
     }
 
-    if (j + 1 < n_steps) commit(buf ^ 1, st);
     __syncthreads();
-  }
+  };
+
+  for (int j = 0; j < n_r; ++j) step(j, std::true_type{});
+  if (BIFOCAL && n_r > 0) load_q_operand(qrow, hl32, a.table, qp, a.q_scale, qop);
+  for (int j = n_r; j < n_steps; ++j) step(j, std::false_type{});
 
   // ---- normalise and write
   const float l_tot = l_run + __shfl_xor(l_run, 32);
