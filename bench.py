@@ -109,6 +109,9 @@ def main() -> int:
                     help="interleaved vanilla/bifocal decode pairs for the overhead figure")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB three times (the "
+                         "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -123,6 +126,15 @@ def main() -> int:
     from paper_2607_07740_amd import api, synth
 
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        nbytes = args.copy_calibration << 20
+        src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": nbytes, "reps": 3}), flush=True)
+        return 0
     wp = synth.WORKLOADS[args.prefill]
     wd = synth.WORKLOADS[args.decode]
     assert wp.kind == "prefill" and wd.kind == "decode"

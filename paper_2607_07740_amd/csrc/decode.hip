@@ -313,9 +313,11 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
 
 // ---------------------------------------------------------------- launcher
 void decode_geometry(int B, int Hkv, int max_len, int* chunk, int* n_split) {
-  // ~1024 workgroups over the chip; chunks are multiples of one 32-key step
+  // about one 8-wave workgroup per CU (256 CUs): enough waves to stream at
+  // full bandwidth while keeping few split states for the reduce; chunks are
+  // multiples of one 32-key step
   const long long groups = (long long)B * ((Hkv + kDecWaves - 1) / kDecWaves);
-  const long long want = (1024 + groups - 1) / groups;
+  const long long want = (256 + groups - 1) / groups;
   long long ch = ((long long)max_len + want - 1) / want;
   ch = (ch + kDecWaveKeys - 1) / kDecWaveKeys * kDecWaveKeys;
   if (ch < 128) ch = 128;
