@@ -76,16 +76,21 @@ int64_t jl_group_size(int64_t L, int64_t w_pretrained);
  * w_pretrained >= 1, w_local >= 0; keys with q - k <= w_local use the base
  * rotation, older keys the remote one.  When G == 1 the output equals
  * jl_rope_attention bit for bit (the method reduces to the base model).
- * Requires Hq % Hkv == 0 and 256 % (Hq / Hkv) == 0.
+ * Requires Hq % Hkv == 0, 128 % (Hq / Hkv) == 0 and B * Hkv <= 65535.
+ * Memory: the call rotates K once per view and transposes V into a
+ * library-owned scratch buffer of (3 * B * Hkv * ceil(L / 64) * 16 KB) bytes,
+ * one per (device, stream), grown on demand (growing waits for the stream)
+ * and freed by jl_release_caches; q, k, v are only read.
  */
 int jl_bifocal_prefill(const void* q, const void* k, const void* v, void* o, float* lse, int B,
                        int Hq, int Hkv, int L, int head_dim, double rope_theta, int w_pretrained,
                        int w_local, void* stream);
 
 /*
- * Vanilla causal RoPE attention with the same tiling and in-register RoPE of
- * raw Q/K at base positions: the base model of Sec. 3 and the denominator of
- * the overhead measurements.  Arguments as in jl_bifocal_prefill.
+ * Vanilla causal RoPE attention with the same tiling and RoPE of raw Q/K at
+ * base positions: the base model of Sec. 3 and the denominator of the
+ * overhead measurements.  Arguments and scratch as in jl_bifocal_prefill
+ * (two images per tile instead of three).
  */
 int jl_rope_attention(const void* q, const void* k, const void* v, void* o, float* lse, int B,
                       int Hq, int Hkv, int L, int head_dim, double rope_theta, void* stream);
@@ -152,8 +157,9 @@ int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_
                            int64_t classes_len, int* block_q, int* block_k, int* n_qblocks,
                            int* n_ktiles, void* stream);
 
-/* Frees the library-owned cos/sin tables on every device (they are rebuilt
- * on demand).  Must not race with running calls. */
+/* Frees the library-owned cos/sin tables and prefill scratch buffers on every
+ * device (they are rebuilt on demand); waits for the streams that own scratch.
+ * Must not race with running calls. */
 void jl_release_caches(void);
 
 #ifdef __cplusplus

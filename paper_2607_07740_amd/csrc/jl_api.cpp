@@ -16,9 +16,10 @@
 
 namespace jl {
 // kernels (prefill.hip, decode.hip, aux.hip)
+size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L);
 hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                           uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
-                          int L, int G, int w0, hipStream_t stream);
+                          int L, int G, int w0, void* ws, hipStream_t stream);
 int prefill_rows_per_block();
 int prefill_block_q(int g);
 int prefill_block_k();
@@ -112,6 +113,54 @@ int get_table(double theta, int n_pos, hipStream_t stream, const float2** out) {
   return JL_OK;
 }
 
+// ------------------------------------------- prefill scratch, per stream
+// The prefill writes each call's rotated K (one image per view) and
+// transposed V to scratch before its attention kernel reads them.  One buffer
+// per (device, stream): calls on one stream are ordered, so they can share
+// it; a call that needs more waits for its stream before replacing it.
+struct Scratch {
+  int device;
+  hipStream_t stream;
+  size_t bytes;
+  void* ptr;
+};
+std::vector<Scratch> g_scratch;
+std::mutex g_prefill_mu;  // held from scratch lookup to launch, so a concurrent
+                          // call on the same stream cannot replace a buffer in between
+
+int get_scratch(hipStream_t stream, size_t bytes, void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_mu);
+  Scratch* found = nullptr;
+  for (auto& sc : g_scratch)
+    if (sc.device == dev && sc.stream == stream) found = &sc;
+  if (found && found->bytes >= bytes) {
+    *out = found->ptr;
+    return JL_OK;
+  }
+  if (found) {
+    e = hipStreamSynchronize(stream);  // earlier calls on this stream may still read it
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    (void)hipFree(found->ptr);
+    found->ptr = nullptr;
+    found->bytes = 0;
+  }
+  const size_t want = bytes + bytes / 8;  // some room for growth
+  void* p = nullptr;
+  e = hipMalloc(&p, want);
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc(prefill scratch)");
+  if (found) {
+    found->ptr = p;
+    found->bytes = want;
+  } else {
+    g_scratch.push_back(Scratch{dev, stream, want, p});
+  }
+  *out = p;
+  return JL_OK;
+}
+
 int check_common(int B, int Hq, int Hkv, int head_dim, double theta) {
   if (B < 1 || Hq < 1 || Hkv < 1)
     return fail(JL_ERR_INVALID_ARG, "B, Hq, Hkv must be >= 1 (got %d, %d, %d)", B, Hq, Hkv);
@@ -152,9 +201,14 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   // G == 1: f is the identity and the method is the base model (Sec. 3), so
   // the bifocal entry runs the vanilla kernel and matches it bit for bit.
   const bool use_bifocal = bifocal && G > 1;
+  if ((long long)B * Hkv > 65535) return fail(JL_ERR_INVALID_ARG, "B * Hkv too large");
+  std::lock_guard<std::mutex> launch_lock(g_prefill_mu);
+  void* scratch = nullptr;
+  st = get_scratch(s, jl::prefill_workspace_bytes(use_bifocal, B, Hkv, L), &scratch);
+  if (st != JL_OK) return st;
   hipError_t e = jl::launch_prefill(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,
                                     (const uint16_t*)v, (uint16_t*)o, lse, table, B, Hq, Hkv, L,
-                                    G, w0, s);
+                                    G, w0, scratch, s);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   return ok();
 }
@@ -301,8 +355,15 @@ void jl_release_caches(void) {
   for (auto& r : g_retired) {
     if (hipSetDevice(r.first) == hipSuccess) (void)hipFree(r.second);
   }
+  for (auto& sc : g_scratch) {
+    if (hipSetDevice(sc.device) == hipSuccess) {
+      (void)hipStreamSynchronize(sc.stream);
+      (void)hipFree(sc.ptr);
+    }
+  }
   g_tables.clear();
   g_retired.clear();
+  g_scratch.clear();
   if (have_cur) (void)hipSetDevice(cur);
 }
 

@@ -54,6 +54,13 @@ __host__ __device__ inline uint32_t fastdiv(uint32_t x, FastDiv f) {
   return (t + ((x - t) >> 1)) >> (f.l - 1);
 }
 
+// The same quotient for d >= 2 only, without the d = 1 branch (straight-line
+// code for kernels that are launched with G >= 2).
+__host__ __device__ inline uint32_t fastdiv_ge2(uint32_t x, FastDiv f) {
+  const uint32_t t = (uint32_t)(((uint64_t)f.m * x) >> 32);
+  return (t + ((x - t) >> 1)) >> (f.l - 1);
+}
+
 // Eq. (3): f(x) = floor(x / G) for x >= 0 (truncating division is the floor).
 __host__ __device__ inline int remote_pos(int x, FastDiv G) { return (int)fastdiv((uint32_t)x, G); }
 // Eq. (5): Delta(x) = f(x) - x.
@@ -143,5 +150,43 @@ __device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
 }
 
 __device__ inline u32x4 load16(const void* p) { return *(const u32x4*)p; }
+
+// ------------------------------------------------- direct-to-LDS staging
+// Byte address of a __shared__ object inside the workgroup's LDS window.
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+// Asynchronous copy of 16 bytes per lane from global memory straight into LDS
+// (global_load_lds_dwordx4): lane i's 16 bytes land at lds_base + 16 i, so one
+// call moves 1 KB per wave and each lane picks its own source address.
+// lds_base must be wave-uniform.  Completion is tracked by the vector-memory
+// counter alone: call wait_vmem() before the bytes are read.  Inline assembly
+// keeps the compiler from adding a conservative wait in front of every LDS
+// read that follows the copy.
+// The compiler loads M0 itself (operand constraint); the s_nop is the wait
+// state an LDS-bound load needs after an M0 write.
+__device__ inline void dma16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gptr), "{m0}"(lds_base)
+               : "memory");
+}
+// Same copy with a wave-uniform 64-bit base in scalar registers and a 32-bit
+// per-lane byte offset; imm is added to both the global and the LDS address.
+template <int imm = 0>
+__device__ inline void dma16_s(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 offset:%2"
+               :
+               : "v"(voff), "s"(sbase), "i"(imm), "{m0}"(lds_base)
+               : "memory");
+}
+__device__ inline void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most N of this wave's vector-memory operations are in flight
+// (they complete in issue order, so everything older than the last N is done).
+template <int N>
+__device__ inline void wait_vmem_n() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"i"(N) : "memory");
+}
 
 }  // namespace jl

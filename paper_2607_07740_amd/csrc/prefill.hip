@@ -3,44 +3,51 @@
 // Jet-Long (arXiv 2607.07740): a key k <= q is scored with the base rotation
 // R(q), R(k) when q - k <= w0 and with the remote rotation R(f(q)), R(f(k)),
 // f(x) = floor(x / G), otherwise (Sec. 3, Eq. (1); Sec. 3.1, Eqs. (2)-(3)).
-// Raw (pre-RoPE) Q/K are rotated in registers; a key's remote rotation is
-// produced while its tile is staged into LDS and is never written to HBM
-// (Sec. 3.2: keys stay in base coordinates, the remote view is formed on the
-// fly).
+// Prefill is the inclusion-exclusion combination of attention passes over the
+// two views (Sec. 3.3, Eq. (7)), fused into one kernel.
+//
+// Two launches per call:
+//  1. prep_kernel rotates every raw key once per view, k_loc = R(k) x_k and
+//     k_rem = R(f(k)) x_k, and transposes V, writing each 64-key tile as the
+//     exact byte image the attention kernel wants in LDS (a call-scoped
+//     buffer; the caller's K and V are only read).  Rotating a key once per
+//     call instead of once per (query block, key tile) takes the rotation and
+//     the cos/sin table out of the quadratic loop.
+//  2. prefill_kernel streams those images with direct-to-LDS copies and runs
+//     the fused two-view attention.
 //
 // Two views, one running state.  For a block of queries the key tiles that
-// hold remote pairs are visited first with the remote-rotated query operand,
-// then the tiles that hold band pairs with the base-rotated operand; a tile
-// straddling the band edge is visited once per view, each visit keeping only
-// its own view's elements.  Every visit produces a partial softmax state over
-// disjoint keys and is folded into the running fp32 state (m, l, O) with the
-// max-shifted, linear-space merge of Sec. 3.3, Eq. (7).  Band keys never enter
-// the remote state, so the exclusion window C of Eq. (7) is empty and nothing
-// is subtracted.  The vanilla kernel is the same code with only the base view.
+// hold remote pairs are visited first with the remote-rotated query operand
+// and k_rem, then the tiles that hold band pairs with the base-rotated operand
+// and k_loc; a tile straddling the band edge is visited once per view, each
+// visit keeping only its own view's elements.  Every visit produces a partial
+// softmax state over disjoint keys and is folded into the running fp32 state
+// (m, l, O) with the max-shifted, linear-space merge of Eq. (7).  Band keys
+// never enter the remote state, so the exclusion window C of Eq. (7) is empty
+// and nothing is subtracted.  The vanilla kernel is the same code with only
+// the base view.
 //
 // Work decomposition: a workgroup is 4 wave64s, one per SIMD, and owns 256
 // query rows = (head hl = r / BQ, position q0 + r % BQ) for the g = Hq/Hkv
 // query heads sharing one kv head (GQA packing), BQ = 256 / g.  Each wave owns
-// 64 rows as two 32-column blocks, so every K and V^T operand it reads from
-// LDS feeds two MFMAs and a staged tile's rotation is spread over 256 rows.
-// Tiles of 64 keys are double-buffered in LDS; the raw rows of tile t+2 are in
-// flight to registers while tile t is computed, and tile t+1 is rotated and
-// stored during the last PV products of tile t.
+// 64 rows as two 32-column blocks (qc = 0, 1).  A lane owns one query column
+// of S^T = K Q^T (v_mfma_f32_32x32x16_bf16), and O^T += V^T P^T takes P^T
+// straight from the S^T accumulator registers.  Tiles of 64 keys rotate
+// through three LDS buffers: tile j+2 is in flight while tile j is computed.
 //
-// Per tile a wave runs four MFMA groups (v_mfma_f32_32x32x16_bf16): S^T of
-// column block 0, S^T of block 1, O^T += V^T P^T for block 0 and for block 1.
-// Their VALU partners are laid next to them so one wave's instruction stream
-// overlaps matrix and vector work: the softmax of block 0 beside S^T of block
-// 1, the softmax of block 1 beside PV of block 0, the next tile's rotation
-// beside PV of block 1.  A lane owns one query column of S^T = K Q^T, so the
-// row maximum is lane-local plus one exchange with lane ^ 32.
+// Schedule of one tile visit: S^T of block 0; S^T of block 1 beside the
+// softmax of block 0; PV of block 0 beside the softmax of block 1; PV of block
+// 1.  Within a phase the MFMAs and the vector work are independent, so one
+// wave keeps the matrix cores and the VALU busy together.
 //
-// Softmax runs in the log2 domain against a per-row reference maximum m that
-// moves only when a tile exceeds it by more than 2^64 (or at the row's first
-// key).  -m enters the MFMA itself as one extra k-step (a constant A operand
-// with a single 1 against a B operand holding -m), so scores come out already
-// shifted and the common path is exp2, sum and convert.  m is kept
-// representable in bf16 so that operand is exact.
+// Softmax runs in the log2 domain against a per-row reference m (initially 0).
+// -m enters the MFMA itself as one extra k-step (a constant A operand with a
+// single 1 against a B operand holding -m), so scores come out shifted and
+// the common path is exp2, convert and a dot product for the row sum.  The
+// reference moves only when a tile's sum leaves [2^-64, 2^64] before anything
+// was accumulated, or exceeds 2^64 later (a rare branch that recomputes the
+// tile against the new maximum and rescales the state).  m is kept
+// representable in bf16 so that its operand is exact.
 #include <climits>
 #include <type_traits>
 
@@ -48,25 +55,122 @@
 
 namespace jl {
 
-constexpr int kPfThreads = 256;  // 4 waves, one per SIMD
-constexpr int kPfRows = 256;     // query rows per workgroup: 64 per wave
+constexpr int kPfThreads = 256;  // 4 waves; two workgroups per CU, so two waves per SIMD
+constexpr int kPfRows = 128;     // query rows per workgroup: 32 per wave
 constexpr int kPfBK = 64;        // keys per tile
-constexpr int kKStride = 136;    // bf16 per K row in LDS (272 B = 68 dwords: 16 rows read at one
-                                 // column hit 16 disjoint 4-bank groups)
-constexpr int kVStride = 160;    // bf16 per V row in LDS (320 B = 80 dwords: the 4 rows x 64 B of
-                                 // a transposing read land on disjoint quarters of the 64 banks)
-constexpr int kKBuf = kPfBK * kKStride;
-constexpr int kVBuf = kPfBK * kVStride;
-constexpr float kRescaleLog2 = 64.f;
+constexpr int kTileBytes = kPfBK * kHeadDim * 2;  // one K image or one V^T image: 16 KB
+constexpr int kSmemBytes = 2 * 2 * kTileBytes;    // double-buffered K + V^T: 64 KB
+constexpr float kSumHi = 18446744073709551616.f;    // 2^64
+constexpr float kSumLo = 5.421010862427522e-20f;    // 2^-64
+
+// Tile images (byte layout, also the LDS layout):
+//   K image:   key r (0..63) at r * 256; its 16-byte chunk c (d = 8c .. 8c+7)
+//              sits in slot c ^ (r & 15).  16 lanes reading 16 keys at one d
+//              hit 16 distinct bank groups.
+//   V^T image: d (0..127) at d * 128; slot s of a row holds the 8 keys of
+//              group g = s ^ ((d >> 1) & 7), g = 2 ks + h, in the order
+//              t -> key 16 ks + 8 (t / 4) + 4 h + t % 4 (the k order of the
+//              P^T operand, i.e. of the S^T accumulator rows).  16 lanes
+//              reading 16 consecutive d at one group hit 16 distinct groups.
+__device__ inline int kimg_off(int r, int c) { return r * 256 + 16 * (c ^ (r & 15)); }
+__device__ inline int vtimg_off(int d, int g) { return d * 128 + 16 * (g ^ ((d >> 1) & 7)); }
+
+struct PrepArgs {
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* kloc;  // [B][Hkv][n_tiles] K images, base view
+  uint16_t* krem;  // same, remote view (bifocal only)
+  uint16_t* vt;    // [B][Hkv][n_tiles] V^T images
+  const float2* table;
+  int B, Hkv, L, n_tiles;
+  FastDiv gdiv;
+};
+
+// One workgroup per (tile, b * Hkv + kvh).  Keys past L are written as zeros.
+template <bool BIFOCAL>
+__global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t sv[kPfBK * kHeadDim];
+  const int tile = blockIdx.x;
+  const int bh = blockIdx.y;
+  const int b = bh / a.Hkv, kvh = bh - b * a.Hkv;
+  const int t = threadIdx.x;
+  const int k0 = tile * kPfBK;
+  const size_t row = (size_t)a.Hkv * kHeadDim;
+  const uint16_t* kseq = a.k + ((size_t)b * a.L * a.Hkv + kvh) * kHeadDim;
+  const uint16_t* vseq = a.v + ((size_t)b * a.L * a.Hkv + kvh) * kHeadDim;
+  const size_t img = ((size_t)bh * a.n_tiles + tile) * (kTileBytes / 2);
+
+  // V tile -> LDS, zeros past L
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int idx = t + 256 * i;  // 64 keys x 16 chunks
+    const int r = idx >> 4, c = idx & 15;
+    u32x4 w = u32x4{0, 0, 0, 0};
+    if (k0 + r < a.L) w = load16(vseq + (size_t)(k0 + r) * row + 8 * c);
+    *(u32x4*)(sv + r * kHeadDim + 8 * c) = w;
+  }
+
+  // K: thread -> key r = t / 4, chunk pairs (c, c + 8), c = t % 4 and t % 4 + 4
+  {
+    const int r = t >> 2;
+    const int key = k0 + r;
+    const bool valid = key < a.L;
+    unsigned char* kl = (unsigned char*)(a.kloc + img);
+    unsigned char* kr = BIFOCAL ? (unsigned char*)(a.krem + img) : nullptr;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int c = (t & 3) + 4 * u;
+      float lo[8], hi[8];
+      unpack8(valid ? load16(kseq + (size_t)key * row + 8 * c) : u32x4{0, 0, 0, 0}, lo);
+      unpack8(valid ? load16(kseq + (size_t)key * row + 8 * c + kHalf) : u32x4{0, 0, 0, 0}, hi);
+#pragma unroll
+      for (int view = 0; view < (BIFOCAL ? 2 : 1); ++view) {
+        const int pos = view == 0 ? (valid ? key : 0) : remote_pos(valid ? key : 0, a.gdiv);
+        const float4* c4 = (const float4*)(a.table + (size_t)pos * kHalf + 8 * c);
+        float ylo[8], yhi[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 w = c4[q];  // (cos_i, sin_i, cos_{i+1}, sin_{i+1})
+          const int i = 2 * q;
+          ylo[i] = lo[i] * w.x - hi[i] * w.y;
+          yhi[i] = hi[i] * w.x + lo[i] * w.y;
+          ylo[i + 1] = lo[i + 1] * w.z - hi[i + 1] * w.w;
+          yhi[i + 1] = hi[i + 1] * w.z + lo[i + 1] * w.w;
+        }
+        unsigned char* dst = view == 0 ? kl : kr;
+        *(bf16x8*)(dst + kimg_off(r, c)) = pack8(ylo);
+        *(bf16x8*)(dst + kimg_off(r, c + 8)) = pack8(yhi);
+      }
+    }
+  }
+  __syncthreads();
+
+  // V^T: 128 d x 8 key groups of 16 bytes, 4 per thread
+  unsigned char* vti = (unsigned char*)(a.vt + img);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int p = t + 256 * i;
+    const int d = p >> 3, g = p & 7;
+    const int ks = g >> 1, h = g & 1;
+    uint16_t e[8];
+#pragma unroll
+    for (int tt = 0; tt < 8; ++tt) e[tt] = sv[(16 * ks + 8 * (tt >> 2) + 4 * h + (tt & 3)) * kHeadDim + d];
+    u32x4 w;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[q] = (unsigned)e[2 * q] | ((unsigned)e[2 * q + 1] << 16);
+    *(u32x4*)(vti + vtimg_off(d, g)) = w;
+  }
+}
 
 struct PrefillArgs {
   const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
   uint16_t* o;
   float* lse;
-  const float2* table;  // [positions][64] (cos, sin) of p * omega_i
-  int B, Hq, Hkv, L;
+  const float2* table;   // [positions][64] (cos, sin) of p * omega_i
+  const uint16_t* kloc;  // tile images from prep_kernel
+  const uint16_t* krem;
+  const uint16_t* vt;
+  int B, Hq, Hkv, L, n_tiles;
   int g, BQ, n_qblocks;
   int w0;         // local window; INT_MAX for the vanilla kernel
   FastDiv gdiv;   // division by G (Eq. (3))
@@ -98,23 +202,48 @@ __device__ inline void load_q_operand(const uint16_t* qrow, int half, const floa
   }
 }
 
-// Raw rows of one tile in flight between their global load and their LDS store.
-// Thread t stages keys t / 8 and t / 8 + 32 of the tile, chunk pair c = t % 8:
-// the slices d = 8c..8c+7 and their rotate-half partners d + 64.
-struct Stage {
-  u32x4 klo[2], khi[2], vlo[2], vhi[2];
-  float4 cs[2][4];  // (cos, sin) of frequencies 8c .. 8c+7 at each key's position
-};
-
 __device__ inline float round_to_bf16(float x) { return (float)(__bf16)x; }
 
+// acc *= s for an MFMA accumulator, kept in accumulation registers: the
+// multiply goes through one VGPR per element, so the loop-carried accumulator
+// never needs a copy in the arithmetic registers.  The MFMAs that last wrote
+// acc and next read it are far away in the instruction stream; the trailing
+// s_nop covers the write-to-MFMA-read distance regardless.
+__device__ inline void scale_acc(f32x16& acc, float s) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    float x = acc[i];
+    float t;
+    asm volatile(
+        "v_accvgpr_read_b32 %1, %0\n\t"
+        "v_mul_f32 %1, %2, %1\n\t"
+        "v_accvgpr_write_b32 %0, %1"
+        : "+a"(x), "=&v"(t)
+        : "v"(s));
+    acc[i] = x;
+  }
+  asm volatile("s_nop 7");
+}
+
+// Row sum of 8 bf16 probabilities (one P^T operand) added to acc.
+__device__ inline float sum8(bf16x8 p, float acc) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2 pair = {p[2 * i], p[2 * i + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(pair, one, acc, false);
+  }
+  return acc;
+}
+
+
 template <bool BIFOCAL>
-__global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2 * kKBuf];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2 * kVBuf];
+__global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmemBytes];
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int hl32 = lane >> 5;  // which 8-wide half of a 16-wide k slice this lane feeds
 
@@ -139,20 +268,14 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   const int q0 = qblk * a.BQ;
   const int q1 = min(q0 + a.BQ, L) - 1;
 
-  // ---- this lane's two query rows (column blocks qc = 0, 1)
-  int qp[2], hd[2];
-  bool row_valid[2];
-  const uint16_t* qrow[2];
-#pragma unroll
-  for (int qc = 0; qc < 2; ++qc) {
-    const int row = 64 * wave + 32 * qc + (lane & 31);
-    const int hl = row / a.BQ;
-    const int qpos = q0 + (row - hl * a.BQ);
-    row_valid[qc] = qpos < L;
-    qp[qc] = row_valid[qc] ? qpos : L - 1;
-    hd[qc] = kvh * a.g + hl;
-    qrow[qc] = a.q + (((size_t)b * L + qp[qc]) * a.Hq + hd[qc]) * kHeadDim;
-  }
+  // ---- this lane's query row: column (lane & 31) of the wave's 32
+  const int row = 32 * wave + (lane & 31);
+  const int hl = row / a.BQ;
+  const int qpos = q0 + (row - hl * a.BQ);
+  const bool row_valid = qpos < L;
+  const int qp = row_valid ? qpos : L - 1;
+  const int hd = kvh * a.g + hl;
+  const uint16_t* qrow = a.q + (((size_t)b * L + qp) * a.Hq + hd) * kHeadDim;
 
   // ---- visit list: remote-view tiles [0, n_r), then base-view tiles from kt_l
   const VisitRanges vr = visit_ranges(q0, q1, w0, kPfBK);
@@ -161,262 +284,250 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   const int kt_l = BIFOCAL ? vr.kt_l : 0;
   const int n_steps = n_r + (n_kt - kt_l);
 
-  // ---- staging geometry
-  const int st_c = tid & 7;
-  const int st_key = tid >> 3;
-  const size_t kv_row = (size_t)a.Hkv * kHeadDim;
-  const uint16_t* kbase = a.k + ((size_t)b * L * a.Hkv + kvh) * kHeadDim + 8 * st_c;
-  const uint16_t* vbase = a.v + ((size_t)b * L * a.Hkv + kvh) * kHeadDim + 8 * st_c;
-
-  // raw K/V rows and cos/sin rows of visit j at its view's positions; keys
-  // past the sequence read row L-1 and their V is zeroed
-  auto issue = [&](int j, Stage& st) {
+  // ---- staging: each wave copies its quarter (4 KB) of visit j's K image
+  // (k_rem or k_loc) and V^T image into buffer j & 1
+  const size_t img_base = (size_t)group * a.n_tiles * (kTileBytes / 2);
+  const uint32_t smem_base = lds_addr(smem);
+  const uint32_t lane_off = 16 * lane;
+  auto issue = [&](int j) {
     const bool remote = j < n_r;
-    const int k0 = (remote ? j : kt_l + (j - n_r)) * kPfBK;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int key = min(k0 + st_key + 32 * u, L - 1);
-      const uint16_t* kr = kbase + (size_t)key * kv_row;
-      const uint16_t* vr2 = vbase + (size_t)key * kv_row;
-      st.klo[u] = load16(kr);
-      st.khi[u] = load16(kr + kHalf);
-      st.vlo[u] = load16(vr2);
-      st.vhi[u] = load16(vr2 + kHalf);
-      const int pos = remote ? remote_pos(key, a.gdiv) : key;
-      const float4* c4 = (const float4*)(a.table + (size_t)pos * kHalf + 8 * st_c);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) st.cs[u][t] = c4[t];
-      if (k0 + st_key + 32 * u >= L) st.vlo[u] = st.vhi[u] = u32x4{0, 0, 0, 0};
-    }
-  };
-  // rotate the chunk pairs and store K and V rows into buffer buf
-  auto commit = [&](int buf, const Stage& st) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      float lo[8], hi[8], ylo[8], yhi[8];
-      unpack8(st.klo[u], lo);
-      unpack8(st.khi[u], hi);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const float4 w = st.cs[u][t];
-        const int i = 2 * t;
-        ylo[i] = lo[i] * w.x - hi[i] * w.y;
-        yhi[i] = hi[i] * w.x + lo[i] * w.y;
-        ylo[i + 1] = lo[i + 1] * w.z - hi[i + 1] * w.w;
-        yhi[i + 1] = hi[i + 1] * w.z + lo[i + 1] * w.w;
-      }
-      const int kl = st_key + 32 * u;
-      uint16_t* kd = sK + buf * kKBuf + kl * kKStride + 8 * st_c;
-      uint16_t* vd = sV + buf * kVBuf + kl * kVStride + 8 * st_c;
-      *(bf16x8*)kd = pack8(ylo);
-      *(bf16x8*)(kd + kHalf) = pack8(yhi);
-      *(u32x4*)vd = st.vlo[u];
-      *(u32x4*)(vd + kHalf) = st.vhi[u];
-    }
+    const int kt = remote ? j : kt_l + (j - n_r);
+    const size_t off = img_base + (size_t)kt * (kTileBytes / 2) + wave * 2048;
+    const unsigned char* gk = (const unsigned char*)((BIFOCAL && remote ? a.krem : a.kloc) + off);
+    const unsigned char* gv = (const unsigned char*)(a.vt + off);
+    const uint32_t lk = smem_base + (j & 1) * 2 * kTileBytes + wave * 4096;
+    const uint32_t lv = lk + kTileBytes;
+    dma16_s<0>(gk, lane_off, lk);
+    dma16_s<1024>(gk, lane_off, lk);
+    dma16_s<2048>(gk, lane_off, lk);
+    dma16_s<3072>(gk, lane_off, lk);
+    dma16_s<0>(gv, lane_off, lv);
+    dma16_s<1024>(gv, lane_off, lv);
+    dma16_s<2048>(gv, lane_off, lv);
+    dma16_s<3072>(gv, lane_off, lv);
   };
 
-  // ---- query operands of the first view, state
-  bf16x8 qop[2][8];
-#pragma unroll
-  for (int qc = 0; qc < 2; ++qc)
-    load_q_operand(qrow[qc], hl32, a.table, n_r > 0 ? remote_pos(qp[qc], a.gdiv) : qp[qc],
-                   a.q_scale, qop[qc]);
+  // ---- query operand of the first view, state
+  bf16x8 qop[8];
+  load_q_operand(qrow, hl32, a.table, n_r > 0 ? remote_pos(qp, a.gdiv) : qp, a.q_scale, qop);
 
-  f32x16 acc_o[2][4];
+  f32x16 acc_o[4];
 #pragma unroll
-  for (int qc = 0; qc < 2; ++qc)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) acc_o[qc][i] = f32x16{};
-  float m_ref[2] = {-INFINITY, -INFINITY};  // reference maximum (log2 units), bf16-exact
-  float l_run[2] = {0.f, 0.f};
+  for (int i = 0; i < 4; ++i) acc_o[i] = f32x16{};
+  float m_ref = 0.f;  // reference (log2 units), bf16-exact; -m is the offset operand
+  float l_run = 0.f;
   // extra k-step operands adding -m to every score of a column: A holds a single
   // 1 (row k = 0 of the step, lanes 0..31), B holds -m in the same k row
   bf16x8 a_one = bf16x8{};
   if (hl32 == 0) a_one[0] = (__bf16)1.0f;
-  bf16x8 b_off[2] = {bf16x8{}, bf16x8{}};
+  bf16x8 b_off = bf16x8{};
 
-  const int g16 = lane >> 4;
-  const int i16 = lane & 15;
-  const int kap_hi = g16 >> 1;
+  issue(0);
 
-  Stage st;
-  issue(0, st);
-  commit(0, st);
-  if (n_steps > 1) issue(1, st);
-
-  // S^T - m for column block qc: 2 blocks of 32 keys, 8 k-steps + the offset step
-  auto qk = [&](int qc, int buf, f32x16* sc) {
-    const uint16_t* kb_lds = sK + buf * kKBuf;
+  const int kr_lane = lane & 31;
+  // S^T - m: 2 blocks of 32 keys, the offset k-step + 8 k-steps each, K
+  // operands read 4 MFMAs ahead
+  auto qk = [&](const unsigned char* kb, f32x16* sc) {
+    auto kop = [&](int m) {
+      const int r = 32 * (m >> 3) + kr_lane;
+      return *(const bf16x8*)(kb + kimg_off(r, 2 * (m & 7) + hl32));
+    };
+    bf16x8 ring[4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      sc[kb] = mfma32(a_one, b_off[qc], f32x16{});
-      const uint16_t* krow = kb_lds + (32 * kb + (lane & 31)) * kKStride + 8 * hl32;
+    for (int m = 0; m < 4; ++m) ring[m] = kop(m);
 #pragma unroll
-      for (int s = 0; s < 8; ++s) sc[kb] = mfma32(*(const bf16x8*)(krow + 16 * s), qop[qc][s], sc[kb]);
+    for (int m = 0; m < 16; ++m) {
+      const int blk = m >> 3, s = m & 7;
+      if (s == 0) sc[blk] = mfma32(a_one, b_off, f32x16{});
+      sc[blk] = mfma32(ring[m & 3], qop[s], sc[blk]);
+      if (m + 4 < 16) ring[m & 3] = kop(m + 4);
+    }
+  };
+  // O^T += V^T P^T: 4 k-steps of 16 keys x 4 d-blocks of 32, V^T operands
+  // read 4 MFMAs ahead
+  auto pv = [&](const unsigned char* vb, const bf16x8* pb) {
+    auto vop = [&](int m) {
+      const int d = 32 * (m & 3) + kr_lane;
+      return *(const bf16x8*)(vb + vtimg_off(d, 2 * (m >> 2) + hl32));
+    };
+    bf16x8 ring[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) ring[m] = vop(m);
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      acc_o[m & 3] = mfma32(ring[m & 3], pb[m >> 2], acc_o[m & 3]);
+      if (m + 4 < 16) ring[m & 3] = vop(m + 4);
     }
   };
 
   // element masks where the tile is not wholly inside the visit's view
-  auto mask = [&](int qc, int k0, bool remote, f32x16* sc) {
+  auto mask = [&](int k0, bool remote, f32x16* sc) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int blk = 0; blk < 2; ++blk) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int diff = qp[qc] - (k0 + 32 * kb + 8 * (i >> 2) + 4 * hl32 + (i & 3));
+        const int diff = qp - (k0 + 32 * blk + 8 * (i >> 2) + 4 * hl32 + (i & 3));
         const bool keep = remote ? diff > w0 : (diff >= 0 && diff <= w0);
-        sc[kb][i] = keep ? sc[kb][i] : -INFINITY;
+        sc[blk][i] = keep ? sc[blk][i] : -INFINITY;
       }
     }
   };
 
-  // exp2 of the shifted scores; moves the reference maximum when needed
-  auto softmax = [&](int qc, f32x16* sc, bf16x8* pb) {
-    float mt = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mt = fmaxf(mt, sc[kb][i]);
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
+  // fast softmax: exp2 against the current reference, P^T operands and their
+  // row sum (of the rounded probabilities the PV product uses)
+  auto softmax = [&](const f32x16* sc, bf16x8* pb) {
     float psum = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int q = 0; q < 4; ++q) {
+      float p[8];
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        float p[8];
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-          p[t] = fast_exp2(sc[kb][8 * hh + t]);
-          psum += p[t];
-        }
-        pb[2 * kb + hh] = pack8(p);
-      }
+      for (int t = 0; t < 8; ++t) p[t] = fast_exp2(sc[q >> 1][8 * (q & 1) + t]);
+      pb[q] = pack8(p);
+      psum = sum8(pb[q], psum);
     }
-    const bool upd = m_ref[qc] == -INFINITY ? mt != -INFINITY : mt > kRescaleLog2;
-    if (__ballot(upd) != 0) {  // rare: the row's first keys or a large jump
-      const float m_old = m_ref[qc] == -INFINITY ? 0.f : m_ref[qc];
-      const float m_new = upd ? round_to_bf16(m_old + mt) : m_old;
-      const float shift = m_new - m_old;
-      psum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          float p[8];
-#pragma unroll
-          for (int t = 0; t < 8; ++t) {
-            p[t] = fast_exp2(sc[kb][8 * hh + t] - shift);
-            psum += p[t];
-          }
-          pb[2 * kb + hh] = pack8(p);
-        }
-      }
-      const float alpha = fast_exp2(-shift);
-#pragma unroll
-      for (int db = 0; db < 4; ++db) acc_o[qc][db] *= alpha;
-      l_run[qc] *= alpha;
-      if (upd) {
-        m_ref[qc] = m_new;
-        if (hl32 == 0) b_off[qc][0] = (__bf16)(-m_new);
-      }
-    }
-    l_run[qc] += psum;
+    return psum;
   };
-
-  // O^T += V^T P^T for column block qc.  k-step ks covers 16 keys; the P^T
-  // operand's k index kappa holds key 8 ((kappa % 8) / 4) + 4 (kappa / 8) +
-  // kappa % 4 of the step (the S^T accumulator layout), so V^T is read with
-  // that permutation: kappa quads {0, 4, 8, 12} start at keys {0, 8, 4, 12}.
-  auto pv = [&](int qc, int buf, const bf16x8* pb) {
-    const uint16_t* v_lds = sV + buf * kVBuf;
+  // Rare path: some column's sum left range.  Per column (both lane halves),
+  // move the reference to the tile maximum where the sum overflowed, or where
+  // nothing was accumulated yet and the sum underflowed; recompute P and
+  // rescale the running state.
+  auto softmax_fix = [&](const f32x16* sc, bf16x8* pb, float& psum) {
+    const bool bad = !(psum <= kSumHi) || (l_run == 0.f && psum < kSumLo);
+    if (__ballot(bad) == 0) return;
+    float mt = -INFINITY;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int key_a = 16 * ks + 4 * kap_hi + (i16 >> 2);
+    for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const int dcol = 32 * db + 16 * (g16 & 1) + 4 * (i16 & 3);
-        const i16x4 lo = lds_read_tr4(v_lds + key_a * kVStride + dcol);
-        const i16x4 hi = lds_read_tr4(v_lds + (key_a + 8) * kVStride + dcol);
-        acc_o[qc][db] = mfma32(concat_tr(lo, hi), pb[ks], acc_o[qc][db]);
-      }
+      for (int i = 0; i < 16; ++i) mt = fmaxf(mt, sc[blk][i]);
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    const float ps = psum + __shfl_xor(psum, 32);
+    const float lc = l_run + __shfl_xor(l_run, 32);
+    const bool upd = mt != -INFINITY && (!(ps <= kSumHi) || (lc == 0.f && ps < kSumLo));
+    const float m_new = upd ? round_to_bf16(m_ref + mt) : m_ref;
+    const float shift = m_new - m_ref;
+    psum = 0.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float p[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) p[t] = fast_exp2(sc[q >> 1][8 * (q & 1) + t] - shift);
+      pb[q] = pack8(p);
+      psum = sum8(pb[q], psum);
     }
+    const float alpha = fast_exp2(-shift);
+    if (__ballot(upd && lc != 0.f) != 0) {
+#pragma unroll
+      for (int db = 0; db < 4; ++db) scale_acc(acc_o[db], alpha);
+    }
+    l_run *= alpha;
+    m_ref = m_new;
+    if (hl32 == 0) b_off[0] = (__bf16)(-m_new);
   };
 
   // one visit of tile j in one view
-  auto step = [&](int j, auto remote_tag) {
+  auto step = [&](int j, auto remote_tag, auto mask_tag) {
     constexpr bool remote = decltype(remote_tag)::value;
+    constexpr bool MASKED = decltype(mask_tag)::value;
     const int k0 = (remote ? j : kt_l + (j - n_r)) * kPfBK;
-    const int buf = j & 1;
-    const bool need_mask = remote ? !(q0 - (k0 + kPfBK - 1) > w0)
-                                  : !(q1 - k0 <= w0 && k0 + kPfBK - 1 <= q0);
-    __syncthreads();  // tile j is staged; the other buffer is free
+    const unsigned char* kb = smem + (j & 1) * 2 * kTileBytes;
+    const unsigned char* vb = kb + kTileBytes;
+    f32x16 sc[2];
+    bf16x8 pb[4];
 
-    f32x16 sc0[2], sc1[2];
-    bf16x8 pb0[4], pb1[4];
-    qk(0, buf, sc0);
-    if (need_mask) mask(0, k0, remote, sc0);
-    __builtin_amdgcn_sched_barrier(0);
-    qk(1, buf, sc1);
-    __builtin_amdgcn_sched_barrier(0);
-    softmax(0, sc0, pb0);
-    if (need_mask) mask(1, k0, remote, sc1);
-    __builtin_amdgcn_sched_barrier(0);
-    pv(0, buf, pb0);
-    __builtin_amdgcn_sched_barrier(0);
-    softmax(1, sc1, pb1);
-    __builtin_amdgcn_sched_barrier(0);
-    pv(1, buf, pb1);
-    __builtin_amdgcn_sched_barrier(0);
-    if (j + 1 < n_steps) commit(buf ^ 1, st);
-    __builtin_amdgcn_sched_barrier(0);
-    if (j + 2 < n_steps) issue(j + 2, st);
+    wait_vmem();      // this wave's copies of tile j
+    __syncthreads();  // everyone's copies of tile j; buffer (j+1) & 1 is free
+    if (j + 1 < n_steps) issue(j + 1);
+    qk(kb, sc);
+    if (MASKED) mask(k0, remote, sc);
+    float psum = softmax(sc, pb);
+    softmax_fix(sc, pb, psum);
+    l_run += psum;
+    pv(vb, pb);
   };
 
-  for (int j = 0; j < n_r; ++j) step(j, std::true_type{});
-  if (BIFOCAL && n_r > 0) {
-#pragma unroll
-    for (int qc = 0; qc < 2; ++qc) load_q_operand(qrow[qc], hl32, a.table, qp[qc], a.q_scale, qop[qc]);
-  }
-  for (int j = n_r; j < n_steps; ++j) step(j, std::false_type{});
+  auto run = [&](int j, auto remote_tag) {
+    constexpr bool remote = decltype(remote_tag)::value;
+    const int k0 = (remote ? j : kt_l + (j - n_r)) * kPfBK;
+    const bool need_mask = remote ? !(q0 - (k0 + kPfBK - 1) > w0)
+                                  : !(q1 - k0 <= w0 && k0 + kPfBK - 1 <= q0);
+    if (need_mask)
+      step(j, remote_tag, std::true_type{});
+    else
+      step(j, remote_tag, std::false_type{});
+  };
+
+  for (int j = 0; j < n_r; ++j) run(j, std::true_type{});
+  if (BIFOCAL && n_r > 0) load_q_operand(qrow, hl32, a.table, qp, a.q_scale, qop);
+  for (int j = n_r; j < n_steps; ++j) run(j, std::false_type{});
 
   // ---- normalise and write
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (row_valid) {
+    const float inv = 1.f / l_tot;
+    uint16_t* orow = a.o + (((size_t)b * L + qp) * a.Hq + hd) * kHeadDim;
 #pragma unroll
-  for (int qc = 0; qc < 2; ++qc) {
-    const float l_tot = l_run[qc] + __shfl_xor(l_run[qc], 32);
-    if (row_valid[qc]) {
-      const float inv = 1.f / l_tot;
-      uint16_t* orow = a.o + (((size_t)b * L + qp[qc]) * a.Hq + hd[qc]) * kHeadDim;
+    for (int db = 0; db < 4; ++db) {
 #pragma unroll
-      for (int db = 0; db < 4; ++db) {
+      for (int q4 = 0; q4 < 4; ++q4) {
+        f32x4 t;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          f32x4 t;
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) t[jj] = acc_o[qc][db][4 * q4 + jj] * inv;
-          *(bf16x4*)(orow + 32 * db + 8 * q4 + 4 * hl32) = __builtin_convertvector(t, bf16x4);
-        }
+        for (int jj = 0; jj < 4; ++jj) t[jj] = acc_o[db][4 * q4 + jj] * inv;
+        *(bf16x4*)(orow + 32 * db + 8 * q4 + 4 * hl32) = __builtin_convertvector(t, bf16x4);
       }
-      if (a.lse != nullptr && hl32 == 0)
-        a.lse[((size_t)b * a.Hq + hd[qc]) * L + qp[qc]] =
-            (m_ref[qc] + log2f(l_tot)) * 0.69314718055994531f;
     }
+    if (a.lse != nullptr && hl32 == 0)
+      a.lse[((size_t)b * a.Hq + hd) * L + qp] = (m_ref + log2f(l_tot)) * 0.69314718055994531f;
   }
 }
 
 // ---------------------------------------------------------------- launcher
+size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L) {
+  const size_t tiles = (size_t)(L + kPfBK - 1) / kPfBK;
+  return (size_t)(bifocal ? 3 : 2) * B * Hkv * tiles * kTileBytes;
+}
+
 hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                           uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
-                          int L, int G, int w0, hipStream_t stream) {
+                          int L, int G, int w0, void* ws, hipStream_t stream) {
+  const int n_tiles = (L + kPfBK - 1) / kPfBK;
+  const size_t img = (size_t)B * Hkv * n_tiles * (kTileBytes / 2);  // bf16 elements per image set
+  uint16_t* kloc = (uint16_t*)ws;
+  uint16_t* vt = kloc + img;
+  uint16_t* krem = bifocal ? vt + img : nullptr;
+
+  PrepArgs p;
+  p.k = k;
+  p.v = v;
+  p.kloc = kloc;
+  p.krem = krem;
+  p.vt = vt;
+  p.table = table;
+  p.B = B;
+  p.Hkv = Hkv;
+  p.L = L;
+  p.n_tiles = n_tiles;
+  p.gdiv = make_fastdiv((uint32_t)G);
+  if ((long long)B * Hkv > 65535) return hipErrorInvalidConfiguration;
+  if (bifocal)
+    hipLaunchKernelGGL(prep_kernel<true>, dim3(n_tiles, B * Hkv), dim3(256), 0, stream, p);
+  else
+    hipLaunchKernelGGL(prep_kernel<false>, dim3(n_tiles, B * Hkv), dim3(256), 0, stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
   PrefillArgs a;
   a.q = q;
-  a.k = k;
-  a.v = v;
   a.o = o;
   a.lse = lse;
   a.table = table;
+  a.kloc = kloc;
+  a.krem = krem;
+  a.vt = vt;
   a.B = B;
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.L = L;
+  a.n_tiles = n_tiles;
   a.g = Hq / Hkv;
   a.BQ = kPfRows / a.g;
   a.n_qblocks = (L + a.BQ - 1) / a.BQ;
