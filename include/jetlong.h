@@ -157,6 +157,17 @@ int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_
                            int64_t classes_len, int* block_q, int* block_k, int* n_qblocks,
                            int* n_ktiles, void* stream);
 
+/*
+ * Debug knob for tests, process-wide: the prefill kernels move a row's softmax
+ * reference (and rescale the running output) when a key tile's row sum
+ * exceeds 2^log2_bound; the default is 64, far from anything ordinary data
+ * reaches.  A small bound (e.g. 3) makes the rescale path run on almost every
+ * tile of ordinary inputs, which tests use to check it.  Values outside
+ * [1, 100] leave the setting unchanged.  Returns the previous value.  Not for
+ * use while prefill calls are in flight.
+ */
+double jl_debug_prefill_rescale_log2(double log2_bound);
+
 /* Frees the library-owned cos/sin tables and prefill scratch buffers on every
  * device (they are rebuilt on demand); waits for the streams that own scratch.
  * Must not race with running calls. */

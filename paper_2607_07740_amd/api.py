@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
         L.jl_debug_prefill_tiles.argtypes = [i32, i32, i32, i32, vp, i64,
                                              ctypes.POINTER(i32), ctypes.POINTER(i32),
                                              ctypes.POINTER(i32), ctypes.POINTER(i32), vp]
+        L.jl_debug_prefill_rescale_log2.restype = dbl
+        L.jl_debug_prefill_rescale_log2.argtypes = [dbl]
         L.jl_release_caches.restype = None
         L.jl_release_caches.argtypes = []
         _lib = L
@@ -214,3 +216,8 @@ def debug_prefill_tiles(L: int, Hq: int, Hkv: int, w_local: int, device="cuda", 
 
 def release_caches() -> None:
     lib().jl_release_caches()
+
+
+def debug_prefill_rescale_log2(log2_bound: float) -> float:
+    """jl_debug_prefill_rescale_log2: set the prefill rescale bound, return the old one."""
+    return float(lib().jl_debug_prefill_rescale_log2(float(log2_bound)))

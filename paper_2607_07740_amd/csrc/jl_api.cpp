@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -19,7 +20,7 @@ namespace jl {
 size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L);
 hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                           uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
-                          int L, int G, int w0, void* ws, hipStream_t stream);
+                          int L, int G, int w0, float sum_hi, void* ws, hipStream_t stream);
 int prefill_rows_per_block();
 int prefill_block_q(int g);
 int prefill_block_k();
@@ -40,6 +41,9 @@ namespace {
 
 constexpr int kHeadDim = 128;
 thread_local std::string t_detail;
+// log2 of the prefill row-sum bound that moves the softmax reference; the
+// debug entry lowers it so tests can drive the rescale path on ordinary data
+std::atomic<double> g_rescale_log2{64.0};
 
 int fail(int status, const char* fmt, ...) {
   char buf[512];
@@ -208,7 +212,7 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   if (st != JL_OK) return st;
   hipError_t e = jl::launch_prefill(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,
                                     (const uint16_t*)v, (uint16_t*)o, lse, table, B, Hq, Hkv, L,
-                                    G, w0, scratch, s);
+                                    G, w0, (float)std::exp2(g_rescale_log2.load()), scratch, s);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   return ok();
 }
@@ -343,6 +347,11 @@ int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_
                                         reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "debug tiles launch");
   return ok();
+}
+
+double jl_debug_prefill_rescale_log2(double log2_bound) {
+  if (!(log2_bound >= 1.0 && log2_bound <= 100.0)) return g_rescale_log2.load();
+  return g_rescale_log2.exchange(log2_bound);
 }
 
 void jl_release_caches(void) {

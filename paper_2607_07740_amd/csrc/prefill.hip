@@ -60,7 +60,6 @@ constexpr int kPfRows = 128;     // query rows per workgroup: 32 per wave
 constexpr int kPfBK = 64;        // keys per tile
 constexpr int kTileBytes = kPfBK * kHeadDim * 2;  // one K image or one V^T image: 16 KB
 constexpr int kSmemBytes = 2 * 2 * kTileBytes;    // double-buffered K + V^T: 64 KB
-constexpr float kSumHi = 18446744073709551616.f;    // 2^64
 constexpr float kSumLo = 5.421010862427522e-20f;    // 2^-64
 
 // Tile images (byte layout, also the LDS layout):
@@ -175,6 +174,7 @@ struct PrefillArgs {
   int w0;         // local window; INT_MAX for the vanilla kernel
   FastDiv gdiv;   // division by G (Eq. (3))
   float q_scale;  // log2(e) / sqrt(head_dim): scores come out in log2 units
+  float sum_hi;   // a tile's row sum above this moves the reference (2^64)
 };
 
 // Load one query row's B operand: 8 k-steps of 8 bf16 (d = 16 s + 8 half + j),
@@ -203,27 +203,6 @@ __device__ inline void load_q_operand(const uint16_t* qrow, int half, const floa
 }
 
 __device__ inline float round_to_bf16(float x) { return (float)(__bf16)x; }
-
-// acc *= s for an MFMA accumulator, kept in accumulation registers: the
-// multiply goes through one VGPR per element, so the loop-carried accumulator
-// never needs a copy in the arithmetic registers.  The MFMAs that last wrote
-// acc and next read it are far away in the instruction stream; the trailing
-// s_nop covers the write-to-MFMA-read distance regardless.
-__device__ inline void scale_acc(f32x16& acc, float s) {
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    float x = acc[i];
-    float t;
-    asm volatile(
-        "v_accvgpr_read_b32 %1, %0\n\t"
-        "v_mul_f32 %1, %2, %1\n\t"
-        "v_accvgpr_write_b32 %0, %1"
-        : "+a"(x), "=&v"(t)
-        : "v"(s));
-    acc[i] = x;
-  }
-  asm volatile("s_nop 7");
-}
 
 // Row sum of 8 bf16 probabilities (one P^T operand) added to acc.
 __device__ inline float sum8(bf16x8 p, float acc) {
@@ -392,7 +371,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // nothing was accumulated yet and the sum underflowed; recompute P and
   // rescale the running state.
   auto softmax_fix = [&](const f32x16* sc, bf16x8* pb, float& psum) {
-    const bool bad = !(psum <= kSumHi) || (l_run == 0.f && psum < kSumLo);
+    const bool bad = !(psum <= a.sum_hi) || (l_run == 0.f && psum < kSumLo);
     if (__ballot(bad) == 0) return;
     float mt = -INFINITY;
 #pragma unroll
@@ -402,7 +381,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     const float ps = psum + __shfl_xor(psum, 32);
     const float lc = l_run + __shfl_xor(l_run, 32);
-    const bool upd = mt != -INFINITY && (!(ps <= kSumHi) || (lc == 0.f && ps < kSumLo));
+    const bool upd = mt != -INFINITY && (!(ps <= a.sum_hi) || (lc == 0.f && ps < kSumLo));
     const float m_new = upd ? round_to_bf16(m_ref + mt) : m_ref;
     const float shift = m_new - m_ref;
     psum = 0.f;
@@ -414,10 +393,12 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       pb[q] = pack8(p);
       psum = sum8(pb[q], psum);
     }
-    const float alpha = fast_exp2(-shift);
+    // a downward move only happens before anything was accumulated (lc == 0),
+    // where 2^-shift may overflow and must not touch l and O
+    const float alpha = lc == 0.f ? 1.f : fast_exp2(-shift);
     if (__ballot(upd && lc != 0.f) != 0) {
 #pragma unroll
-      for (int db = 0; db < 4; ++db) scale_acc(acc_o[db], alpha);
+      for (int db = 0; db < 4; ++db) acc_o[db] *= alpha;
     }
     l_run *= alpha;
     m_ref = m_new;
@@ -488,7 +469,7 @@ size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L) {
 
 hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                           uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
-                          int L, int G, int w0, void* ws, hipStream_t stream) {
+                          int L, int G, int w0, float sum_hi, void* ws, hipStream_t stream) {
   const int n_tiles = (L + kPfBK - 1) / kPfBK;
   const size_t img = (size_t)B * Hkv * n_tiles * (kTileBytes / 2);  // bf16 elements per image set
   uint16_t* kloc = (uint16_t*)ws;
@@ -534,6 +515,7 @@ hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, co
   a.w0 = bifocal ? w0 : INT_MAX;
   a.gdiv = make_fastdiv((uint32_t)G);
   a.q_scale = 1.4426950408889634f / sqrtf((float)kHeadDim);
+  a.sum_hi = sum_hi;
   const long long nwg = (long long)a.n_qblocks * B * Hkv;
   if (nwg > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   if (bifocal)

@@ -64,6 +64,47 @@ def test_ragged_shapes_full_tensor(L, g, w_pre, w0):
         assert torch.equal(out.view(torch.int16), van.view(torch.int16))
 
 
+@pytest.mark.parametrize("bifocal", [True, False])
+@pytest.mark.parametrize("L,g,w_pre,w0", [(300, 4, 70, 20), (517, 2, 100, 128), (64, 1, 16, 5)])
+def test_rescale_path_on_every_tile(bifocal, L, g, w_pre, w0):
+    """With the rescale bound lowered to 2^3 the kernel moves a row's softmax
+    reference and rescales its running output on almost every tile of
+    ordinary data; the result must still match the oracle.  (A jump large
+    enough to cross the default 2^64 bound only occurs with scores of tens of
+    nats, where bf16 rounding of the operands alone already changes the
+    softmax weights, so the path is checked this way.)"""
+    B, Hkv = 1, 2
+    q, k, v = synth.prefill_inputs(B, g * Hkv, Hkv, L, 128, seed=L + 3 * g, outlier_channels=8)
+    old = api.debug_prefill_rescale_log2(3.0)
+    try:
+        say("rescale-every-tile prefill L=%d g=%d bifocal=%d" % (L, g, bifocal))
+        out, lse = _run(bifocal, q, k, v, w_pre, w0, want_lse=True)
+    finally:
+        api.debug_prefill_rescale_log2(old)
+    want, want_lse = O.prefill(q, k, v, theta=1e6, w_pretrained=w_pre, w_local=w0,
+                               bifocal=bifocal)
+    assert_close(to_f64(out), want, what="rescale path")
+    assert_close(lse.cpu().numpy(), want_lse, max_abs=5e-2, mean_abs=5e-3, what="rescale lse")
+
+
+def test_all_scores_far_below_zero():
+    """Every score of a row is about -300 nats: exp2 against the initial
+    reference underflows, so the reference must move down to the row maximum
+    before anything is accumulated."""
+    B, Hq, Hkv, L, w_pre, w0 = 1, 2, 1, 300, 100, 20
+    q, k, v = (synth.bf16_to_f32(x) for x in synth.prefill_inputs(B, Hq, Hkv, L, 128, seed=9))
+    q, k = q.copy(), k.copy()
+    # the lowest RoPE frequency pair (dims 63, 127) barely rotates over 300
+    # positions, so a shared component there makes every q.k strongly negative
+    q[..., 63] = -60.0
+    k[..., 63] = 60.0
+    qb, kb, vb = synth.bf16_bits(q), synth.bf16_bits(k), synth.bf16_bits(v)
+    say("far-negative scores prefill")
+    out = _run(True, qb, kb, vb, w_pre, w0)
+    want, _ = O.prefill(qb, kb, vb, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    assert_close(to_f64(out), want, what="negative scores")
+
+
 def test_deterministic_and_theta_variants():
     q, k, v = synth.prefill_inputs(1, 4, 2, 333, 128, seed=41)
     for theta in (1e4, 5e5):
