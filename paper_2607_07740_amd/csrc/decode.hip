@@ -8,8 +8,9 @@
 // L = kv_len[b] (Eq. (2)), computed on the device, so one launch serves a
 // ragged batch whose sequences have different G.
 //
-// Split-K: workgroup (b, kv head, split) streams CH keys of one kv head.  The
-// g query heads of the group are rotated twice (base and remote) and placed
+// Split-K: workgroup (b, group of up to 4 kv heads, split) streams a chunk of
+// keys, one wave per kv head.  The g query heads of a kv head are rotated twice
+// (base and remote) and placed
 // in the 16 columns of a v_mfma_f32_16x16x32_bf16 B operand: columns 0..7 hold
 // the base-rotated heads, 8..15 the remote-rotated ones.  Each key is rotated
 // once, to the view its distance selects (Eq. (1)), and scored against both
@@ -22,11 +23,17 @@
 
 namespace jl {
 
-constexpr int kDecWaves = 8;  // kv heads per workgroup, one wave each
+constexpr int kDecWaves = 4;  // kv heads per workgroup, one wave each
 constexpr int kDecThreads = 64 * kDecWaves;
-constexpr int kDecWaveKeys = 32;
-constexpr int kDecVStride = 144;     // bf16 per staged V row (transposing reads)
-constexpr int kStateFloats = 132;    // m, l, 2 pad, O[128]
+constexpr int kDecTile = 16;  // keys per step
+constexpr int kDecBufs = 4;   // LDS buffers: three steps in flight while one is used
+constexpr int kDecImgBytes = kDecTile * kDecWaves * kHeadDim * 2;  // K or V of one step: 16 KB
+constexpr int kDecBufBytes = 2 * kDecImgBytes + 1024;  // K, V and the step's two query cos/sin rows
+constexpr int kDecOffTab = kDecBufs * kDecBufBytes;
+constexpr int kDecOffDummy = kDecOffTab + kDecTile * kHalf * 8;     // + 16 offset rows (8 KB)
+constexpr int kDecSmem = kDecOffDummy + 1024;                      // + landing slot for padding copies
+constexpr int kDecCopies = 9;  // copies per wave and step (padded to a fixed count)
+constexpr int kStateFloats = 132;  // m, l, 2 pad, O[128]
 
 struct DecodeArgs {
   const uint16_t* q;
@@ -43,14 +50,13 @@ struct DecodeArgs {
 
 __device__ inline int clamp_len(int n, int max_len) { return n < 1 ? 1 : (n > max_len ? max_len : n); }
 
-// Rotate an 8-element pair of slices (d, d + 64) to the position whose table
-// row starts at cs (frequencies d..d+7), optional scale.
-__device__ inline void rotate8(const u32x4 rlo, const u32x4 rhi, const float2* cs, float scale,
+// Rotate an 8-element pair of slices (d, d + 64) by the (cos, sin) pairs c4[0..3]
+// (frequencies d..d+7), optional scale.
+__device__ inline void rotate8(const u32x4 rlo, const u32x4 rhi, const float4* c4, float scale,
                                bf16x8& olo, bf16x8& ohi) {
   float lo[8], hi[8], ylo[8], yhi[8];
   unpack8(rlo, lo);
   unpack8(rhi, hi);
-  const float4* c4 = (const float4*)cs;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     float4 w = c4[t];
@@ -64,173 +70,215 @@ __device__ inline void rotate8(const u32x4 rlo, const u32x4 rhi, const float2* c
   ohi = pack8(yhi);
 }
 
-// Raw K/V of 32 keys in flight: K in the MFMA A-operand layout (lane holds key
-// i16 + 16 hh at d = 32 s + 8 g4 .. +7), V as 16-byte row slices (key 4 r + g4,
-// d = 8 i16 .. +7).
-struct DecRaw {
-  u32x4 k[2][4];
-  u32x4 v[8];
-  float4 cs[2][2][4];  // cos/sin of each key's view position, frequencies 32 s + 8 g4 .. +7
-};
+__device__ inline f32x4 mfma16k16(bf16x4 a, bf16x4 b, f32x4 c) {
+  typedef short i16x4v __attribute__((ext_vector_type(4)));
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4v, a),
+                                                   __builtin_bit_cast(i16x4v, b), c, 0, 0, 0);
+}
 
+// Split-K workgroup (b, group of up to 4 kv heads, key chunk).  Every 16-key
+// step copies the keys' contiguous head slices (K and V, one key's heads are
+// adjacent in the cache) straight into LDS; four buffers keep three steps in
+// flight.  Wave w then serves kv head 4 * group + w.
+//
+// Rotation by tile offset: with k0 the step's first key, a key at k0 + t is
+// rotated by t only, R(t) x_k (base view) or by f(k0 + t) - f(k0) (remote
+// view), from 16 cos/sin rows kept in LDS, and the query columns are rotated
+// by q - k0 or f(q) - f(k0) instead: <R(a) x_q, R(b) x_k> = <R(a - c) x_q,
+// R(b - c) x_k> for any c (rotations compose additively, Sec. 3.2 Eq. (6)).
+// So no per-key cos/sin row is fetched from memory.
+//
+// LDS layouts (16-byte slots inside one head's 256-byte row of a key t):
+//   K: slot s holds chunk s ^ t          (16 keys read at one d: 16 bank groups)
+//   V: slot s holds chunk s ^ 2 (t & 7)  (8 keys x 32 B of a transposing read)
+//   offset table row r (512 B): slot s holds frequencies 2 (s ^ r), +1
 template <bool BIFOCAL>
 __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t sV[kDecWaves * kDecWaveKeys * kDecVStride];
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[kDecSmem];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int i16 = lane & 15;
   const int g4 = lane >> 4;
 
-  // workgroup = (b, group of up to 8 kv heads, key chunk); wave = one kv head,
-  // so the workgroup reads each key's contiguous heads together
   const int bid = blockIdx.x;
   const int split = bid % a.n_split;
-  const int t = bid / a.n_split;
-  const int hgroup = t % a.n_hgroups;
-  const int b = t / a.n_hgroups;
-  const int kvh = hgroup * kDecWaves + wave;
-  if (kvh >= a.Hkv) return;  // uniform over the wave; no block-level barrier follows
+  const int t0 = bid / a.n_split;
+  const int hgroup = t0 % a.n_hgroups;
+  const int b = t0 / a.n_hgroups;
+  const int h0 = hgroup * kDecWaves;
+  const int Hg = min(kDecWaves, a.Hkv - h0);  // heads in this group
+  const int kvh = h0 + wave;
+  const bool head_on = wave < Hg;
   const int kv_len = clamp_len(a.kv_lens[b], a.max_len);
   const int c0 = split * a.chunk;
-  if (c0 >= kv_len) return;
+  if (c0 >= kv_len) return;  // whole workgroup, before any barrier
   const int c1 = min(c0 + a.chunk, kv_len);
   const int G = BIFOCAL ? group_size(kv_len, a.w_pre) : 1;
   const FastDiv gdiv = make_fastdiv((uint32_t)G);
   const int qpos = kv_len - 1;
+  const int fq = BIFOCAL ? remote_pos(qpos, gdiv) : qpos;
+  const int n_steps = (c1 - c0 + kDecTile - 1) / kDecTile;
 
-  // ---- query operand: column col = (view, head) with view = col / 8
+  // ---- copies: a step's K image is 16 keys x Hg heads x 256 B = 4 Hg chunks
+  // of 1 KB, V likewise; chunk n < 4 Hg is K, n < 8 Hg is V.  Wave w takes
+  // chunks w + 4 i, i < 8; past 8 Hg it copies the step's first K chunk into a
+  // landing slot nobody reads, so every wave has 8 copies per step.  Lane ->
+  // LDS slot 16 * lane of its chunk; it fetches the global chunk that slot
+  // holds (keys past the chunk read the chunk's last key).
+  const uint32_t row_bytes = (uint32_t)Hg * 256;
+  const uint32_t smem_base = lds_addr(smem);
+  const unsigned char* kseq = (const unsigned char*)(a.kc + ((size_t)b * a.max_len * a.Hkv + h0) * kHeadDim);
+  const unsigned char* vseq = (const unsigned char*)(a.vc + ((size_t)b * a.max_len * a.Hkv + h0) * kHeadDim);
+  const uint32_t kv_row_bytes = (uint32_t)a.Hkv * 256;
+  auto issue = [&](int j) {
+    const int k0 = c0 + min(j, n_steps - 1) * kDecTile;
+    const uint32_t buf = smem_base + (j % kDecBufs) * kDecBufBytes;
+    {
+      // the cos/sin rows that rotate the query columns for this step: q - k0
+      // (lanes 0..31) and f(q) - f(k0) (lanes 32..63); one copy, by wave 0
+      const int fk0 = BIFOCAL ? remote_pos(k0, gdiv) : k0;
+      const int row = lane < 32 ? qpos - k0 : fq - fk0;
+      const uint32_t off = (uint32_t)row * 512 + 16 * (lane & 31);
+      dma16_s(a.table, off, wave == 0 ? buf + 2 * kDecImgBytes : smem_base + kDecOffDummy);
+    }
+#pragma unroll
+    for (int i = 0; i < kDecCopies - 1; ++i) {
+      const int n = wave + kDecWaves * i;
+      const bool is_v = n >= 4 * Hg;
+      const bool real = n < 8 * Hg;
+      const uint32_t o = (real ? (is_v ? n - 4 * Hg : n) : 0) * 1024 + 16 * lane;
+      const uint32_t t = o / row_bytes;
+      const uint32_t rem = o - t * row_bytes;
+      const uint32_t h = rem >> 8, slot = (rem & 255) >> 4;
+      const uint32_t key = (uint32_t)min(k0 + (int)t, c1 - 1);
+      const uint32_t src = key * kv_row_bytes + h * 256 + 16 * (slot ^ (is_v ? 2 * (t & 7) : t));
+      const uint32_t dst = real ? buf + (is_v ? kDecImgBytes : 0) + (o - 16 * lane)
+                                : smem_base + kDecOffDummy;
+      dma16_s(is_v && real ? vseq : kseq, src, dst);
+    }
+  };
+  // ---- offset table: cos/sin of t * omega_i for t = 0..15 (table rows 0..15)
+  {
+    unsigned char* tab = smem + kDecOffTab;
+    for (int i = threadIdx.x; i < kDecTile * 32; i += kDecThreads) {
+      const int r = i >> 5, s = i & 31;
+      *(float4*)(tab + r * 512 + 16 * (s ^ r)) = *(const float4*)(a.table + r * kHalf + 2 * s);
+    }
+  }
+  const unsigned char* tab = smem + kDecOffTab;
+
+  // ---- query columns: col = (view, head) with view = col / 8; raw slices kept
   const int col = i16;
   const int view = col >> 3;
   const int hj = col & 7;
-  const bool col_on = hj < a.g && (BIFOCAL || view == 0);
-  bf16x8 qop[4];
-  if (col_on) {
-    const uint16_t* qrow = a.q + ((size_t)b * a.Hq + kvh * a.g + hj) * kHeadDim;
-    const int pos = view ? remote_pos(qpos, gdiv) : qpos;
+  const bool col_on = head_on && hj < a.g && (BIFOCAL || view == 0);
+  u32x4 qraw[4];
+  {
+    const uint16_t* qrow =
+        a.q + ((size_t)b * a.Hq + min(kvh, a.Hkv - 1) * a.g + min(hj, a.g - 1)) * kHeadDim;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int d = 32 * s + 8 * g4;
-      rotate8(load16(qrow + d), load16(qrow + d + kHalf), a.table + (size_t)pos * kHalf + d,
-              a.q_scale, qop[s], qop[s + 2]);
-    }
-  } else {
-#pragma unroll
-    for (int s = 0; s < 4; ++s) qop[s] = bf16x8{};
+    for (int s = 0; s < 4; ++s) qraw[s] = load16(qrow + 32 * s + 8 * g4);
   }
+
+  // the plain loads above complete before the first copy is requested, so the
+  // compiler's waits for them never hold back the copies
+  wait_vmem();
+  issue(0);
+  issue(1);
+  issue(2);
 
   f32x4 acc_o[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc_o[i] = f32x4{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  uint16_t* sVw = sV + wave * kDecWaveKeys * kDecVStride;  // this wave's V staging rows
-  const size_t kv_row = (size_t)a.Hkv * kHeadDim;
-  const uint16_t* kbase = a.kc + ((size_t)b * a.max_len * a.Hkv + kvh) * kHeadDim;
-  const uint16_t* vbase = a.vc + ((size_t)b * a.max_len * a.Hkv + kvh) * kHeadDim;
+  for (int j = 0; j < n_steps; ++j) {
+    const int k0 = c0 + j * kDecTile;
+    wait_vmem_n<2 * kDecCopies>();  // this wave's copies of step j (two later steps may fly)
+    __syncthreads();  // everyone's copies (and the offset table); buffer (j+3) % 4 is free
+    issue(j + 3);
+    if (!head_on) continue;
+    const unsigned char* sb = smem + (j % kDecBufs) * kDecBufBytes;
+    const unsigned char* kb = sb + wave * 256;
+    const unsigned char* vb = kb + kDecImgBytes;
+    const int fk0 = BIFOCAL ? remote_pos(k0, gdiv) : k0;
 
-  // keys past the chunk read row c1 - 1 (inside the sequence) and are masked;
-  // each key's cos/sin row is the one of the view its distance selects (Eq. (1))
-  auto load_raw = [&](int kb0, DecRaw& r) {
+    // query operand rotated by q - k0 (base columns) or f(q) - f(k0) (remote)
+    bf16x8 qop[4];
+    {
+      const float4* c4 = (const float4*)(sb + 2 * kDecImgBytes + 512 * view);
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int keyc = min(kb0 + 16 * hh + i16, c1 - 1);
-      const uint16_t* row = kbase + (size_t)keyc * kv_row + 8 * g4;
+      for (int s = 0; s < 2; ++s) rotate8(qraw[s], qraw[s + 2], c4 + 16 * s + 4 * g4, a.q_scale, qop[s], qop[s + 2]);
+      if (!col_on) {
 #pragma unroll
-      for (int s = 0; s < 4; ++s) r.k[hh][s] = load16(row + 32 * s);
-      int pos = keyc;
-      if (BIFOCAL && qpos - keyc > a.w0) pos = remote_pos(keyc, gdiv);
+        for (int s = 0; s < 4; ++s) qop[s] = bf16x8{};
+      }
+    }
+
+    // key t = i16 of this lane, rotated once, by its view's offset
+    const int key = k0 + i16;
+    int r = i16;
+    if (BIFOCAL && qpos - key > a.w0) r = remote_pos(key, gdiv) - fk0;
+    f32x4 sc = f32x4{};
+    {
+      u32x4 kr[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) kr[s] = *(const u32x4*)(kb + i16 * row_bytes + 16 * ((4 * s + g4) ^ i16));
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
-        const float4* c4 = (const float4*)(a.table + (size_t)pos * kHalf + 32 * s + 8 * g4);
+        float4 cs[4];
 #pragma unroll
-        for (int t4 = 0; t4 < 4; ++t4) r.cs[hh][s][t4] = c4[t4];
+        for (int u = 0; u < 4; ++u) cs[u] = *(const float4*)(tab + r * 512 + 16 * ((16 * s + 4 * g4 + u) ^ r));
+        bf16x8 lo, hi;
+        rotate8(kr[s], kr[s + 2], cs, 1.f, lo, hi);
+        sc = mfma16(lo, qop[s], sc);
+        sc = mfma16(hi, qop[s + 2], sc);
       }
     }
-#pragma unroll
-    for (int rr = 0; rr < 8; ++rr)
-      r.v[rr] = load16(vbase + (size_t)min(kb0 + 4 * rr + g4, c1 - 1) * kv_row + 8 * i16);
-  };
 
-  auto process = [&](int kb0, const DecRaw& r) {
-    // V rows -> this wave's LDS slice
+    // each column keeps only the keys of its own view; lane holds keys 4 g4 + i
+    float sv[4];
 #pragma unroll
-    for (int rr = 0; rr < 8; ++rr) *(u32x4*)(sVw + (4 * rr + g4) * kDecVStride + 8 * i16) = r.v[rr];
-
-    // each key rotated once, to the position its view selects (Eq. (1))
-    bf16x8 ka[2][4];
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-      for (int s = 0; s < 2; ++s)
-        rotate8(r.k[hh][s], r.k[hh][s + 2], (const float2*)r.cs[hh][s], 1.f, ka[hh][s],
-                ka[hh][s + 2]);
-
-    // S^T (16 keys x 16 columns per block)
-    f32x4 sc[2];
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      sc[hh] = f32x4{};
-#pragma unroll
-      for (int s = 0; s < 4; ++s) sc[hh] = mfma16(ka[hh][s], qop[s], sc[hh]);
-    }
-
-    // each column keeps only the keys of its own view
-    float sv[8];
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = kb0 + 16 * hh + 4 * g4 + i;
-        bool ok = col_on && key < c1;
-        if (BIFOCAL) {
-          const bool local = qpos - key <= a.w0;
-          ok = ok && (view == 0 ? local : !local);
-        }
-        sv[4 * hh + i] = ok ? sc[hh][i] : -INFINITY;
+    for (int i = 0; i < 4; ++i) {
+      const int kk = k0 + 4 * g4 + i;
+      bool ok = col_on && kk < c1;
+      if (BIFOCAL) {
+        const bool local = qpos - kk <= a.w0;
+        ok = ok && (view == 0 ? local : !local);
       }
+      sv[i] = ok ? sc[i] : -INFINITY;
     }
 
     // online softmax per column (the 4 lanes i16, i16+16, i16+32, i16+48)
-    float mt = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) mt = fmaxf(mt, sv[j]);
+    float mt = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
     mt = fmaxf(mt, __shfl_xor(mt, 16));
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     const float m_new = fmaxf(m_run, mt);
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
     const float alpha = fast_exp2(m_run - m_use);
-    float p[8], psum = 0.f;
+    f32x4 p;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      p[j] = fast_exp2(sv[j] - m_use);
-      psum += p[j];
-    }
-    l_run = l_run * alpha + psum;
+    for (int i = 0; i < 4; ++i) p[i] = fast_exp2(sv[i] - m_use);
+    l_run = l_run * alpha + (p[0] + p[1]) + (p[2] + p[3]);
     m_run = m_new;
 #pragma unroll
     for (int db = 0; db < 8; ++db) acc_o[db] *= alpha;
-    // P^T operand: k index kappa = 8 g4 + j holds key 16 (j / 4) + 4 g4 + j % 4
-    const bf16x8 pb = pack8(p);
+    // P^T operand of the k = 16 product: k index 4 g4 + i is key 4 g4 + i
+    const bf16x4 pb = __builtin_convertvector(p, bf16x4);
 
-    // O^T += V^T P^T; V^T read transposed: quad t of this lane group starts at
-    // key 16 t + 4 g4
+    // O^T += V^T P^T; a transposing read gives lane i of group g4 the keys
+    // 4 g4 .. 4 g4 + 3 at d = 16 db + i
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
-      const int dcol = 16 * db + 4 * (i16 & 3);
-      const i16x4 v0 = lds_read_tr4(sVw + (4 * g4 + (i16 >> 2)) * kDecVStride + dcol);
-      const i16x4 v1 = lds_read_tr4(sVw + (16 + 4 * g4 + (i16 >> 2)) * kDecVStride + dcol);
-      acc_o[db] = mfma16(concat_tr(v0, v1), pb, acc_o[db]);
+      const int c = 2 * db + ((i16 & 3) >> 1);
+      const int ta = 4 * g4 + (i16 >> 2);
+      const i16x4 v = lds_read_tr4(vb + ta * row_bytes + 16 * (c ^ (2 * (ta & 7))) + 8 * (i16 & 1));
+      acc_o[db] = mfma16k16(__builtin_bit_cast(bf16x4, v), pb, acc_o[db]);
     }
-  };
-
-  // ---- stream the chunk, 32 keys per step; the other waves of the workgroup
-  // stream the neighbouring heads of the same keys
-  for (int kb0 = c0; kb0 < c1; kb0 += kDecWaveKeys) {
-    DecRaw r;
-    load_raw(kb0, r);
-    process(kb0, r);
   }
+  wait_vmem();  // copies requested past the last step
+  if (!head_on) return;
 
   // ---- one state per head: Eq. (7) over the local-window state (column hj)
   // and the remote-only state (column 8 + hj); the exclusion window is empty
@@ -313,13 +361,13 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
 
 // ---------------------------------------------------------------- launcher
 void decode_geometry(int B, int Hkv, int max_len, int* chunk, int* n_split) {
-  // about one 8-wave workgroup per CU (256 CUs): enough waves to stream at
-  // full bandwidth while keeping few split states for the reduce; chunks are
-  // multiples of one 32-key step
+  // about one workgroup per CU (256 CUs; each holds 144 KB of LDS): enough
+  // copies in flight to stream at full bandwidth while keeping few split
+  // states for the reduce; chunks are multiples of one 32-key step
   const long long groups = (long long)B * ((Hkv + kDecWaves - 1) / kDecWaves);
   const long long want = (256 + groups - 1) / groups;
   long long ch = ((long long)max_len + want - 1) / want;
-  ch = (ch + kDecWaveKeys - 1) / kDecWaveKeys * kDecWaveKeys;
+  ch = (ch + kDecTile - 1) / kDecTile * kDecTile;
   if (ch < 128) ch = 128;
   *chunk = (int)ch;
   *n_split = (int)((max_len + ch - 1) / ch);

@@ -231,6 +231,8 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
     return fail(JL_ERR_INVALID_ARG, "q, k_cache, v_cache, o must be non-null and 16-byte aligned");
   if (!aligned4(kv_lens)) return fail(JL_ERR_INVALID_ARG, "kv_lens must be non-null and aligned");
   if (Hq / Hkv > 8) return fail(JL_ERR_UNSUPPORTED, "decode GQA group %d > 8", Hq / Hkv);
+  if ((long long)max_len * Hkv * kHeadDim * 2 >= (1LL << 32))
+    return fail(JL_ERR_UNSUPPORTED, "one sequence of the cache must stay under 4 GiB");
   const size_t need = jl::decode_workspace_bytes(B, Hq, Hkv, max_len);
   if (ws == nullptr || ws_bytes < need)
     return fail(JL_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
