@@ -23,16 +23,17 @@
 
 namespace jl {
 
-constexpr int kDecWaves = 4;  // kv heads per workgroup, one wave each
+constexpr int kDecHeads = 4;  // kv heads per workgroup
+constexpr int kDecWaves = 8;  // two waves per head: one takes the even steps, one the odd
 constexpr int kDecThreads = 64 * kDecWaves;
 constexpr int kDecTile = 16;  // keys per step
-constexpr int kDecBufs = 4;   // LDS buffers: three steps in flight while one is used
-constexpr int kDecImgBytes = kDecTile * kDecWaves * kHeadDim * 2;  // K or V of one step: 16 KB
+constexpr int kDecBufs = 4;   // LDS buffers: the two steps in use and the next two in flight
+constexpr int kDecImgBytes = kDecTile * kDecHeads * kHeadDim * 2;  // K or V of one step: 16 KB
 constexpr int kDecBufBytes = 2 * kDecImgBytes + 1024;  // K, V and the step's two query cos/sin rows
 constexpr int kDecOffTab = kDecBufs * kDecBufBytes;
 constexpr int kDecOffDummy = kDecOffTab + kDecTile * kHalf * 8;     // + 16 offset rows (8 KB)
 constexpr int kDecSmem = kDecOffDummy + 1024;                      // + landing slot for padding copies
-constexpr int kDecCopies = 9;  // copies per wave and step (padded to a fixed count)
+constexpr int kDecCopies = 5;  // copies per wave and step (padded to a fixed count)
 constexpr int kStateFloats = 132;  // m, l, 2 pad, O[128]
 
 struct DecodeArgs {
@@ -78,15 +79,18 @@ __device__ inline f32x4 mfma16k16(bf16x4 a, bf16x4 b, f32x4 c) {
 
 // Split-K workgroup (b, group of up to 4 kv heads, key chunk).  Every 16-key
 // step copies the keys' contiguous head slices (K and V, one key's heads are
-// adjacent in the cache) straight into LDS; four buffers keep three steps in
-// flight.  Wave w then serves kv head 4 * group + w.
+// adjacent in the cache) straight into LDS.  Waves w and w + 4 serve kv head
+// 4 * group + w on the even and the odd steps, so two waves share each SIMD
+// and hide each other's latency; their partial states are merged at the end.
+// Four buffers hold the two steps being computed and the next two in flight.
 //
 // Rotation by tile offset: with k0 the step's first key, a key at k0 + t is
 // rotated by t only, R(t) x_k (base view) or by f(k0 + t) - f(k0) (remote
 // view), from 16 cos/sin rows kept in LDS, and the query columns are rotated
 // by q - k0 or f(q) - f(k0) instead: <R(a) x_q, R(b) x_k> = <R(a - c) x_q,
 // R(b - c) x_k> for any c (rotations compose additively, Sec. 3.2 Eq. (6)).
-// So no per-key cos/sin row is fetched from memory.
+// So no per-key cos/sin row is fetched from memory; the step's two query rows
+// arrive with its copies.
 //
 // LDS layouts (16-byte slots inside one head's 256-byte row of a key t):
 //   K: slot s holds chunk s ^ t          (16 keys read at one d: 16 bank groups)
@@ -98,6 +102,8 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int hw = wave & (kDecHeads - 1);  // head slot
+  const int par = wave / kDecHeads;       // step parity
   const int i16 = lane & 15;
   const int g4 = lane >> 4;
 
@@ -106,10 +112,10 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   const int t0 = bid / a.n_split;
   const int hgroup = t0 % a.n_hgroups;
   const int b = t0 / a.n_hgroups;
-  const int h0 = hgroup * kDecWaves;
-  const int Hg = min(kDecWaves, a.Hkv - h0);  // heads in this group
-  const int kvh = h0 + wave;
-  const bool head_on = wave < Hg;
+  const int h0 = hgroup * kDecHeads;
+  const int Hg = min(kDecHeads, a.Hkv - h0);  // heads in this group
+  const int kvh = h0 + hw;
+  const bool head_on = hw < Hg;
   const int kv_len = clamp_len(a.kv_lens[b], a.max_len);
   const int c0 = split * a.chunk;
   if (c0 >= kv_len) return;  // whole workgroup, before any barrier
@@ -119,21 +125,39 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   const int qpos = kv_len - 1;
   const int fq = BIFOCAL ? remote_pos(qpos, gdiv) : qpos;
   const int n_steps = (c1 - c0 + kDecTile - 1) / kDecTile;
+  const int n_iter = (n_steps + 1) / 2;
 
   // ---- copies: a step's K image is 16 keys x Hg heads x 256 B = 4 Hg chunks
   // of 1 KB, V likewise; chunk n < 4 Hg is K, n < 8 Hg is V.  Wave w takes
-  // chunks w + 4 i, i < 8; past 8 Hg it copies the step's first K chunk into a
-  // landing slot nobody reads, so every wave has 8 copies per step.  Lane ->
+  // chunks w + 8 i, i < 4; past 8 Hg it copies into a landing slot nobody
+  // reads, so every wave has the same number of copies per step.  Lane ->
   // LDS slot 16 * lane of its chunk; it fetches the global chunk that slot
   // holds (keys past the chunk read the chunk's last key).
   const uint32_t row_bytes = (uint32_t)Hg * 256;
   const uint32_t smem_base = lds_addr(smem);
-  const unsigned char* kseq = (const unsigned char*)(a.kc + ((size_t)b * a.max_len * a.Hkv + h0) * kHeadDim);
-  const unsigned char* vseq = (const unsigned char*)(a.vc + ((size_t)b * a.max_len * a.Hkv + h0) * kHeadDim);
+  const unsigned char* kseq =
+      (const unsigned char*)(a.kc + ((size_t)b * a.max_len * a.Hkv + h0) * kHeadDim);
+  const unsigned char* vseq =
+      (const unsigned char*)(a.vc + ((size_t)b * a.max_len * a.Hkv + h0) * kHeadDim);
   const uint32_t kv_row_bytes = (uint32_t)a.Hkv * 256;
-  auto issue = [&](int j) {
-    const int k0 = c0 + min(j, n_steps - 1) * kDecTile;
-    const uint32_t buf = smem_base + (j % kDecBufs) * kDecBufBytes;
+  // per copy i of this lane: the key row t it serves and the byte offset of its
+  // chunk inside that key's slice of the cache (the same for every step)
+  uint32_t cp_t[kDecCopies - 1], cp_off[kDecCopies - 1];
+#pragma unroll
+  for (int i = 0; i < kDecCopies - 1; ++i) {
+    const int n = wave + kDecWaves * i;
+    const bool is_v = n >= 4 * Hg;
+    const bool real = n < 8 * Hg;
+    const uint32_t o = (real ? (is_v ? n - 4 * Hg : n) : 0) * 1024 + 16 * lane;
+    const uint32_t t = o / row_bytes;
+    const uint32_t rem = o - t * row_bytes;
+    const uint32_t h = rem >> 8, slot = (rem & 255) >> 4;
+    cp_t[i] = t;
+    cp_off[i] = h * 256 + 16 * (slot ^ (is_v ? 2 * (t & 7) : t));
+  }
+  auto issue = [&](int jb) {
+    const int k0 = c0 + min(jb, n_steps - 1) * kDecTile;
+    const uint32_t buf = smem_base + (jb % kDecBufs) * kDecBufBytes;
     {
       // the cos/sin rows that rotate the query columns for this step: q - k0
       // (lanes 0..31) and f(q) - f(k0) (lanes 32..63); one copy, by wave 0
@@ -144,20 +168,16 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     }
 #pragma unroll
     for (int i = 0; i < kDecCopies - 1; ++i) {
-      const int n = wave + kDecWaves * i;
+      const int n = wave + kDecWaves * i;  // wave-uniform
       const bool is_v = n >= 4 * Hg;
       const bool real = n < 8 * Hg;
-      const uint32_t o = (real ? (is_v ? n - 4 * Hg : n) : 0) * 1024 + 16 * lane;
-      const uint32_t t = o / row_bytes;
-      const uint32_t rem = o - t * row_bytes;
-      const uint32_t h = rem >> 8, slot = (rem & 255) >> 4;
-      const uint32_t key = (uint32_t)min(k0 + (int)t, c1 - 1);
-      const uint32_t src = key * kv_row_bytes + h * 256 + 16 * (slot ^ (is_v ? 2 * (t & 7) : t));
-      const uint32_t dst = real ? buf + (is_v ? kDecImgBytes : 0) + (o - 16 * lane)
+      const uint32_t key = (uint32_t)min(k0 + (int)cp_t[i], c1 - 1);
+      const uint32_t dst = real ? buf + (is_v ? kDecImgBytes + (n - 4 * Hg) * 1024 : n * 1024)
                                 : smem_base + kDecOffDummy;
-      dma16_s(is_v && real ? vseq : kseq, src, dst);
+      dma16_s(is_v && real ? vseq : kseq, key * kv_row_bytes + cp_off[i], dst);
     }
   };
+
   // ---- offset table: cos/sin of t * omega_i for t = 0..15 (table rows 0..15)
   {
     unsigned char* tab = smem + kDecOffTab;
@@ -184,101 +204,134 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   // the plain loads above complete before the first copy is requested, so the
   // compiler's waits for them never hold back the copies
   wait_vmem();
-  issue(0);
-  issue(1);
-  issue(2);
+  for (int jb = 0; jb < 4; ++jb) issue(jb);
 
   f32x4 acc_o[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc_o[i] = f32x4{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  for (int j = 0; j < n_steps; ++j) {
-    const int k0 = c0 + j * kDecTile;
-    wait_vmem_n<2 * kDecCopies>();  // this wave's copies of step j (two later steps may fly)
-    __syncthreads();  // everyone's copies (and the offset table); buffer (j+3) % 4 is free
-    issue(j + 3);
-    if (!head_on) continue;
-    const unsigned char* sb = smem + (j % kDecBufs) * kDecBufBytes;
-    const unsigned char* kb = sb + wave * 256;
-    const unsigned char* vb = kb + kDecImgBytes;
-    const int fk0 = BIFOCAL ? remote_pos(k0, gdiv) : k0;
+  for (int it = 0; it < n_iter; ++it) {
+    wait_vmem_n<2 * kDecCopies>();  // this wave's copies of steps 2it, 2it+1 (the next pair may fly)
+    __syncthreads();  // everyone's copies (and the offset table)
+    const int j = 2 * it + par;
+    if (head_on && j < n_steps) {
+      const int k0 = c0 + j * kDecTile;
+      const unsigned char* sb = smem + (j % kDecBufs) * kDecBufBytes;
+      const unsigned char* kb = sb + hw * 256;
+      const unsigned char* vb = kb + kDecImgBytes;
+      const int fk0 = BIFOCAL ? remote_pos(k0, gdiv) : k0;
 
-    // query operand rotated by q - k0 (base columns) or f(q) - f(k0) (remote)
-    bf16x8 qop[4];
-    {
-      const float4* c4 = (const float4*)(sb + 2 * kDecImgBytes + 512 * view);
+      // query operand rotated by q - k0 (base columns) or f(q) - f(k0) (remote)
+      bf16x8 qop[4];
+      {
+        const float4* c4 = (const float4*)(sb + 2 * kDecImgBytes + 512 * view);
 #pragma unroll
-      for (int s = 0; s < 2; ++s) rotate8(qraw[s], qraw[s + 2], c4 + 16 * s + 4 * g4, a.q_scale, qop[s], qop[s + 2]);
-      if (!col_on) {
+        for (int s = 0; s < 2; ++s)
+          rotate8(qraw[s], qraw[s + 2], c4 + 16 * s + 4 * g4, a.q_scale, qop[s], qop[s + 2]);
+        if (!col_on) {
 #pragma unroll
-        for (int s = 0; s < 4; ++s) qop[s] = bf16x8{};
+          for (int s = 0; s < 4; ++s) qop[s] = bf16x8{};
+        }
+      }
+
+      // key t = i16 of this lane, rotated once, by its view's offset
+      const int key = k0 + i16;
+      int r = i16;
+      if (BIFOCAL && qpos - key > a.w0) r = remote_pos(key, gdiv) - fk0;
+      f32x4 sc = f32x4{};
+      {
+        u32x4 kr[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          kr[s] = *(const u32x4*)(kb + i16 * row_bytes + 16 * ((4 * s + g4) ^ i16));
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          float4 cs[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            cs[u] = *(const float4*)(tab + r * 512 + 16 * ((16 * s + 4 * g4 + u) ^ r));
+          bf16x8 lo, hi;
+          rotate8(kr[s], kr[s + 2], cs, 1.f, lo, hi);
+          sc = mfma16(lo, qop[s], sc);
+          sc = mfma16(hi, qop[s + 2], sc);
+        }
+      }
+
+      // each column keeps only the keys of its own view; lane holds keys 4 g4 + i
+      float sv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int kk = k0 + 4 * g4 + i;
+        bool ok = col_on && kk < c1;
+        if (BIFOCAL) {
+          const bool local = qpos - kk <= a.w0;
+          ok = ok && (view == 0 ? local : !local);
+        }
+        sv[i] = ok ? sc[i] : -INFINITY;
+      }
+
+      // online softmax per column (the 4 lanes i16, i16+16, i16+32, i16+48)
+      float mt = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float m_new = fmaxf(m_run, mt);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = fast_exp2(m_run - m_use);
+      f32x4 p;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p[i] = fast_exp2(sv[i] - m_use);
+      l_run = l_run * alpha + (p[0] + p[1]) + (p[2] + p[3]);
+      m_run = m_new;
+      if (__ballot(alpha != 1.f) != 0) {  // most steps leave every column's maximum alone
+#pragma unroll
+        for (int db = 0; db < 8; ++db) acc_o[db] *= alpha;
+      }
+      // P^T operand of the k = 16 product: k index 4 g4 + i is key 4 g4 + i
+      const bf16x4 pb = __builtin_convertvector(p, bf16x4);
+
+      // O^T += V^T P^T; a transposing read gives lane i of group g4 the keys
+      // 4 g4 .. 4 g4 + 3 at d = 16 db + i
+#pragma unroll
+      for (int db = 0; db < 8; ++db) {
+        const int c = 2 * db + ((i16 & 3) >> 1);
+        const int ta = 4 * g4 + (i16 >> 2);
+        const i16x4 v =
+            lds_read_tr4(vb + ta * row_bytes + 16 * (c ^ (2 * (ta & 7))) + 8 * (i16 & 1));
+        acc_o[db] = mfma16k16(__builtin_bit_cast(bf16x4, v), pb, acc_o[db]);
       }
     }
-
-    // key t = i16 of this lane, rotated once, by its view's offset
-    const int key = k0 + i16;
-    int r = i16;
-    if (BIFOCAL && qpos - key > a.w0) r = remote_pos(key, gdiv) - fk0;
-    f32x4 sc = f32x4{};
-    {
-      u32x4 kr[4];
-#pragma unroll
-      for (int s = 0; s < 4; ++s) kr[s] = *(const u32x4*)(kb + i16 * row_bytes + 16 * ((4 * s + g4) ^ i16));
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        float4 cs[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) cs[u] = *(const float4*)(tab + r * 512 + 16 * ((16 * s + 4 * g4 + u) ^ r));
-        bf16x8 lo, hi;
-        rotate8(kr[s], kr[s + 2], cs, 1.f, lo, hi);
-        sc = mfma16(lo, qop[s], sc);
-        sc = mfma16(hi, qop[s + 2], sc);
-      }
-    }
-
-    // each column keeps only the keys of its own view; lane holds keys 4 g4 + i
-    float sv[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int kk = k0 + 4 * g4 + i;
-      bool ok = col_on && kk < c1;
-      if (BIFOCAL) {
-        const bool local = qpos - kk <= a.w0;
-        ok = ok && (view == 0 ? local : !local);
-      }
-      sv[i] = ok ? sc[i] : -INFINITY;
-    }
-
-    // online softmax per column (the 4 lanes i16, i16+16, i16+32, i16+48)
-    float mt = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    f32x4 p;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) p[i] = fast_exp2(sv[i] - m_use);
-    l_run = l_run * alpha + (p[0] + p[1]) + (p[2] + p[3]);
-    m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < 8; ++db) acc_o[db] *= alpha;
-    // P^T operand of the k = 16 product: k index 4 g4 + i is key 4 g4 + i
-    const bf16x4 pb = __builtin_convertvector(p, bf16x4);
-
-    // O^T += V^T P^T; a transposing read gives lane i of group g4 the keys
-    // 4 g4 .. 4 g4 + 3 at d = 16 db + i
-#pragma unroll
-    for (int db = 0; db < 8; ++db) {
-      const int c = 2 * db + ((i16 & 3) >> 1);
-      const int ta = 4 * g4 + (i16 >> 2);
-      const i16x4 v = lds_read_tr4(vb + ta * row_bytes + 16 * (c ^ (2 * (ta & 7))) + 8 * (i16 & 1));
-      acc_o[db] = mfma16k16(__builtin_bit_cast(bf16x4, v), pb, acc_o[db]);
-    }
+    __syncthreads();  // steps 2it, 2it+1 consumed: their buffers take steps 2it+4, 2it+5
+    issue(2 * it + 4);
+    issue(2 * it + 5);
   }
   wait_vmem();  // copies requested past the last step
-  if (!head_on) return;
+  __syncthreads();  // every buffer is free again
+
+  // ---- merge the odd-step wave's state into the even-step wave's (max-shifted)
+  {
+    float* xs = (float*)smem + ((size_t)hw * 64 + lane) * 34;
+    if (par == 1) {
+      xs[0] = m_run;
+      xs[1] = l_run;
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) xs[2 + 4 * db + i] = acc_o[db][i];
+    }
+    __syncthreads();
+    if (par == 1 || !head_on) return;
+    const float m_b = xs[0];
+    const float M = fmaxf(m_run, m_b);
+    const float wa = M == -INFINITY ? 0.f : fast_exp2(m_run - M);
+    const float wb = M == -INFINITY ? 0.f : fast_exp2(m_b - M);
+    l_run = wa * l_run + wb * xs[1];
+#pragma unroll
+    for (int db = 0; db < 8; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc_o[db][i] = wa * acc_o[db][i] + wb * xs[2 + 4 * db + i];
+    m_run = M;
+  }
 
   // ---- one state per head: Eq. (7) over the local-window state (column hj)
   // and the remote-only state (column 8 + hj); the exclusion window is empty
@@ -311,38 +364,56 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
 }
 
 // Final merge over the splits of one head (Eq. (7) weights exp2(m - M)):
-// O = sum W O~ / sum W l.  Thread t accumulates output slice t % 32 (4
-// channels) over splits t / 32, t / 32 + 8, ...; partial sums meet in LDS.
-__global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16_t* o) {
-  __shared__ float sMax[4];
-  __shared__ __attribute__((aligned(16))) float sAcc[8][kHeadDim];
-  __shared__ float sDen[8];
+// O = sum W O~ / sum W l.  16 groups of 32 threads; group grp takes splits
+// grp, grp + 16, ... (at most kRedPerGroup each, loads issued together),
+// thread c of a group owns output channels 4c .. 4c+3; partial sums meet in
+// LDS.
+constexpr int kRedGroups = 16;
+constexpr int kRedPerGroup = 8;  // splits per group: n_split <= 128
+__global__ __launch_bounds__(512) void decode_reduce_kernel(DecodeArgs a, uint16_t* o) {
+  __shared__ float sMax[kRedGroups];
+  __shared__ __attribute__((aligned(16))) float sAcc[kRedGroups][kHeadDim];
+  __shared__ float sDen[kRedGroups];
   const int bh = blockIdx.x;
   const int b = bh / a.Hq;
   const int tid = threadIdx.x;
   const int kv_len = clamp_len(a.kv_lens[b], a.max_len);
   const int ns = (kv_len + a.chunk - 1) / a.chunk;
   const float* base = a.ws + (size_t)bh * a.n_split * kStateFloats;
-
-  float M = -INFINITY;
-  for (int s = tid; s < ns; s += 256) M = fmaxf(M, base[(size_t)s * kStateFloats]);
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
-  if ((tid & 63) == 0) sMax[tid >> 6] = M;
-  __syncthreads();
-  M = fmaxf(fmaxf(sMax[0], sMax[1]), fmaxf(sMax[2], sMax[3]));
-
   const int c = tid & 31;
   const int grp = tid >> 5;
+
+  float m[kRedPerGroup], l[kRedPerGroup];
+  f32x4 ov[kRedPerGroup];
+#pragma unroll
+  for (int i = 0; i < kRedPerGroup; ++i) {
+    const int s = grp + kRedGroups * i;
+    if (s < ns) {
+      const float* stt = base + (size_t)s * kStateFloats;
+      m[i] = stt[0];
+      l[i] = stt[1];
+      ov[i] = *(const f32x4*)(stt + 4 + 4 * c);
+    } else {
+      m[i] = -INFINITY;
+      l[i] = 0.f;
+      ov[i] = f32x4{};
+    }
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kRedPerGroup; ++i) M = fmaxf(M, m[i]);
+  if (c == 0) sMax[grp] = M;
+  __syncthreads();
+#pragma unroll
+  for (int g2 = 0; g2 < kRedGroups; ++g2) M = fmaxf(M, sMax[g2]);
+
   f32x4 acc = f32x4{};
   float den = 0.f;
-#pragma unroll 4
-  for (int s = grp; s < ns; s += 8) {
-    const float* stt = base + (size_t)s * kStateFloats;
-    const float m = stt[0];
-    const float w = m == -INFINITY ? 0.f : fast_exp2(m - M);
-    den += w * stt[1];
-    acc += w * *(const f32x4*)(stt + 4 + 4 * c);
+#pragma unroll
+  for (int i = 0; i < kRedPerGroup; ++i) {
+    const float w = m[i] == -INFINITY ? 0.f : fast_exp2(m[i] - M);
+    den += w * l[i];
+    acc += w * ov[i];
   }
   *(f32x4*)&sAcc[grp][4 * c] = acc;
   if (c == 0) sDen[grp] = den;
@@ -350,7 +421,7 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
   if (tid < kHeadDim) {
     float num = 0.f, dsum = 0.f;
 #pragma unroll
-    for (int g2 = 0; g2 < 8; ++g2) {
+    for (int g2 = 0; g2 < kRedGroups; ++g2) {
       num += sAcc[g2][tid];
       dsum += sDen[g2];
     }
@@ -363,9 +434,11 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
 void decode_geometry(int B, int Hkv, int max_len, int* chunk, int* n_split) {
   // about one workgroup per CU (256 CUs; each holds 144 KB of LDS): enough
   // copies in flight to stream at full bandwidth while keeping few split
-  // states for the reduce; chunks are multiples of one 32-key step
-  const long long groups = (long long)B * ((Hkv + kDecWaves - 1) / kDecWaves);
-  const long long want = (256 + groups - 1) / groups;
+  // states for the reduce (at most kRedGroups * kRedPerGroup per head);
+  // chunks are multiples of one 16-key step
+  const long long groups = (long long)B * ((Hkv + kDecHeads - 1) / kDecHeads);
+  long long want = (256 + groups - 1) / groups;
+  if (want > kRedGroups * kRedPerGroup) want = kRedGroups * kRedPerGroup;
   long long ch = ((long long)max_len + want - 1) / want;
   ch = (ch + kDecTile - 1) / kDecTile * kDecTile;
   if (ch < 128) ch = 128;
@@ -396,7 +469,7 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
   a.g = Hq / Hkv;
   a.max_len = max_len;
   decode_geometry(B, Hkv, max_len, &a.chunk, &a.n_split);
-  a.n_hgroups = (Hkv + kDecWaves - 1) / kDecWaves;
+  a.n_hgroups = (Hkv + kDecHeads - 1) / kDecHeads;
   a.w_pre = w_pre;
   a.w0 = w0;
   a.q_scale = 1.4426950408889634f / sqrtf((float)kHeadDim);
@@ -405,11 +478,11 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
   if (bifocal) {
     hipLaunchKernelGGL(decode_split_kernel<true>, dim3((unsigned)nwg), dim3(kDecThreads), 0,
                        stream, a);
-    hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq), dim3(256), 0, stream, a, o);
+    hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq), dim3(512), 0, stream, a, o);
   } else {
     hipLaunchKernelGGL(decode_split_kernel<false>, dim3((unsigned)nwg), dim3(kDecThreads), 0,
                        stream, a);
-    hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq), dim3(256), 0, stream, a, o);
+    hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq), dim3(512), 0, stream, a, o);
   }
   return hipGetLastError();
 }
