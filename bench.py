@@ -105,8 +105,9 @@ def main() -> int:
     ap.add_argument("--decode", default="qwen3_4b_decode_128k")
     ap.add_argument("--overhead-reps", type=int, default=3,
                     help="interleaved vanilla/bifocal prefill pairs for the overhead figure")
-    ap.add_argument("--decode-reps", type=int, default=20,
-                    help="interleaved vanilla/bifocal decode pairs for the overhead figure")
+    ap.add_argument("--decode-reps", type=int, default=100,
+                    help="interleaved vanilla/bifocal decode pairs (overhead figure and the "
+                         "decode median)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -221,6 +222,10 @@ def main() -> int:
         dv_.append(timed(lambda: decode(r, False)))
         db_.append(timed(lambda: decode(r, True)))
     med = lambda x: sorted(x)[len(x) // 2] if x else float("nan")
+    # one decode call is ~0.1 ms and varies by several percent from call to
+    # call: report the median over the in-step calls and the interleaved ones
+    dec_med = med(dec_ms + db_)
+    dec_gbps = (kv_bytes + io_bytes) / (dec_med * 1e-3) / 1e9
 
     traffic = _traffic_from_profile()
     line = {
@@ -248,7 +253,7 @@ def main() -> int:
         },
         "prefill_ms": round(pre_avg, 3),
         "prefill_mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-        "decode_us": round(dec_avg * 1e3, 2),
+        "decode_us": round(dec_med * 1e3, 2),
         "decode_GBps": round(dec_gbps, 1),
         "decode_hbm_frac": round(dec_gbps / PEAK_HBM_GBPS, 4),
         "overhead_prefill_vs_vanilla": round(med(pb) / med(pv) - 1.0, 4),

@@ -364,24 +364,25 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
 }
 
 // Final merge over the splits of one head (Eq. (7) weights exp2(m - M)):
-// O = sum W O~ / sum W l.  16 groups of 32 threads; group grp takes splits
-// grp, grp + 16, ... (at most kRedPerGroup each, loads issued together),
-// thread c of a group owns output channels 4c .. 4c+3; partial sums meet in
-// LDS.
-constexpr int kRedGroups = 16;
-constexpr int kRedPerGroup = 8;  // splits per group: n_split <= 128
-__global__ __launch_bounds__(512) void decode_reduce_kernel(DecodeArgs a, uint16_t* o) {
+// O = sum W O~ / sum W l.  Workgroup (head, quarter of the 128 channels):
+// 32 groups of 8 threads; group grp takes splits grp, grp + 32, ... (at most
+// kRedPerGroup each, loads issued together), thread c of a group owns
+// channels 32 quarter + 4c .. +3; partial sums meet in LDS.
+constexpr int kRedGroups = 32;
+constexpr int kRedPerGroup = 4;  // splits per group: n_split <= 128
+__global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16_t* o) {
   __shared__ float sMax[kRedGroups];
-  __shared__ __attribute__((aligned(16))) float sAcc[kRedGroups][kHeadDim];
+  __shared__ __attribute__((aligned(16))) float sAcc[kRedGroups][32];
   __shared__ float sDen[kRedGroups];
   const int bh = blockIdx.x;
+  const int quarter = blockIdx.y;
   const int b = bh / a.Hq;
   const int tid = threadIdx.x;
   const int kv_len = clamp_len(a.kv_lens[b], a.max_len);
   const int ns = (kv_len + a.chunk - 1) / a.chunk;
   const float* base = a.ws + (size_t)bh * a.n_split * kStateFloats;
-  const int c = tid & 31;
-  const int grp = tid >> 5;
+  const int c = tid & 7;
+  const int grp = tid >> 3;
 
   float m[kRedPerGroup], l[kRedPerGroup];
   f32x4 ov[kRedPerGroup];
@@ -392,7 +393,7 @@ __global__ __launch_bounds__(512) void decode_reduce_kernel(DecodeArgs a, uint16
       const float* stt = base + (size_t)s * kStateFloats;
       m[i] = stt[0];
       l[i] = stt[1];
-      ov[i] = *(const f32x4*)(stt + 4 + 4 * c);
+      ov[i] = *(const f32x4*)(stt + 4 + 32 * quarter + 4 * c);
     } else {
       m[i] = -INFINITY;
       l[i] = 0.f;
@@ -418,7 +419,7 @@ __global__ __launch_bounds__(512) void decode_reduce_kernel(DecodeArgs a, uint16
   *(f32x4*)&sAcc[grp][4 * c] = acc;
   if (c == 0) sDen[grp] = den;
   __syncthreads();
-  if (tid < kHeadDim) {
+  if (tid < 32) {
     float num = 0.f, dsum = 0.f;
 #pragma unroll
     for (int g2 = 0; g2 < kRedGroups; ++g2) {
@@ -426,7 +427,7 @@ __global__ __launch_bounds__(512) void decode_reduce_kernel(DecodeArgs a, uint16
       dsum += sDen[g2];
     }
     const __bf16 r = (__bf16)(num / dsum);
-    o[(size_t)bh * kHeadDim + tid] = __builtin_bit_cast(uint16_t, r);
+    o[(size_t)bh * kHeadDim + 32 * quarter + tid] = __builtin_bit_cast(uint16_t, r);
   }
 }
 
@@ -478,11 +479,11 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
   if (bifocal) {
     hipLaunchKernelGGL(decode_split_kernel<true>, dim3((unsigned)nwg), dim3(kDecThreads), 0,
                        stream, a);
-    hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq), dim3(512), 0, stream, a, o);
+    hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq, 4), dim3(256), 0, stream, a, o);
   } else {
     hipLaunchKernelGGL(decode_split_kernel<false>, dim3((unsigned)nwg), dim3(kDecThreads), 0,
                        stream, a);
-    hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq), dim3(512), 0, stream, a, o);
+    hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq, 4), dim3(256), 0, stream, a, o);
   }
   return hipGetLastError();
 }
