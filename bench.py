@@ -108,6 +108,8 @@ def main() -> int:
     ap.add_argument("--decode-reps", type=int, default=100,
                     help="interleaved vanilla/bifocal decode pairs (overhead figure and the "
                          "decode median)")
+    ap.add_argument("--literal-reps", type=int, default=2,
+                    help="timed calls of the literal three-pass prefill (0 skips it)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -180,11 +182,19 @@ def main() -> int:
         decode(i)
     torch.cuda.synchronize()
 
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    # e[0..3]: whole prefill and decode calls; e[4..7]: the attention kernel
+    # and the decode split kernel alone, recorded by the library on the same
+    # stream right around those launches
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(args.steps)]
+    for e in ev:
+        for x in e:
+            x.record(stream)  # creates the HIP events before they are handed over
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         e = ev[i]
+        api.debug_kernel_events(0, e[4], e[5])
+        api.debug_kernel_events(1, e[6], e[7])
         e[0].record(stream)
         prefill()
         e[1].record(stream)
@@ -193,14 +203,21 @@ def main() -> int:
         e[3].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    api.debug_kernel_events(0)
+    api.debug_kernel_events(1)
 
     pre_ms = [e[0].elapsed_time(e[1]) for e in ev]
     dec_ms = [e[2].elapsed_time(e[3]) for e in ev]
+    attn_ms = [e[4].elapsed_time(e[5]) for e in ev]
+    split_ms = [e[6].elapsed_time(e[7]) for e in ev]
     pre_avg = sum(pre_ms) / len(pre_ms)
     dec_avg = sum(dec_ms) / len(dec_ms)
+    attn_avg = sum(attn_ms) / len(attn_ms)
+    split_avg = sum(split_ms) / len(split_ms)
 
     flops = 4.0 * wp.d * wp.B * wp.Hq * wp.L * (wp.L + 1) / 2.0
     tflops = flops / (pre_avg * 1e-3) / 1e12
+    attn_tflops = flops / (attn_avg * 1e-3) / 1e12
     kv_bytes = 2.0 * float(np.sum(lens)) * wd.Hkv * wd.d * 2.0
     io_bytes = 2.0 * wd.B * wd.Hq * wd.d * 2.0
     dec_gbps = (kv_bytes + io_bytes) / (dec_avg * 1e-3) / 1e9
@@ -226,6 +243,24 @@ def main() -> int:
     # call: report the median over the in-step calls and the interleaved ones
     dec_med = med(dec_ms + db_)
     dec_gbps = (kv_bytes + io_bytes) / (dec_med * 1e-3) / 1e9
+    split_gbps = kv_bytes / (split_avg * 1e-3) / 1e9
+
+    # ---- Eq. (7) taken literally: three window passes plus the merge
+    lit = {}
+    if args.literal_reps > 0:
+        lws = torch.empty(api.prefill_literal_workspace_bytes(wp.B, wp.Hq, wp.Hkv, wp.L),
+                          dtype=torch.uint8, device="cuda")
+
+        def literal():
+            api.bifocal_prefill_literal(q, k, v, w_pretrained=wp.w_pretrained,
+                                        w_local=wp.w_local, rope_theta=wp.theta, out=out,
+                                        workspace=lws, stream=stream)
+        literal()
+        lt = [timed(literal) for _ in range(args.literal_reps)]
+        del lws
+        lit = {"literal_prefill_ms": round(med(lt), 3),
+               "literal_throughput_vs_vanilla": round(med(pv) / med(lt), 4),
+               "fused_speedup_vs_literal": round(med(lt) / med(pb), 4)}
 
     traffic = _traffic_from_profile()
     line = {
@@ -260,18 +295,21 @@ def main() -> int:
         "overhead_decode_vs_vanilla": round(med(db_) / med(dv_) - 1.0, 4),
         "vanilla_prefill_ms": round(med(pv), 3),
         "vanilla_decode_us": round(med(dv_) * 1e3, 2),
+        **lit,
         "roofline": {
             "bound": "mfma",
-            "kernel": "prefill_kernel<bifocal>",
-            "achieved": round(tflops, 2),
+            "kernel": "prefill_kernel<fused>",
+            "achieved": round(attn_tflops, 2),
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
-            "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+            "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
+            "kernel_ms": round(attn_avg, 3),
         },
         "decode_roofline": {
-            "bound": "hbm", "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-            "frac": round(dec_gbps / PEAK_HBM_GBPS, 4),
+            "bound": "hbm", "kernel": "decode_split_kernel<bifocal>",
+            "achieved": round(split_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(split_gbps / PEAK_HBM_GBPS, 4), "kernel_us": round(split_avg * 1e3, 2),
         },
     }
     if not args.no_cpu_baseline:

@@ -96,6 +96,43 @@ int jl_rope_attention(const void* q, const void* k, const void* v, void* o, floa
                       int Hq, int Hkv, int L, int head_dim, double rope_theta, void* stream);
 
 /*
+ * Bytes of device workspace jl_bifocal_prefill_literal needs for this shape:
+ * 3 * B * L * Hq * head_dim * 4 (the window outputs) + the window LSEs
+ * (3 * B * Hq * L * 4, rounded up to 256) + 3 * B * Hkv * ceil(L / 64) * 16 KB
+ * (rotated key and transposed value tiles).  Returns 0 for invalid arguments.
+ */
+size_t jl_prefill_literal_workspace_bytes(int B, int Hq, int Hkv, int L, int head_dim);
+
+/*
+ * Bifocal prefill with Eq. (7) of Sec. 3.3 taken literally: the three
+ * attention calls A (band q - k <= w_local, base rotation), B (all causal
+ * keys, remote rotation) and C (band, remote rotation) run as three launches
+ * of the attention kernel, each writing its normalised output O_X and its
+ * natural-log LSE_X, and a fourth kernel merges them per row with
+ *   M = max(LSE_A, LSE_B, LSE_C), W_X = exp(LSE_X - M),
+ *   O = (W_A O_A + (W_B O_B - W_C O_C)) / (W_A + (W_B - W_C)),
+ *   lse = M + ln(W_A + (W_B - W_C)),
+ * in fp32.  This is the unfused variant the fused kernel of
+ * jl_bifocal_prefill replaces; the two agree up to rounding, except where the
+ * band dominates window B so strongly that the subtraction cancels (the
+ * literal form loses precision there; the fused form does not subtract).
+ * Arguments as in jl_bifocal_prefill, plus
+ *   workspace, workspace_bytes: device memory of at least
+ *     jl_prefill_literal_workspace_bytes(B, Hq, Hkv, L, head_dim) bytes,
+ *     256-byte aligned, owned by the caller; contents on entry do not matter.
+ *     On return (after the stream completes) it holds, for X = A, B, C
+ *     (x = 0, 1, 2), O_X as fp32 [B, L, Hq, head_dim] at float offset
+ *     x * B * L * Hq * head_dim, and LSE_X as fp32 [B, Hq, L] at float offset
+ *     3 * B * L * Hq * head_dim + x * B * Hq * L.
+ * When G == 1 the call runs the vanilla kernel, as jl_bifocal_prefill does,
+ * and leaves the workspace unwritten.  No library scratch is used.
+ */
+int jl_bifocal_prefill_literal(const void* q, const void* k, const void* v, void* o, float* lse,
+                               int B, int Hq, int Hkv, int L, int head_dim, double rope_theta,
+                               int w_pretrained, int w_local, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/*
  * Bytes of device workspace the decode entry points need for this shape
  * (split-K partial softmax states).  Returns 0 for invalid arguments.
  */
@@ -167,6 +204,19 @@ int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_
  * use while prefill calls are in flight.
  */
 double jl_debug_prefill_rescale_log2(double log2_bound);
+
+/*
+ * Timing hook for benchmarks, process-wide.  which = 0: every later
+ * jl_bifocal_prefill / jl_rope_attention call records the HIP event `start`
+ * on its stream right before its attention kernel and `stop` right after it,
+ * so hipEventElapsedTime(start, stop) is that kernel's duration alone (the
+ * key-rotation kernel in front of it stays outside).  which = 1: the same
+ * around the split kernel of every decode call (the reduce stays outside).
+ * start, stop: hipEvent_t created and owned by the caller; NULL, NULL clears
+ * the hook.  JL_ERR_INVALID_ARG for another `which` or when only one event is
+ * NULL.  The events must outlive every call that records them.
+ */
+int jl_debug_kernel_events(int which, void* start, void* stop);
 
 /* Frees the library-owned cos/sin tables and prefill scratch buffers on every
  * device (they are rebuilt on demand); waits for the streams that own scratch.

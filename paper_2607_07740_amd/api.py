@@ -49,6 +49,11 @@ def lib() -> ctypes.CDLL:
                                          i32, vp]
         L.jl_rope_attention.restype = i32
         L.jl_rope_attention.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl, vp]
+        L.jl_prefill_literal_workspace_bytes.restype = sz
+        L.jl_prefill_literal_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
+        L.jl_bifocal_prefill_literal.restype = i32
+        L.jl_bifocal_prefill_literal.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl,
+                                                 i32, i32, vp, sz, vp]
         L.jl_decode_workspace_bytes.restype = sz
         L.jl_decode_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
         L.jl_bifocal_decode.restype = i32
@@ -65,6 +70,8 @@ def lib() -> ctypes.CDLL:
                                              ctypes.POINTER(i32), ctypes.POINTER(i32), vp]
         L.jl_debug_prefill_rescale_log2.restype = dbl
         L.jl_debug_prefill_rescale_log2.argtypes = [dbl]
+        L.jl_debug_kernel_events.restype = i32
+        L.jl_debug_kernel_events.argtypes = [i32, vp, vp]
         L.jl_release_caches.restype = None
         L.jl_release_caches.argtypes = []
         _lib = L
@@ -139,6 +146,50 @@ def rope_attention(q, k, v, *, rope_theta: float = 1e6, out=None, lse=None,
     """jl_rope_attention: vanilla causal RoPE attention with the same kernel."""
     return _prefill(False, q, k, v, 1, 0, rope_theta, out, lse, want_lse or lse is not None,
                     stream)
+
+
+def prefill_literal_workspace_bytes(B: int, Hq: int, Hkv: int, L: int,
+                                    head_dim: int = 128) -> int:
+    return int(lib().jl_prefill_literal_workspace_bytes(B, Hq, Hkv, L, head_dim))
+
+
+def bifocal_prefill_literal(q, k, v, *, w_pretrained: int, w_local: int, rope_theta: float = 1e6,
+                            out=None, lse=None, want_lse: bool = False, workspace=None,
+                            stream=None):
+    """jl_bifocal_prefill_literal: Eq. (7) as three window passes and a merge.
+
+    Returns out (and lse when asked).  workspace, if given, is a uint8 CUDA
+    tensor of at least prefill_literal_workspace_bytes(...) bytes; after the
+    call literal_window_states(workspace, ...) views the per-window results.
+    """
+    import torch
+    B, L, Hq, D = q.shape
+    Hkv = k.shape[2]
+    if k.shape != (B, L, Hkv, D) or v.shape != k.shape:
+        raise ValueError("k and v must be [B, L, Hkv, D] matching q [B, L, Hq, D]")
+    want_lse = want_lse or lse is not None
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, L), dtype=torch.float32, device=q.device)
+    need = prefill_literal_workspace_bytes(B, Hq, Hkv, L, D)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
+    _check(lib().jl_bifocal_prefill_literal(
+        _dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
+        _dev(v, "v", torch.bfloat16), _dev(out, "out", torch.bfloat16),
+        _dev(lse, "lse", torch.float32) if lse is not None else None, B, Hq, Hkv, L, D,
+        float(rope_theta), int(w_pretrained), int(w_local), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+    return (out, lse) if want_lse else out
+
+
+def literal_window_states(workspace, B: int, Hq: int, L: int, head_dim: int = 128):
+    """Views of a literal-prefill workspace: (O [3, B, L, Hq, D] fp32, LSE [3, B, Hq, L] fp32)."""
+    import torch
+    n_o = 3 * B * L * Hq * head_dim
+    f = workspace[: 4 * (n_o + 3 * B * Hq * L)].view(torch.float32)
+    return (f[:n_o].view(3, B, L, Hq, head_dim), f[n_o:].view(3, B, Hq, L))
 
 
 def decode_workspace_bytes(B: int, Hq: int, Hkv: int, max_len: int, head_dim: int = 128) -> int:
@@ -221,3 +272,16 @@ def release_caches() -> None:
 def debug_prefill_rescale_log2(log2_bound: float) -> float:
     """jl_debug_prefill_rescale_log2: set the prefill rescale bound, return the old one."""
     return float(lib().jl_debug_prefill_rescale_log2(float(log2_bound)))
+
+
+def debug_kernel_events(which: int, start=None, stop=None) -> None:
+    """jl_debug_kernel_events: record torch.cuda.Event pair (start, stop) around
+    the prefill attention kernel (which = 0) or the decode split kernel
+    (which = 1) of every later call; no events clears the hook."""
+    def ev(e):
+        if e is None:
+            return None
+        if e.cuda_event == 0:  # torch creates the HIP event at its first record
+            e.record()
+        return ctypes.c_void_p(e.cuda_event)
+    _check(lib().jl_debug_kernel_events(int(which), ev(start), ev(stop)))

@@ -456,7 +456,7 @@ size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len) {
 hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                          const int32_t* kv_lens, int max_len, uint16_t* o, const float2* table,
                          int B, int Hq, int Hkv, int w_pre, int w0, float* ws,
-                         hipStream_t stream) {
+                         hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
   DecodeArgs a;
   a.q = q;
   a.kc = kc;
@@ -476,15 +476,18 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
   a.q_scale = 1.4426950408889634f / sqrtf((float)kHeadDim);
   const long long nwg = (long long)a.n_split * a.n_hgroups * B;
   if (nwg > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  if (bifocal) {
+  // ev0 / ev1 (optional) are recorded on the stream around the split kernel
+  hipError_t e = hipSuccess;
+  if (ev0 != nullptr && (e = hipEventRecord(ev0, stream)) != hipSuccess) return e;
+  if (bifocal)
     hipLaunchKernelGGL(decode_split_kernel<true>, dim3((unsigned)nwg), dim3(kDecThreads), 0,
                        stream, a);
-    hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq, 4), dim3(256), 0, stream, a, o);
-  } else {
+  else
     hipLaunchKernelGGL(decode_split_kernel<false>, dim3((unsigned)nwg), dim3(kDecThreads), 0,
                        stream, a);
-    hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq, 4), dim3(256), 0, stream, a, o);
-  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (ev1 != nullptr && (e = hipEventRecord(ev1, stream)) != hipSuccess) return e;
+  hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq, 4), dim3(256), 0, stream, a, o);
   return hipGetLastError();
 }
 

@@ -20,7 +20,13 @@ namespace jl {
 size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L);
 hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                           uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
-                          int L, int G, int w0, float sum_hi, void* ws, hipStream_t stream);
+                          int L, int G, int w0, float sum_hi, void* ws, hipStream_t stream,
+                          hipEvent_t ev0, hipEvent_t ev1);
+size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L);
+hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                  uint16_t* o, float* lse, const float2* table, int B, int Hq,
+                                  int Hkv, int L, int G, int w0, float sum_hi, void* ws,
+                                  hipStream_t stream);
 int prefill_rows_per_block();
 int prefill_block_q(int g);
 int prefill_block_k();
@@ -28,7 +34,7 @@ size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len);
 hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                          const int32_t* kv_lens, int max_len, uint16_t* o, const float2* table,
                          int B, int Hq, int Hkv, int w_pre, int w0, float* ws,
-                         hipStream_t stream);
+                         hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_build_table(float2* table, int n_pos, const double* omega, hipStream_t stream);
 hipError_t launch_debug_schedule(const int32_t* lengths, int nl, const int32_t* positions, int np,
                                  int w, int32_t* gout, int32_t* fout, int32_t* dout,
@@ -44,6 +50,16 @@ thread_local std::string t_detail;
 // log2 of the prefill row-sum bound that moves the softmax reference; the
 // debug entry lowers it so tests can drive the rescale path on ordinary data
 std::atomic<double> g_rescale_log2{64.0};
+// benchmark timing hook: events recorded around the prefill attention kernel
+// ([0]) and the decode split kernel ([1]); null when unset
+std::mutex g_ev_mu;
+hipEvent_t g_events[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
+
+void timing_events(int which, hipEvent_t* ev0, hipEvent_t* ev1) {
+  std::lock_guard<std::mutex> lock(g_ev_mu);
+  *ev0 = g_events[which][0];
+  *ev1 = g_events[which][1];
+}
 
 int fail(int status, const char* fmt, ...) {
   char buf[512];
@@ -179,9 +195,12 @@ int check_common(int B, int Hq, int Hkv, int head_dim, double theta) {
   return JL_OK;
 }
 
+// literal: run Eq. (7) as three window passes plus a merge, in the caller's
+// workspace (ws, ws_bytes); otherwise the fused or vanilla kernel with the
+// library scratch.
 int prefill_common(bool bifocal, const void* q, const void* k, const void* v, void* o, float* lse,
                    int B, int Hq, int Hkv, int L, int head_dim, double theta, int w_pre, int w0,
-                   void* stream) {
+                   void* stream, bool literal = false, void* ws = nullptr, size_t ws_bytes = 0) {
   int st = check_common(B, Hq, Hkv, head_dim, theta);
   if (st != JL_OK) return st;
   if (L < 1) return fail(JL_ERR_INVALID_ARG, "L must be >= 1 (got %d)", L);
@@ -197,6 +216,14 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
     return fail(JL_ERR_UNSUPPORTED, "GQA group Hq/Hkv = %d must divide %d", g, rows);
   const long long nqb = (L + (rows / g) - 1) / (rows / g);
   if (nqb * B * Hkv > 0x7fffffffLL) return fail(JL_ERR_INVALID_ARG, "problem too large");
+  if ((long long)B * Hkv > 65535) return fail(JL_ERR_INVALID_ARG, "B * Hkv too large");
+  if (literal) {
+    const size_t need = jl::literal_workspace_bytes(B, Hq, Hkv, L);
+    if (ws == nullptr || ws_bytes < need)
+      return fail(JL_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+    if ((reinterpret_cast<uintptr_t>(ws) & 255) != 0)
+      return fail(JL_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  }
   const int G = bifocal ? (int)jl_group_size(L, w_pre) : 1;
   const float2* table = nullptr;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -205,14 +232,25 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   // G == 1: f is the identity and the method is the base model (Sec. 3), so
   // the bifocal entry runs the vanilla kernel and matches it bit for bit.
   const bool use_bifocal = bifocal && G > 1;
-  if ((long long)B * Hkv > 65535) return fail(JL_ERR_INVALID_ARG, "B * Hkv too large");
+  const float sum_hi = (float)std::exp2(g_rescale_log2.load());
+  if (literal) {
+    if (use_bifocal) {
+      hipError_t e = jl::launch_prefill_literal((const uint16_t*)q, (const uint16_t*)k,
+                                                (const uint16_t*)v, (uint16_t*)o, lse, table, B,
+                                                Hq, Hkv, L, G, w0, sum_hi, ws, s);
+      if (e != hipSuccess) return hip_fail(e, "literal prefill launch");
+      return ok();
+    }
+  }
   std::lock_guard<std::mutex> launch_lock(g_prefill_mu);
   void* scratch = nullptr;
   st = get_scratch(s, jl::prefill_workspace_bytes(use_bifocal, B, Hkv, L), &scratch);
   if (st != JL_OK) return st;
+  hipEvent_t ev0, ev1;
+  timing_events(0, &ev0, &ev1);
   hipError_t e = jl::launch_prefill(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,
                                     (const uint16_t*)v, (uint16_t*)o, lse, table, B, Hq, Hkv, L,
-                                    G, w0, (float)std::exp2(g_rescale_log2.load()), scratch, s);
+                                    G, w0, sum_hi, scratch, s, ev0, ev1);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   return ok();
 }
@@ -241,9 +279,11 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   st = get_table(theta, max_len, s, &table);
   if (st != JL_OK) return st;
+  hipEvent_t ev0, ev1;
+  timing_events(1, &ev0, &ev1);
   hipError_t e = jl::launch_decode(bifocal, (const uint16_t*)q, (const uint16_t*)kc,
                                    (const uint16_t*)vc, kv_lens, max_len, (uint16_t*)o, table, B,
-                                   Hq, Hkv, w_pre, w0, (float*)ws, s);
+                                   Hq, Hkv, w_pre, w0, (float*)ws, s, ev0, ev1);
   if (e != hipSuccess) return hip_fail(e, "decode launch");
   return ok();
 }
@@ -284,6 +324,19 @@ int jl_rope_attention(const void* q, const void* k, const void* v, void* o, floa
                       int Hq, int Hkv, int L, int head_dim, double rope_theta, void* stream) {
   return prefill_common(false, q, k, v, o, lse, B, Hq, Hkv, L, head_dim, rope_theta, 1, 0,
                         stream);
+}
+
+size_t jl_prefill_literal_workspace_bytes(int B, int Hq, int Hkv, int L, int head_dim) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || L < 1 || head_dim != kHeadDim) return 0;
+  return jl::literal_workspace_bytes(B, Hq, Hkv, L);
+}
+
+int jl_bifocal_prefill_literal(const void* q, const void* k, const void* v, void* o, float* lse,
+                               int B, int Hq, int Hkv, int L, int head_dim, double rope_theta,
+                               int w_pretrained, int w_local, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  return prefill_common(true, q, k, v, o, lse, B, Hq, Hkv, L, head_dim, rope_theta, w_pretrained,
+                        w_local, stream, true, workspace, workspace_bytes);
 }
 
 size_t jl_decode_workspace_bytes(int B, int Hq, int Hkv, int max_len, int head_dim) {
@@ -348,6 +401,16 @@ int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_
   hipError_t e = jl::launch_debug_tiles(L, BQ, BK, w_local, nqb, nkt, classes_out,
                                         reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "debug tiles launch");
+  return ok();
+}
+
+int jl_debug_kernel_events(int which, void* start, void* stop) {
+  if (which != 0 && which != 1) return fail(JL_ERR_INVALID_ARG, "which must be 0 or 1");
+  if ((start == nullptr) != (stop == nullptr))
+    return fail(JL_ERR_INVALID_ARG, "start and stop must both be set or both be NULL");
+  std::lock_guard<std::mutex> lock(g_ev_mu);
+  g_events[which][0] = reinterpret_cast<hipEvent_t>(start);
+  g_events[which][1] = reinterpret_cast<hipEvent_t>(stop);
   return ok();
 }
 

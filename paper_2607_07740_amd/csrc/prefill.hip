@@ -25,20 +25,19 @@
 // (m, l, O) with the max-shifted, linear-space merge of Eq. (7).  Band keys
 // never enter the remote state, so the exclusion window C of Eq. (7) is empty
 // and nothing is subtracted.  The vanilla kernel is the same code with only
-// the base view.
+// the base view.  The same kernel also runs Eq. (7) literally: three launches
+// for the windows A, B and C, each over one view, then a merge kernel.
 //
-// Work decomposition: a workgroup is 4 wave64s, one per SIMD, and owns 256
-// query rows = (head hl = r / BQ, position q0 + r % BQ) for the g = Hq/Hkv
-// query heads sharing one kv head (GQA packing), BQ = 256 / g.  Each wave owns
-// 64 rows as two 32-column blocks (qc = 0, 1).  A lane owns one query column
-// of S^T = K Q^T (v_mfma_f32_32x32x16_bf16), and O^T += V^T P^T takes P^T
-// straight from the S^T accumulator registers.  Tiles of 64 keys rotate
-// through three LDS buffers: tile j+2 is in flight while tile j is computed.
-//
-// Schedule of one tile visit: S^T of block 0; S^T of block 1 beside the
-// softmax of block 0; PV of block 0 beside the softmax of block 1; PV of block
-// 1.  Within a phase the MFMAs and the vector work are independent, so one
-// wave keeps the matrix cores and the VALU busy together.
+// Work decomposition: a workgroup is 4 wave64s and owns 128 query rows =
+// (head hl = r / BQ, position q0 + r % BQ) for the g = Hq/Hkv query heads
+// sharing one kv head (GQA packing), BQ = 128 / g.  Two workgroups share a CU
+// (64 KB of LDS each), so every SIMD runs two waves.  A wave owns 32 rows; a
+// lane owns one query column of S^T = K Q^T (v_mfma_f32_32x32x16_bf16, lanes l
+// and l + 32 split the column's 16 accumulator rows), and O^T += V^T P^T takes
+// P^T straight from the S^T accumulator registers.  Tiles of 64 keys are
+// double-buffered: all four waves copy their quarter of tile j+1 into LDS
+// while tile j is computed.  The O^T accumulator (4 x 16 fp32 per lane) stays
+// in VGPRs.
 //
 // Softmax runs in the log2 domain against a per-row reference m (initially 0).
 // -m enters the MFMA itself as one extra k-step (a constant A operand with a
@@ -171,11 +170,22 @@ struct PrefillArgs {
   const uint16_t* vt;
   int B, Hq, Hkv, L, n_tiles;
   int g, BQ, n_qblocks;
-  int w0;         // local window; INT_MAX for the vanilla kernel
+  int w0;         // local window; INT_MAX for the vanilla kernel and window B
   FastDiv gdiv;   // division by G (Eq. (3))
   float q_scale;  // log2(e) / sqrt(head_dim): scores come out in log2 units
   float sum_hi;   // a tile's row sum above this moves the reference (2^64)
+  float* o32;     // window passes: normalised fp32 O_X [B][L][Hq][128]
 };
+
+// What one launch of the attention kernel computes.
+//   kModeFused    the bifocal result in one pass: remote-view tiles holding
+//                 pairs with q - k > w0, then base-view tiles of the band
+//   kModeVanilla  causal attention in the base view (the unmodified model)
+//   kModeWinA/B/C the three attention calls of Eq. (7), each a single view
+//                 over one key set: A = band in the base view, B = all causal
+//                 keys in the remote view, C = band in the remote view.
+//                 They write normalised fp32 O_X and the natural-log LSE_X.
+enum PrefillMode : int { kModeFused = 0, kModeVanilla = 1, kModeWinA = 2, kModeWinB = 3, kModeWinC = 4 };
 
 // Load one query row's B operand: 8 k-steps of 8 bf16 (d = 16 s + 8 half + j),
 // rotated to position pos and scaled.  Pairs (s, s + 4) are rotate-half partners.
@@ -217,8 +227,15 @@ __device__ inline float sum8(bf16x8 p, float acc) {
 }
 
 
-template <bool BIFOCAL>
+template <int MODE>
 __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
+  // The visit list has at most two segments: the fused kernel's remote tiles
+  // (segment 1), then tiles [kt_l, n_kt) in one view, keeping 0 <= q - k <= w0
+  // (segment 2; w0 = INT_MAX makes it the causal set).
+  constexpr bool FUSED = MODE == kModeFused;
+  constexpr bool REMOTE2 = MODE == kModeWinB || MODE == kModeWinC;  // segment 2's view
+  constexpr bool OUT_F32 = MODE == kModeWinA || MODE == kModeWinB || MODE == kModeWinC;
+  constexpr bool FROM_ZERO = MODE == kModeVanilla || MODE == kModeWinB;  // kt_l = 0
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmemBytes];
 
   const int tid = threadIdx.x;
@@ -256,11 +273,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const int hd = kvh * a.g + hl;
   const uint16_t* qrow = a.q + (((size_t)b * L + qp) * a.Hq + hd) * kHeadDim;
 
-  // ---- visit list: remote-view tiles [0, n_r), then base-view tiles from kt_l
+  // ---- visit list: segment 1 = tiles [0, n_r), segment 2 = tiles [kt_l, n_kt)
   const VisitRanges vr = visit_ranges(q0, q1, w0, kPfBK);
   const int n_kt = vr.n_kt;
-  const int n_r = BIFOCAL ? vr.n_r : 0;
-  const int kt_l = BIFOCAL ? vr.kt_l : 0;
+  const int n_r = FUSED ? vr.n_r : 0;
+  const int kt_l = FROM_ZERO ? 0 : vr.kt_l;
   const int n_steps = n_r + (n_kt - kt_l);
 
   // ---- staging: each wave copies its quarter (4 KB) of visit j's K image
@@ -269,10 +286,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const uint32_t smem_base = lds_addr(smem);
   const uint32_t lane_off = 16 * lane;
   auto issue = [&](int j) {
-    const bool remote = j < n_r;
-    const int kt = remote ? j : kt_l + (j - n_r);
+    const bool seg1 = j < n_r;
+    const int kt = seg1 ? j : kt_l + (j - n_r);
     const size_t off = img_base + (size_t)kt * (kTileBytes / 2) + wave * 2048;
-    const unsigned char* gk = (const unsigned char*)((BIFOCAL && remote ? a.krem : a.kloc) + off);
+    const bool use_rem = REMOTE2 || (FUSED && seg1);
+    const unsigned char* gk = (const unsigned char*)((use_rem ? a.krem : a.kloc) + off);
     const unsigned char* gv = (const unsigned char*)(a.vt + off);
     const uint32_t lk = smem_base + (j & 1) * 2 * kTileBytes + wave * 4096;
     const uint32_t lv = lk + kTileBytes;
@@ -288,7 +306,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
 
   // ---- query operand of the first view, state
   bf16x8 qop[8];
-  load_q_operand(qrow, hl32, a.table, n_r > 0 ? remote_pos(qp, a.gdiv) : qp, a.q_scale, qop);
+  load_q_operand(qrow, hl32, a.table, (n_r > 0 || REMOTE2) ? remote_pos(qp, a.gdiv) : qp,
+                 a.q_scale, qop);
 
   f32x16 acc_o[4];
 #pragma unroll
@@ -339,14 +358,14 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
   };
 
-  // element masks where the tile is not wholly inside the visit's view
-  auto mask = [&](int k0, bool remote, f32x16* sc) {
+  // element masks where the tile is not wholly inside the visit's key set
+  auto mask = [&](int k0, bool seg1, f32x16* sc) {
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int diff = qp - (k0 + 32 * blk + 8 * (i >> 2) + 4 * hl32 + (i & 3));
-        const bool keep = remote ? diff > w0 : (diff >= 0 && diff <= w0);
+        const bool keep = seg1 ? diff > w0 : (diff >= 0 && diff <= w0);
         sc[blk][i] = keep ? sc[blk][i] : -INFINITY;
       }
     }
@@ -406,10 +425,10 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   };
 
   // one visit of tile j in one view
-  auto step = [&](int j, auto remote_tag, auto mask_tag) {
-    constexpr bool remote = decltype(remote_tag)::value;
+  auto step = [&](int j, auto seg1_tag, auto mask_tag) {
+    constexpr bool seg1 = decltype(seg1_tag)::value;
     constexpr bool MASKED = decltype(mask_tag)::value;
-    const int k0 = (remote ? j : kt_l + (j - n_r)) * kPfBK;
+    const int k0 = (seg1 ? j : kt_l + (j - n_r)) * kPfBK;
     const unsigned char* kb = smem + (j & 1) * 2 * kTileBytes;
     const unsigned char* vb = kb + kTileBytes;
     f32x16 sc[2];
@@ -419,33 +438,35 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     __syncthreads();  // everyone's copies of tile j; buffer (j+1) & 1 is free
     if (j + 1 < n_steps) issue(j + 1);
     qk(kb, sc);
-    if (MASKED) mask(k0, remote, sc);
+    if (MASKED) mask(k0, seg1, sc);
     float psum = softmax(sc, pb);
     softmax_fix(sc, pb, psum);
     l_run += psum;
     pv(vb, pb);
   };
 
-  auto run = [&](int j, auto remote_tag) {
-    constexpr bool remote = decltype(remote_tag)::value;
-    const int k0 = (remote ? j : kt_l + (j - n_r)) * kPfBK;
-    const bool need_mask = remote ? !(q0 - (k0 + kPfBK - 1) > w0)
-                                  : !(q1 - k0 <= w0 && k0 + kPfBK - 1 <= q0);
+  auto run = [&](int j, auto seg1_tag) {
+    constexpr bool seg1 = decltype(seg1_tag)::value;
+    const int k0 = (seg1 ? j : kt_l + (j - n_r)) * kPfBK;
+    const bool need_mask = seg1 ? !(q0 - (k0 + kPfBK - 1) > w0)
+                                : !(q1 - k0 <= w0 && k0 + kPfBK - 1 <= q0);
     if (need_mask)
-      step(j, remote_tag, std::true_type{});
+      step(j, seg1_tag, std::true_type{});
     else
-      step(j, remote_tag, std::false_type{});
+      step(j, seg1_tag, std::false_type{});
   };
 
-  for (int j = 0; j < n_r; ++j) run(j, std::true_type{});
-  if (BIFOCAL && n_r > 0) load_q_operand(qrow, hl32, a.table, qp, a.q_scale, qop);
+  if (FUSED) {
+    for (int j = 0; j < n_r; ++j) run(j, std::true_type{});
+    if (n_r > 0) load_q_operand(qrow, hl32, a.table, qp, a.q_scale, qop);
+  }
   for (int j = n_r; j < n_steps; ++j) run(j, std::false_type{});
 
   // ---- normalise and write
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (row_valid) {
     const float inv = 1.f / l_tot;
-    uint16_t* orow = a.o + (((size_t)b * L + qp) * a.Hq + hd) * kHeadDim;
+    const size_t orow_off = (((size_t)b * L + qp) * a.Hq + hd) * kHeadDim;
 #pragma unroll
     for (int db = 0; db < 4; ++db) {
 #pragma unroll
@@ -453,7 +474,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
         f32x4 t;
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) t[jj] = acc_o[db][4 * q4 + jj] * inv;
-        *(bf16x4*)(orow + 32 * db + 8 * q4 + 4 * hl32) = __builtin_convertvector(t, bf16x4);
+        const int d = 32 * db + 8 * q4 + 4 * hl32;
+        if (OUT_F32)
+          *(f32x4*)(a.o32 + orow_off + d) = t;
+        else
+          *(bf16x4*)(a.o + orow_off + d) = __builtin_convertvector(t, bf16x4);
       }
     }
     if (a.lse != nullptr && hl32 == 0)
@@ -461,68 +486,178 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   }
 }
 
-// ---------------------------------------------------------------- launcher
+// ------------------------------------------------------ Eq. (7) merge kernel
+// The literal combination of the three window states, per query row:
+//   M = max(l_A, l_B, l_C),  W_X = exp(l_X - M),
+//   O = (W_A O_A + (W_B O_B - W_C O_C)) / (W_A + (W_B - W_C)),  lse = M + ln(den),
+// in fp32 with contraction off.  B and C are subtracted first: for a row whose
+// remote-only key set is empty (q <= w0) the two passes are bit-identical and
+// their terms cancel exactly.
+struct MergeArgs {
+  const float* o3;    // O_A, O_B, O_C: [B][L][Hq][128] each, o_stride floats apart
+  const float* lse3;  // LSE_A, LSE_B, LSE_C: [B][Hq][L] each, l_stride floats apart
+  uint16_t* o;        // bf16 [B][L][Hq][128]
+  float* lse;         // optional fp32 [B][Hq][L]
+  int L, Hq;
+  size_t rows, o_stride, l_stride;
+};
+
+// 32 lanes per row (4 channels each), 8 rows per 256-thread workgroup.
+__global__ __launch_bounds__(256) void literal_merge_kernel(MergeArgs a) {
+#pragma clang fp contract(off)
+  const size_t r = (size_t)blockIdx.x * 8 + (threadIdx.x >> 5);
+  if (r >= a.rows) return;
+  const int c = 4 * (threadIdx.x & 31);
+  const int h = (int)(r % a.Hq);
+  const size_t bq = r / a.Hq;
+  const int qpos = (int)(bq % a.L);
+  const size_t b = bq / a.L;
+  const size_t li = (b * a.Hq + h) * a.L + qpos;
+  const float la = a.lse3[li], lb = a.lse3[li + a.l_stride], lc = a.lse3[li + 2 * a.l_stride];
+  const float M = fmaxf(la, fmaxf(lb, lc));
+  const float wa = expf(la - M), wb = expf(lb - M), wc = expf(lc - M);
+  const float* src = a.o3 + r * kHeadDim + c;
+  const f32x4 oa = *(const f32x4*)src;
+  const f32x4 ob = *(const f32x4*)(src + a.o_stride);
+  const f32x4 oc = *(const f32x4*)(src + 2 * a.o_stride);
+  const float den = wa + (wb - wc);
+  f32x4 out;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = (wa * oa[i] + (wb * ob[i] - wc * oc[i])) / den;
+  *(bf16x4*)(a.o + r * kHeadDim + c) = __builtin_convertvector(out, bf16x4);
+  if (a.lse != nullptr && c == 0) a.lse[li] = M + logf(den);
+}
+
+// ---------------------------------------------------------------- launchers
 size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L) {
   const size_t tiles = (size_t)(L + kPfBK - 1) / kPfBK;
   return (size_t)(bifocal ? 3 : 2) * B * Hkv * tiles * kTileBytes;
 }
 
-hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                          uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
-                          int L, int G, int w0, float sum_hi, void* ws, hipStream_t stream) {
+// Literal mode workspace: O_A, O_B, O_C (fp32 [B][L][Hq][128] each), then
+// LSE_A, LSE_B, LSE_C (fp32 [B][Hq][L] each), then the tile images at the next
+// 256-byte boundary.
+static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
+size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L) {
+  const size_t rows = (size_t)B * L * Hq;
+  return 3 * rows * kHeadDim * sizeof(float) + round256(3 * rows * sizeof(float)) +
+         prefill_workspace_bytes(true, B, Hkv, L);
+}
+
+static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v,
+                              const float2* table, int B, int Hkv, int L, int G, void* images,
+                              PrefillArgs& a, hipStream_t stream) {
   const int n_tiles = (L + kPfBK - 1) / kPfBK;
   const size_t img = (size_t)B * Hkv * n_tiles * (kTileBytes / 2);  // bf16 elements per image set
-  uint16_t* kloc = (uint16_t*)ws;
-  uint16_t* vt = kloc + img;
-  uint16_t* krem = bifocal ? vt + img : nullptr;
+  a.kloc = (const uint16_t*)images;
+  a.vt = a.kloc + img;
+  a.krem = bifocal ? a.vt + img : nullptr;
+  a.n_tiles = n_tiles;
+  a.table = table;
+  a.gdiv = make_fastdiv((uint32_t)G);
 
   PrepArgs p;
   p.k = k;
   p.v = v;
-  p.kloc = kloc;
-  p.krem = krem;
-  p.vt = vt;
+  p.kloc = (uint16_t*)a.kloc;
+  p.krem = (uint16_t*)a.krem;
+  p.vt = (uint16_t*)a.vt;
   p.table = table;
   p.B = B;
   p.Hkv = Hkv;
   p.L = L;
   p.n_tiles = n_tiles;
-  p.gdiv = make_fastdiv((uint32_t)G);
+  p.gdiv = a.gdiv;
   if ((long long)B * Hkv > 65535) return hipErrorInvalidConfiguration;
   if (bifocal)
     hipLaunchKernelGGL(prep_kernel<true>, dim3(n_tiles, B * Hkv), dim3(256), 0, stream, p);
   else
     hipLaunchKernelGGL(prep_kernel<false>, dim3(n_tiles, B * Hkv), dim3(256), 0, stream, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
 
-  PrefillArgs a;
-  a.q = q;
-  a.o = o;
-  a.lse = lse;
-  a.table = table;
-  a.kloc = kloc;
-  a.krem = krem;
-  a.vt = vt;
+static void fill_geometry(PrefillArgs& a, int B, int Hq, int Hkv, int L, float sum_hi) {
   a.B = B;
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.L = L;
-  a.n_tiles = n_tiles;
   a.g = Hq / Hkv;
   a.BQ = kPfRows / a.g;
   a.n_qblocks = (L + a.BQ - 1) / a.BQ;
-  a.w0 = bifocal ? w0 : INT_MAX;
-  a.gdiv = make_fastdiv((uint32_t)G);
   a.q_scale = 1.4426950408889634f / sqrtf((float)kHeadDim);
   a.sum_hi = sum_hi;
-  const long long nwg = (long long)a.n_qblocks * B * Hkv;
+}
+
+static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream) {
+  const long long nwg = (long long)a.n_qblocks * a.B * a.Hkv;
   if (nwg > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  if (bifocal)
-    hipLaunchKernelGGL(prefill_kernel<true>, dim3((unsigned)nwg), dim3(kPfThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL(prefill_kernel<false>, dim3((unsigned)nwg), dim3(kPfThreads), 0, stream,
-                       a);
+  const dim3 grid((unsigned)nwg), block(kPfThreads);
+  switch (mode) {
+    case kModeFused: hipLaunchKernelGGL(prefill_kernel<kModeFused>, grid, block, 0, stream, a); break;
+    case kModeVanilla: hipLaunchKernelGGL(prefill_kernel<kModeVanilla>, grid, block, 0, stream, a); break;
+    case kModeWinA: hipLaunchKernelGGL(prefill_kernel<kModeWinA>, grid, block, 0, stream, a); break;
+    case kModeWinB: hipLaunchKernelGGL(prefill_kernel<kModeWinB>, grid, block, 0, stream, a); break;
+    case kModeWinC: hipLaunchKernelGGL(prefill_kernel<kModeWinC>, grid, block, 0, stream, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// ev0 / ev1 (optional) are recorded on the stream around the attention kernel.
+hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                          uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
+                          int L, int G, int w0, float sum_hi, void* ws, hipStream_t stream,
+                          hipEvent_t ev0, hipEvent_t ev1) {
+  PrefillArgs a = {};
+  fill_geometry(a, B, Hq, Hkv, L, sum_hi);
+  hipError_t e = launch_prep(bifocal, k, v, table, B, Hkv, L, G, ws, a, stream);
+  if (e != hipSuccess) return e;
+  a.q = q;
+  a.o = o;
+  a.lse = lse;
+  a.w0 = bifocal ? w0 : INT_MAX;
+  if (ev0 != nullptr && (e = hipEventRecord(ev0, stream)) != hipSuccess) return e;
+  e = launch_attn(bifocal ? kModeFused : kModeVanilla, a, stream);
+  if (e == hipSuccess && ev1 != nullptr) e = hipEventRecord(ev1, stream);
+  return e;
+}
+
+// Eq. (7) taken literally: the three window passes, then the merge.
+hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                  uint16_t* o, float* lse, const float2* table, int B, int Hq,
+                                  int Hkv, int L, int G, int w0, float sum_hi, void* ws,
+                                  hipStream_t stream) {
+  const size_t rows = (size_t)B * L * Hq;
+  float* o3 = (float*)ws;
+  float* lse3 = o3 + 3 * rows * kHeadDim;
+  void* images = (unsigned char*)ws + 3 * rows * kHeadDim * sizeof(float) +
+                 round256(3 * rows * sizeof(float));
+  PrefillArgs a = {};
+  fill_geometry(a, B, Hq, Hkv, L, sum_hi);
+  hipError_t e = launch_prep(true, k, v, table, B, Hkv, L, G, images, a, stream);
+  if (e != hipSuccess) return e;
+  a.q = q;
+  const int modes[3] = {kModeWinA, kModeWinB, kModeWinC};
+  for (int x = 0; x < 3; ++x) {
+    a.o32 = o3 + (size_t)x * rows * kHeadDim;
+    a.lse = lse3 + (size_t)x * rows;
+    a.w0 = modes[x] == kModeWinB ? INT_MAX : w0;
+    e = launch_attn(modes[x], a, stream);
+    if (e != hipSuccess) return e;
+  }
+  MergeArgs m;
+  m.o3 = o3;
+  m.lse3 = lse3;
+  m.o = o;
+  m.lse = lse;
+  m.L = L;
+  m.Hq = Hq;
+  m.rows = rows;
+  m.o_stride = rows * kHeadDim;
+  m.l_stride = rows;
+  const size_t nblk = (rows + 7) / 8;
+  if (nblk > 0x7fffffffULL) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL(literal_merge_kernel, dim3((unsigned)nblk), dim3(256), 0, stream, m);
   return hipGetLastError();
 }
 

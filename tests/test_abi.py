@@ -118,3 +118,26 @@ def test_debug_entry_points_reject_bad_arguments():
     assert rc == api.JL_ERR_INVALID_ARG  # no buffer, but the geometry is reported
     assert (bq.value, bk.value) == (64, 64)  # 128 rows = 64 positions x 2 heads
     assert (nq.value, nk.value) == (32, 32)
+
+
+def _literal(ws=A, ws_bytes=None, B=1, Hq=4, Hkv=2, L=64, w=16, w0=4, o=A):
+    if ws_bytes is None:
+        ws_bytes = api.prefill_literal_workspace_bytes(B, Hq, Hkv, L)
+    return api.lib().jl_bifocal_prefill_literal(A, A, A, o, None, B, Hq, Hkv, L, 128, 1e6, w, w0,
+                                                ws, ws_bytes, None)
+
+
+def test_literal_workspace_size_and_rejections():
+    B, Hq, Hkv, L = 2, 8, 2, 1000
+    n = api.prefill_literal_workspace_bytes(B, Hq, Hkv, L)
+    o_bytes = 3 * B * L * Hq * 128 * 4
+    lse_bytes = -(-3 * B * Hq * L * 4 // 256) * 256
+    img = 3 * B * Hkv * (-(-L // 64)) * 16384
+    assert n == o_bytes + lse_bytes + img
+    assert api.prefill_literal_workspace_bytes(B, 7, Hkv, L) == 0
+    assert api.prefill_literal_workspace_bytes(B, Hq, Hkv, L, 64) == 0
+    assert _literal(ws=None) == api.JL_ERR_WORKSPACE
+    assert _literal(ws_bytes=1024) == api.JL_ERR_WORKSPACE
+    assert _literal(ws=P(0x1010)) == api.JL_ERR_INVALID_ARG  # not 256-byte aligned
+    assert _literal(o=None) == api.JL_ERR_INVALID_ARG
+    assert _literal(w=0) == api.JL_ERR_INVALID_ARG
