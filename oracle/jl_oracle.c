@@ -20,6 +20,9 @@
  *     each returning (O_X, lse_X), merged by inclusion-exclusion  Sec. 3.3, Eq. (7)
  *   - decode: the same row at q = kv_len - 1 with G taken from
  *     L = kv_len (the cache holds raw keys, rotated on the fly)  Sec. 3.2, Eqs. (4)-(6)
+ *   - the ablated remote map of Sec. 4.5, Table 6: remote keys keep their
+ *     positions and are rotated with YaRN-style rescaled frequencies instead
+ *     of being aliased to f(x)
  *
  * RoPE convention (the paper does not print it; rotate-half pairing of the
  * Qwen3 family is assumed): for i < d/2 with omega_i = theta^(-2i/d),
@@ -88,6 +91,52 @@ void jlo_rope_rotate(const double* x, int d, double pos, double theta, double* y
   }
 }
 
+/* The same rotation with explicit per-pair angular frequencies omega[i]. */
+void jlo_rope_rotate_freqs(const double* x, int d, double pos, const double* omega, double* y) {
+  int half = d / 2;
+  for (int i = 0; i < half; ++i) {
+    double ang = pos * omega[i];
+    double c = cos(ang), s = sin(ang);
+    double a = x[i], b = x[i + half];
+    y[i] = a * c - b * s;
+    y[i + half] = b * c + a * s;
+  }
+}
+
+/*
+ * Frequencies of the frequency-interpolation remote map (the ablation of
+ * Sec. 4.5, Table 6, that keeps positions and rescales frequencies, in the
+ * style of YaRN).  The
+ * continuous factor is the one Sec. 3.1 names for such methods,
+ * s = max(1, L / w_pretrained).  Per pair i, following YaRN's per-dimension
+ * rule: wavelength lambda_i = 2 pi / omega_i, r_i = w_pretrained / lambda_i
+ * (turns completed over the pretraining window), ramp
+ *   gamma = 0 if r_i < alpha,  1 if r_i > beta,  (r_i - alpha) / (beta - alpha) else,
+ * and omega'_i = (1 - gamma) omega_i / s + gamma omega_i: pairs that turn
+ * many times inside the window keep their frequency, slow pairs are divided
+ * by s.  No attention temperature (only the rotation is replaced).
+ * omega_out: d/2 values.
+ */
+void jlo_yarn_frequencies(int d, double theta, double L, double w_pretrained, double alpha,
+                          double beta, double* omega_out) {
+  double s = L / w_pretrained;
+  if (s < 1.0) s = 1.0;
+  int half = d / 2;
+  for (int i = 0; i < half; ++i) {
+    double omega = pow(theta, -2.0 * (double)i / (double)d);
+    double lambda = 2.0 * acos(-1.0) / omega;
+    double r = w_pretrained / lambda;
+    double gamma;
+    if (r < alpha)
+      gamma = 0.0;
+    else if (r > beta)
+      gamma = 1.0;
+    else
+      gamma = (r - alpha) / (beta - alpha);
+    omega_out[i] = (1.0 - gamma) * omega / s + gamma * omega;
+  }
+}
+
 /* One softmax "call" over a key set: returns O (d values) and the natural-log
  * LSE of the scores.  scores[j] are already divided by sqrt(d). */
 static double softmax_call(const double* scores, const double* const* vals, int64_t n, int d,
@@ -114,8 +163,9 @@ static double dot(const double* a, const double* b, int d) {
 
 /*
  * Per (b, kv-head) rotated keys: kb[k] = R(k) x_k and kr[k] = R(f(k)) x_k for
- * k < n_keys, plus raw values, all in fp64.  key_stride is the distance in
- * elements between consecutive positions of one head.
+ * k < n_keys (or, with remote frequencies romega, kr[k] = R'(k) x_k at the
+ * unchanged position), plus raw values, all in fp64.  key_stride is the
+ * distance in elements between consecutive positions of one head.
  */
 typedef struct {
   int64_t n;
@@ -126,7 +176,8 @@ typedef struct {
 } keyset_t;
 
 static int keyset_build(keyset_t* ks, const uint16_t* k, const uint16_t* v, int64_t n, int d,
-                        int64_t key_stride, int64_t G, double theta, int want_remote) {
+                        int64_t key_stride, int64_t G, double theta, int want_remote,
+                        const double* romega) {
   ks->n = n;
   ks->d = d;
   ks->kb = (double*)malloc(sizeof(double) * (size_t)(n * d));
@@ -146,7 +197,9 @@ static int keyset_build(keyset_t* ks, const uint16_t* k, const uint16_t* v, int6
       if (!raw) continue;
       for (int c = 0; c < d; ++c) raw[c] = bf16_to_double(k[j * key_stride + c]);
       jlo_rope_rotate(raw, d, (double)j, theta, ks->kb + j * d);
-      if (want_remote)
+      if (want_remote && romega)
+        jlo_rope_rotate_freqs(raw, d, (double)j, romega, ks->kr + j * d);
+      else if (want_remote)
         jlo_rope_rotate(raw, d, (double)jlo_remote_position(j, G), theta, ks->kr + j * d);
       for (int c = 0; c < d; ++c) ks->v[j * d + c] = bf16_to_double(v[j * key_stride + c]);
     }
@@ -165,10 +218,12 @@ static void keyset_free(keyset_t* ks) {
  * One bifocal output row, Sec. 3.3: windows A, B, C computed separately, then
  * merged by Eq. (7) with M = max(lse_A, lse_B, lse_C), W_X = exp(lse_X - M).
  * xq: raw query (fp64, d); qpos: its 0-based position; G: the call's group
- * size; w0: local window.  Writes out[d] and returns the merged LSE.
+ * size; w0: local window; romega: NULL for the aliasing map f, else the
+ * remote frequencies (the query keeps its position).  Writes out[d] and
+ * returns the merged LSE.
  */
 static double bifocal_row(const double* xq, int64_t qpos, int64_t G, int64_t w0, double theta,
-                          const keyset_t* ks, double* out) {
+                          const keyset_t* ks, const double* romega, double* out) {
   int d = ks->d;
   double scale = 1.0 / sqrt((double)d);
   double* qb = (double*)malloc(sizeof(double) * (size_t)d);
@@ -180,7 +235,10 @@ static double bifocal_row(const double* xq, int64_t qpos, int64_t G, int64_t w0,
   double* s = (double*)malloc(sizeof(double) * (size_t)nb);
   const double** vv = (const double**)malloc(sizeof(double*) * (size_t)nb);
   jlo_rope_rotate(xq, d, (double)qpos, theta, qb);
-  jlo_rope_rotate(xq, d, (double)jlo_remote_position(qpos, G), theta, qr);
+  if (romega)
+    jlo_rope_rotate_freqs(xq, d, (double)qpos, romega, qr);
+  else
+    jlo_rope_rotate(xq, d, (double)jlo_remote_position(qpos, G), theta, qr);
 
   int64_t lo = qpos - w0;
   if (lo < 0) lo = 0;
@@ -249,16 +307,26 @@ static int check_shape(int B, int Hq, int Hkv, int L, int d, double theta) {
 /*
  * Prefill rows.  q: bf16 [B, L, Hq, d]; k, v: bf16 [B, L, Hkv, d].
  * rows: nrows triples (b, h, qpos).  bifocal != 0 selects Jet-Long, else
- * vanilla RoPE attention (w_pretrained and w0 ignored).  out: fp64 [nrows, d];
- * lse (nullable): fp64 [nrows], natural log.  G is one value for the whole
- * call, from the call's L.  Returns the number of threads used (>= 1) on
- * success, or -JLO_EINVAL / -JLO_ENOMEM.
+ * vanilla RoPE attention (w_pretrained and w0 ignored).  remote_map: 0 = the
+ * aliasing map f(x) = floor(x / G) of Eq. (3), 1 = frequency interpolation
+ * (jlo_yarn_frequencies with alpha = 1, beta = 32).  out: fp64 [nrows, d];
+ * lse (nullable): fp64 [nrows], natural log.  G (or s) is one value for the
+ * whole call, from the call's L.  Returns the number of threads used (>= 1)
+ * on success, or -JLO_EINVAL / -JLO_ENOMEM.
  */
-int jlo_prefill_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v, int B, int Hq,
-                     int Hkv, int L, int d, double theta, int64_t w_pretrained, int64_t w0,
-                     int bifocal, const int64_t* rows, int64_t nrows, double* out, double* lse) {
+int jlo_prefill_rows_map(const uint16_t* q, const uint16_t* k, const uint16_t* v, int B, int Hq,
+                         int Hkv, int L, int d, double theta, int64_t w_pretrained, int64_t w0,
+                         int bifocal, int remote_map, const int64_t* rows, int64_t nrows,
+                         double* out, double* lse) {
   if (!check_shape(B, Hq, Hkv, L, d, theta)) return -JLO_EINVAL;
   if (bifocal && (w_pretrained < 1 || w0 < 0)) return -JLO_EINVAL;
+  if (remote_map != 0 && remote_map != 1) return -JLO_EINVAL;
+  double* romega = NULL;
+  if (bifocal && remote_map == 1) {
+    romega = (double*)malloc(sizeof(double) * (size_t)(d / 2));
+    if (!romega) return -JLO_ENOMEM;
+    jlo_yarn_frequencies(d, theta, (double)L, (double)w_pretrained, 1.0, 32.0, romega);
+  }
   for (int64_t r = 0; r < nrows; ++r) {
     int64_t b = rows[3 * r], h = rows[3 * r + 1], qp = rows[3 * r + 2];
     if (b < 0 || b >= B || h < 0 || h >= Hq || qp < 0 || qp >= L) return -JLO_EINVAL;
@@ -279,7 +347,8 @@ int jlo_prefill_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v, in
       int64_t kstride = (int64_t)Hkv * d;
       const uint16_t* kbase = k + ((int64_t)b * L * Hkv + kvh) * d;
       const uint16_t* vbase = v + ((int64_t)b * L * Hkv + kvh) * d;
-      if (keyset_build(&ks, kbase, vbase, maxq + 1, d, kstride, G, theta, bifocal) != JLO_OK) {
+      if (keyset_build(&ks, kbase, vbase, maxq + 1, d, kstride, G, theta, bifocal, romega) !=
+          JLO_OK) {
         keyset_free(&ks);
         status = JLO_ENOMEM;
         break;
@@ -297,7 +366,7 @@ int jlo_prefill_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v, in
           int64_t h = rows[3 * r + 1], qp = rows[3 * r + 2];
           const uint16_t* qsrc = q + (((int64_t)b * L + qp) * Hq + h) * d;
           for (int c = 0; c < d; ++c) xq[c] = bf16_to_double(qsrc[c]);
-          double l = bifocal ? bifocal_row(xq, qp, G, w0, theta, &ks, out + r * d)
+          double l = bifocal ? bifocal_row(xq, qp, G, w0, theta, &ks, romega, out + r * d)
                              : rope_row(xq, qp, theta, &ks, out + r * d);
           if (lse) lse[r] = l;
         }
@@ -306,7 +375,16 @@ int jlo_prefill_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v, in
       keyset_free(&ks);
     }
   }
+  free(romega);
   return status == JLO_OK ? threads : -status;
+}
+
+/* Prefill rows with the aliasing remote map of Eq. (3). */
+int jlo_prefill_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v, int B, int Hq,
+                     int Hkv, int L, int d, double theta, int64_t w_pretrained, int64_t w0,
+                     int bifocal, const int64_t* rows, int64_t nrows, double* out, double* lse) {
+  return jlo_prefill_rows_map(q, k, v, B, Hq, Hkv, L, d, theta, w_pretrained, w0, bifocal, 0,
+                              rows, nrows, out, lse);
 }
 
 /*
@@ -334,7 +412,7 @@ int jlo_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
       int64_t kstride = (int64_t)Hkv * d;
       const uint16_t* kbase = k_cache + ((int64_t)b * max_len * Hkv + kvh) * d;
       const uint16_t* vbase = v_cache + ((int64_t)b * max_len * Hkv + kvh) * d;
-      if (keyset_build(&ks, kbase, vbase, n, d, kstride, G, theta, bifocal) != JLO_OK) {
+      if (keyset_build(&ks, kbase, vbase, n, d, kstride, G, theta, bifocal, NULL) != JLO_OK) {
         keyset_free(&ks);
         status = JLO_ENOMEM;
         break;
@@ -352,7 +430,7 @@ int jlo_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
           const uint16_t* qsrc = q + ((int64_t)b * Hq + h) * d;
           for (int c = 0; c < d; ++c) xq[c] = bf16_to_double(qsrc[c]);
           double* o = out + ((int64_t)b * Hq + h) * d;
-          double l = bifocal ? bifocal_row(xq, n - 1, G, w0, theta, &ks, o)
+          double l = bifocal ? bifocal_row(xq, n - 1, G, w0, theta, &ks, NULL, o)
                              : rope_row(xq, n - 1, theta, &ks, o);
           if (lse) lse[(int64_t)b * Hq + h] = l;
         }
@@ -379,7 +457,7 @@ int jlo_window_states(const uint16_t* q, const uint16_t* k, const uint16_t* v, i
   keyset_t ks;
   const uint16_t* kbase = k + ((int64_t)b * L * Hkv + kvh) * d;
   const uint16_t* vbase = v + ((int64_t)b * L * Hkv + kvh) * d;
-  if (keyset_build(&ks, kbase, vbase, qpos + 1, d, (int64_t)Hkv * d, G, theta, 1) != JLO_OK) {
+  if (keyset_build(&ks, kbase, vbase, qpos + 1, d, (int64_t)Hkv * d, G, theta, 1, NULL) != JLO_OK) {
     keyset_free(&ks);
     return -JLO_ENOMEM;
   }

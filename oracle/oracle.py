@@ -4,7 +4,8 @@ TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and the
 benchmark's CPU-baseline leg, never by the product path.  It shares no code
 with the HIP implementation.  Every function follows Jet-Long (arXiv
 2607.07740): Eq. (2) group size, Eq. (3) remote map, Eq. (1) two-window score,
-Sec. 3.3 three windows merged by Eq. (7), Sec. 3.2 decode on a raw cache.
+Sec. 3.3 three windows merged by Eq. (7), Sec. 3.2 decode on a raw cache, and
+the frequency-interpolation remote map of the Sec. 4.5 ablation.
 """
 from __future__ import annotations
 
@@ -46,6 +47,13 @@ def _load():
         lib.jlo_position_offset.argtypes = [i64, i64]
         lib.jlo_rope_rotate.restype = None
         lib.jlo_rope_rotate.argtypes = [vp, i32, dbl, dbl, vp]
+        lib.jlo_rope_rotate_freqs.restype = None
+        lib.jlo_rope_rotate_freqs.argtypes = [vp, i32, dbl, vp, vp]
+        lib.jlo_yarn_frequencies.restype = None
+        lib.jlo_yarn_frequencies.argtypes = [i32, dbl, dbl, dbl, dbl, dbl, vp]
+        lib.jlo_prefill_rows_map.restype = i32
+        lib.jlo_prefill_rows_map.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, dbl, i64, i64,
+                                             i32, i32, vp, i64, vp, vp]
         lib.jlo_prefill_rows.restype = i32
         lib.jlo_prefill_rows.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, dbl, i64, i64, i32,
                                          vp, i64, vp, vp]
@@ -95,17 +103,41 @@ def rope_rotate(x: np.ndarray, pos: float, theta: float) -> np.ndarray:
     return y
 
 
+def rope_rotate_freqs(x: np.ndarray, pos: float, omega: np.ndarray) -> np.ndarray:
+    """Rotate-half rotation of one fp64 vector with explicit frequencies omega [d/2]."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    omega = np.ascontiguousarray(omega, dtype=np.float64)
+    assert omega.shape == (x.shape[0] // 2,)
+    y = np.empty_like(x)
+    _load().jlo_rope_rotate_freqs(_ptr(x), x.shape[0], float(pos), _ptr(omega), _ptr(y))
+    return y
+
+
+def yarn_frequencies(d: int, theta: float, L: float, w_pretrained: float, alpha: float = 1.0,
+                     beta: float = 32.0) -> np.ndarray:
+    """Remote-view frequencies of the frequency-interpolation map (Sec. 4.5,
+    Table 6): YaRN's per-pair ramp with s = max(1, L / w_pretrained)."""
+    out = np.empty(d // 2, dtype=np.float64)
+    _load().jlo_yarn_frequencies(int(d), float(theta), float(L), float(w_pretrained),
+                                 float(alpha), float(beta), _ptr(out))
+    return out
+
+
+REMOTE_MAPS = {"alias": 0, "freq": 1}
+
+
 def max_threads() -> int:
     return int(_load().jlo_max_threads())
 
 
 def prefill_rows(q, k, v, rows, *, theta: float, w_pretrained: int = 1, w_local: int = 0,
-                 bifocal: bool = True, want_lse: bool = False):
+                 bifocal: bool = True, want_lse: bool = False, remote_map: str = "alias"):
     """Oracle output rows of a prefill call.
 
     q: uint16 [B, L, Hq, d]; k, v: uint16 [B, L, Hkv, d] (bf16 bits, raw pre-RoPE).
-    rows: int64 [n, 3] of (b, h, q).  Returns fp64 [n, d] (and fp64 [n] LSE),
-    plus the number of host threads the oracle used.
+    rows: int64 [n, 3] of (b, h, q).  remote_map: "alias" (Eq. (3)) or "freq"
+    (frequency interpolation, Sec. 4.5).  Returns fp64 [n, d] (and fp64 [n]
+    LSE), plus the number of host threads the oracle used.
     """
     q, k, v = _bf16(q), _bf16(k), _bf16(v)
     B, L, Hq, d = q.shape
@@ -114,10 +146,11 @@ def prefill_rows(q, k, v, rows, *, theta: float, w_pretrained: int = 1, w_local:
     rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3)
     out = np.empty((rows.shape[0], d), dtype=np.float64)
     lse = np.empty(rows.shape[0], dtype=np.float64) if want_lse else None
-    rc = _load().jlo_prefill_rows(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, L, d, float(theta),
-                                  int(w_pretrained), int(w_local), 1 if bifocal else 0,
-                                  _ptr(rows), rows.shape[0], _ptr(out),
-                                  _ptr(lse) if lse is not None else None)
+    rc = _load().jlo_prefill_rows_map(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, L, d,
+                                      float(theta), int(w_pretrained), int(w_local),
+                                      1 if bifocal else 0, REMOTE_MAPS[remote_map], _ptr(rows),
+                                      rows.shape[0], _ptr(out),
+                                      _ptr(lse) if lse is not None else None)
     if rc < 0:
         raise ValueError("oracle prefill_rows failed with status %d" % -rc)
     return (out, lse, rc) if want_lse else (out, rc)
@@ -129,12 +162,13 @@ def all_rows(B: int, Hq: int, L: int) -> np.ndarray:
 
 
 def prefill(q, k, v, *, theta: float, w_pretrained: int = 1, w_local: int = 0,
-            bifocal: bool = True):
+            bifocal: bool = True, remote_map: str = "alias"):
     """Full-tensor oracle prefill: fp64 [B, L, Hq, d] and LSE fp64 [B, Hq, L]."""
     B, L, Hq, d = q.shape
     rows = all_rows(B, Hq, L)
     out, lse, _ = prefill_rows(q, k, v, rows, theta=theta, w_pretrained=w_pretrained,
-                               w_local=w_local, bifocal=bifocal, want_lse=True)
+                               w_local=w_local, bifocal=bifocal, want_lse=True,
+                               remote_map=remote_map)
     o = out.reshape(B, Hq, L, d).transpose(0, 2, 1, 3).copy()
     return o, lse.reshape(B, Hq, L)
 

@@ -395,3 +395,105 @@ def test_prefill_rows_rejects_bad_arguments():
         O.prefill_rows(q, k, v, np.array([[0, 0, 8]]), theta=1e6, w_pretrained=4, w_local=1)
     with pytest.raises(ValueError):
         O.prefill_rows(q, k, v, np.array([[0, 0, 0]]), theta=1e6, w_pretrained=0, w_local=1)
+
+
+# ------------------------------ frequency-interpolation remote map (Sec. 4.5)
+def test_yarn_frequencies_regimes_at_the_128k_configuration():
+    """theta = 1e6, d = 128, w = 32768, L = 131072 (s = 4): pairs that turn more
+    than beta = 32 times inside the pretraining window keep RoPE's frequency,
+    pairs that turn less than alpha = 1 time are divided by s exactly, the
+    rest lie strictly between, and the result is monotone in the pair index."""
+    d, theta, w, L = 128, 1e6, 32768, 131072
+    om = O.yarn_frequencies(d, theta, L, w)
+    base = theta ** (-2.0 * np.arange(d // 2) / d)
+    turns = w * base / (2 * math.pi)
+    fast, slow = turns > 32, turns < 1
+    assert fast.sum() == 24 and slow.sum() == 24  # pairs 0..23 and 40..63
+    np.testing.assert_allclose(om[fast], base[fast], rtol=1e-15)
+    np.testing.assert_allclose(om[slow], base[slow] / 4, rtol=1e-15)
+    mid = ~fast & ~slow
+    assert np.all(om[mid] < base[mid]) and np.all(om[mid] > base[mid] / 4)
+    assert np.all(np.diff(om) < 0)
+
+
+def test_yarn_frequencies_identity_within_window_and_ramp_midpoint():
+    # s = 1 (L <= w): every frequency is RoPE's own
+    base = 1e6 ** (-2.0 * np.arange(64) / 128)
+    np.testing.assert_allclose(O.yarn_frequencies(128, 1e6, 32768, 32768), base, rtol=1e-15)
+    np.testing.assert_allclose(O.yarn_frequencies(128, 1e6, 1000, 32768), base, rtol=1e-15)
+    # d = 4, theta chosen so pair 1 completes 16.5 turns over w = 1000, the
+    # middle of the [1, 32] ramp: gamma = 1/2 and omega' = omega (1 + 1/s) / 2
+    w = 1000.0
+    theta = (w / (2 * math.pi * 16.5)) ** 2
+    om = O.yarn_frequencies(4, theta, 2500, w)  # s = 2.5 (continuous, not G = 3)
+    w1 = theta ** -0.5
+    assert om[0] == 1.0  # 159 turns: fast pair unchanged
+    assert om[1] == pytest.approx(w1 * (1 + 1 / 2.5) / 2, rel=1e-12)
+
+
+def test_freq_map_with_every_pair_slow_is_position_interpolation():
+    """w = 4, d = 8: every pair turns less than once over the window, so the
+    remote rotation is RoPE at the fractional position x / s (linear position
+    interpolation).  The oracle's bifocal output must equal Eq. (1) evaluated
+    with remote scores at positions q / s, k / s."""
+    B, Hq, Hkv, L, d, theta, w, w0 = 1, 2, 1, 26, 8, 10.0, 4, 3  # s = 6.5, not G = 7
+    q, k, v = synth.prefill_inputs(B, Hq, Hkv, L, d, seed=9)
+    qf, kf, vf = _f64(q), _f64(k), _f64(v)
+    s = L / w
+    pos = np.arange(L)
+    qq, kk = np.meshgrid(pos, pos, indexing="ij")
+    local = (kk <= qq) & (qq - kk <= w0)
+    remote = (kk <= qq) & (qq - kk > w0)
+    want = np.empty_like(qf)
+    for h in range(Hq):
+        S = np.full((L, L), -np.inf)
+        S[local] = (_complex_rope(qf[0, :, h], pos, theta) @ _complex_rope(kf[0, :, 0], pos, theta).T)[local]
+        S[remote] = (_complex_rope(qf[0, :, h], pos / s, theta) @ _complex_rope(kf[0, :, 0], pos / s, theta).T)[remote]
+        S /= math.sqrt(d)
+        P = np.exp(S - S.max(axis=1, keepdims=True))
+        want[0, :, h] = (P / P.sum(axis=1, keepdims=True)) @ vf[0, :, 0]
+    got, _ = O.prefill(q, k, v, theta=theta, w_pretrained=w, w_local=w0, remote_map="freq")
+    assert np.max(np.abs(got - want)) < 1e-12
+    alias, _ = O.prefill(q, k, v, theta=theta, w_pretrained=w, w_local=w0)
+    assert np.max(np.abs(got - alias)) > 1e-3  # a different map
+
+
+def test_freq_map_with_every_pair_fast_is_vanilla():
+    """theta = 100, d = 4, w = 2100: both pairs turn more than 32 times over
+    the window, so the remote rotation is the base one and the bifocal output
+    is plain causal RoPE attention, while the aliasing map is not."""
+    B, Hq, Hkv, L, d, theta, w, w0 = 1, 2, 1, 2300, 4, 100.0, 2100, 50
+    q, k, v = synth.prefill_inputs(B, Hq, Hkv, L, d, seed=4)
+    rows = np.array([[0, h, x] for h in range(Hq) for x in (0, 51, 700, 2101, 2299)])
+    got, _ = O.prefill_rows(q, k, v, rows, theta=theta, w_pretrained=w, w_local=w0,
+                            remote_map="freq")
+    van, _ = O.prefill_rows(q, k, v, rows, theta=theta, bifocal=False)
+    assert np.max(np.abs(got - van)) < 1e-12
+    alias, _ = O.prefill_rows(q, k, v, rows, theta=theta, w_pretrained=w, w_local=w0)
+    assert np.max(np.abs(alias - van)) > 1e-3
+
+
+def test_freq_map_literal_merge_equals_mask_form():
+    """The Eq. (7) merge with the frequency map equals Eq. (1) with the
+    remote scores rotated by the interpolated frequencies (L = 300, w = 64)."""
+    B, Hq, Hkv, L, d, theta, w, w0 = 1, 2, 1, 300, 16, 1e4, 64, 20
+    q, k, v = synth.prefill_inputs(B, Hq, Hkv, L, d, seed=21, outlier_channels=2)
+    qf, kf, vf = _f64(q), _f64(k), _f64(v)
+    om = O.yarn_frequencies(d, theta, L, w)
+    h2 = d // 2
+    rot = lambda x, p: np.concatenate(
+        [((x[:, :h2] + 1j * x[:, h2:]) * np.exp(1j * p[:, None] * om)).real,
+         ((x[:, :h2] + 1j * x[:, h2:]) * np.exp(1j * p[:, None] * om)).imag], axis=1)
+    pos = np.arange(L)
+    qq, kk = np.meshgrid(pos, pos, indexing="ij")
+    local = (kk <= qq) & (qq - kk <= w0)
+    remote = (kk <= qq) & (qq - kk > w0)
+    got, _ = O.prefill(q, k, v, theta=theta, w_pretrained=w, w_local=w0, remote_map="freq")
+    for h in range(Hq):
+        S = np.full((L, L), -np.inf)
+        S[local] = (_complex_rope(qf[0, :, h], pos, theta) @ _complex_rope(kf[0, :, 0], pos, theta).T)[local]
+        S[remote] = (rot(qf[0, :, h], pos) @ rot(kf[0, :, 0], pos).T)[remote]
+        S /= math.sqrt(d)
+        P = np.exp(S - S.max(axis=1, keepdims=True))
+        want = (P / P.sum(axis=1, keepdims=True)) @ vf[0, :, 0]
+        assert np.max(np.abs(got[0, :, h] - want)) < 1e-11
