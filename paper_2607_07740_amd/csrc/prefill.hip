@@ -34,19 +34,19 @@
 // (64 KB of LDS each), so every SIMD runs two waves.  A wave owns 32 rows; a
 // lane owns one query column of S^T = K Q^T (v_mfma_f32_32x32x16_bf16, lanes l
 // and l + 32 split the column's 16 accumulator rows), and O^T += V^T P^T takes
-// P^T straight from the S^T accumulator registers.  Tiles of 64 keys are
-// double-buffered: all four waves copy their quarter of tile j+1 into LDS
-// while tile j is computed.  The O^T accumulator (4 x 16 fp32 per lane) stays
-// in VGPRs.
+// P^T straight from the S^T accumulator registers.  K images and V^T images
+// of 64-key tiles are double-buffered separately.  The loop is software
+// pipelined: while the softmax of tile j runs on the VALU, the QK product of
+// tile j+1 is already on the matrix cores, followed by PV of tile j; all four
+// waves copy their quarter of K(j+2) and V(j+1) into LDS meanwhile.  The O^T
+// accumulator (4 x 16 fp32 per lane) stays in VGPRs, and each segment's loop
+// is unrolled twice so the two score buffers alternate without copies.
 //
-// Softmax runs in the log2 domain against a per-row reference m (initially 0).
-// -m enters the MFMA itself as one extra k-step (a constant A operand with a
-// single 1 against a B operand holding -m), so scores come out shifted and
-// the common path is exp2, convert and a dot product for the row sum.  The
-// reference moves only when a tile's sum leaves [2^-64, 2^64] before anything
-// was accumulated, or exceeds 2^64 later (a rare branch that recomputes the
-// tile against the new maximum and rescales the state).  m is kept
-// representable in bf16 so that its operand is exact.
+// Softmax runs in the log2 domain against a per-row reference m (initially 0):
+// the common path is subtract, exp2, convert and a dot product for the row
+// sum.  The reference moves only when a tile's sum leaves [2^-64, 2^64]
+// before anything was accumulated, or exceeds 2^64 later (a rare branch that
+// recomputes the tile against the new maximum and rescales the state).
 #include <climits>
 #include <type_traits>
 
@@ -212,8 +212,6 @@ __device__ inline void load_q_operand(const uint16_t* qrow, int half, const floa
   }
 }
 
-__device__ inline float round_to_bf16(float x) { return (float)(__bf16)x; }
-
 // Row sum of 8 bf16 probabilities (one P^T operand) added to acc.
 __device__ inline float sum8(bf16x8 p, float acc) {
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -236,6 +234,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   constexpr bool REMOTE2 = MODE == kModeWinB || MODE == kModeWinC;  // segment 2's view
   constexpr bool OUT_F32 = MODE == kModeWinA || MODE == kModeWinB || MODE == kModeWinC;
   constexpr bool FROM_ZERO = MODE == kModeVanilla || MODE == kModeWinB;  // kt_l = 0
+  // LDS: K images in [0, 32K) (two buffers), V^T images in [32K, 64K) (two buffers)
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmemBytes];
 
   const int tid = threadIdx.x;
@@ -280,53 +279,50 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const int kt_l = FROM_ZERO ? 0 : vr.kt_l;
   const int n_steps = n_r + (n_kt - kt_l);
 
-  // ---- staging: each wave copies its quarter (4 KB) of visit j's K image
-  // (k_rem or k_loc) and V^T image into buffer j & 1
+  // ---- staging: each wave copies its quarter (4 KB) of a K image (k_rem or
+  // k_loc) or a V^T image into buffer j & 1 of that kind
   const size_t img_base = (size_t)group * a.n_tiles * (kTileBytes / 2);
   const uint32_t smem_base = lds_addr(smem);
   const uint32_t lane_off = 16 * lane;
-  auto issue = [&](int j) {
-    const bool seg1 = j < n_r;
-    const int kt = seg1 ? j : kt_l + (j - n_r);
-    const size_t off = img_base + (size_t)kt * (kTileBytes / 2) + wave * 2048;
-    const bool use_rem = REMOTE2 || (FUSED && seg1);
+  auto tile_of = [&](int j) __attribute__((always_inline)) { return j < n_r ? j : kt_l + (j - n_r); };
+  auto issue_k = [&](int j) __attribute__((always_inline)) {
+    const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * 2048;
+    const bool use_rem = REMOTE2 || (FUSED && j < n_r);
     const unsigned char* gk = (const unsigned char*)((use_rem ? a.krem : a.kloc) + off);
-    const unsigned char* gv = (const unsigned char*)(a.vt + off);
-    const uint32_t lk = smem_base + (j & 1) * 2 * kTileBytes + wave * 4096;
-    const uint32_t lv = lk + kTileBytes;
+    const uint32_t lk = smem_base + (j & 1) * kTileBytes + wave * 4096;
     dma16_s<0>(gk, lane_off, lk);
     dma16_s<1024>(gk, lane_off, lk);
     dma16_s<2048>(gk, lane_off, lk);
     dma16_s<3072>(gk, lane_off, lk);
+  };
+  auto issue_v = [&](int j) __attribute__((always_inline)) {
+    const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * 2048;
+    const unsigned char* gv = (const unsigned char*)(a.vt + off);
+    const uint32_t lv = smem_base + 2 * kTileBytes + (j & 1) * kTileBytes + wave * 4096;
     dma16_s<0>(gv, lane_off, lv);
     dma16_s<1024>(gv, lane_off, lv);
     dma16_s<2048>(gv, lane_off, lv);
     dma16_s<3072>(gv, lane_off, lv);
   };
+  auto kbuf = [&](int j) __attribute__((always_inline)) { return (const unsigned char*)smem + (j & 1) * kTileBytes; };
+  auto vbuf = [&](int j) __attribute__((always_inline)) { return (const unsigned char*)smem + (2 + (j & 1)) * kTileBytes; };
 
-  // ---- query operand of the first view, state
+  // ---- state.  Scores are log2-domain (q_scale folded into Q); the
+  // probabilities are exp2(s - m_ref) against a per-row reference m_ref that
+  // moves only on the rare path below.
   bf16x8 qop[8];
-  load_q_operand(qrow, hl32, a.table, (n_r > 0 || REMOTE2) ? remote_pos(qp, a.gdiv) : qp,
-                 a.q_scale, qop);
-
   f32x16 acc_o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) acc_o[i] = f32x16{};
-  float m_ref = 0.f;  // reference (log2 units), bf16-exact; -m is the offset operand
+  float m_ref = 0.f;
   float l_run = 0.f;
-  // extra k-step operands adding -m to every score of a column: A holds a single
-  // 1 (row k = 0 of the step, lanes 0..31), B holds -m in the same k row
-  bf16x8 a_one = bf16x8{};
-  if (hl32 == 0) a_one[0] = (__bf16)1.0f;
-  bf16x8 b_off = bf16x8{};
-
-  issue(0);
+  f32x16 sc_a[2], sc_b[2];
 
   const int kr_lane = lane & 31;
-  // S^T - m: 2 blocks of 32 keys, the offset k-step + 8 k-steps each, K
-  // operands read 4 MFMAs ahead
-  auto qk = [&](const unsigned char* kb, f32x16* sc) {
-    auto kop = [&](int m) {
+  // S^T = K Q^T for one tile: 2 blocks of 32 keys x 8 k-steps, K operands
+  // read 4 MFMAs ahead
+  auto qk = [&](const unsigned char* kb, f32x16* sc) __attribute__((always_inline)) {
+    auto kop = [&](int m) __attribute__((always_inline)) {
       const int r = 32 * (m >> 3) + kr_lane;
       return *(const bf16x8*)(kb + kimg_off(r, 2 * (m & 7) + hl32));
     };
@@ -336,15 +332,14 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int m = 0; m < 16; ++m) {
       const int blk = m >> 3, s = m & 7;
-      if (s == 0) sc[blk] = mfma32(a_one, b_off, f32x16{});
-      sc[blk] = mfma32(ring[m & 3], qop[s], sc[blk]);
+      sc[blk] = mfma32(ring[m & 3], qop[s], s == 0 ? f32x16{} : sc[blk]);
       if (m + 4 < 16) ring[m & 3] = kop(m + 4);
     }
   };
   // O^T += V^T P^T: 4 k-steps of 16 keys x 4 d-blocks of 32, V^T operands
   // read 4 MFMAs ahead
-  auto pv = [&](const unsigned char* vb, const bf16x8* pb) {
-    auto vop = [&](int m) {
+  auto pv = [&](const unsigned char* vb, const bf16x8* pb) __attribute__((always_inline)) {
+    auto vop = [&](int m) __attribute__((always_inline)) {
       const int d = 32 * (m & 3) + kr_lane;
       return *(const bf16x8*)(vb + vtimg_off(d, 2 * (m >> 2) + hl32));
     };
@@ -358,28 +353,38 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
   };
 
-  // element masks where the tile is not wholly inside the visit's key set
-  auto mask = [&](int k0, bool seg1, f32x16* sc) {
+  // element masks where tile j is not wholly inside its visit's key set
+  auto need_mask = [&](int j) __attribute__((always_inline)) {
+    const int k0 = tile_of(j) * kPfBK;
+    return j < n_r ? !(q0 - (k0 + kPfBK - 1) > w0) : !(q1 - k0 <= w0 && k0 + kPfBK - 1 <= q0);
+  };
+  auto mask = [&](int j, f32x16* sc) __attribute__((always_inline)) {
+    // keep iff lo <= q - k <= hi: segment 1 keeps q - k > w0, segment 2
+    // keeps 0 <= q - k <= w0; one unsigned compare per element
+    const bool seg1 = j < n_r;
+    const int k0 = tile_of(j) * kPfBK;
+    const int lo = seg1 ? w0 + 1 : 0;
+    const uint32_t span = seg1 ? (uint32_t)(INT_MAX - lo) : (uint32_t)w0;
+    const int base = qp - k0 - lo - 4 * hl32;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int diff = qp - (k0 + 32 * blk + 8 * (i >> 2) + 4 * hl32 + (i & 3));
-        const bool keep = seg1 ? diff > w0 : (diff >= 0 && diff <= w0);
-        sc[blk][i] = keep ? sc[blk][i] : -INFINITY;
+        const uint32_t off = (uint32_t)(base - (32 * blk + 8 * (i >> 2) + (i & 3)));
+        sc[blk][i] = off <= span ? sc[blk][i] : -INFINITY;
       }
     }
   };
 
-  // fast softmax: exp2 against the current reference, P^T operands and their
-  // row sum (of the rounded probabilities the PV product uses)
-  auto softmax = [&](const f32x16* sc, bf16x8* pb) {
+  // P^T operands and their row sum (of the rounded probabilities that the PV
+  // product uses) against the reference m
+  auto softmax = [&](const f32x16* sc, float m, bf16x8* pb) __attribute__((always_inline)) {
     float psum = 0.f;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       float p[8];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) p[t] = fast_exp2(sc[q >> 1][8 * (q & 1) + t]);
+      for (int t = 0; t < 8; ++t) p[t] = fast_exp2(sc[q >> 1][8 * (q & 1) + t] - m);
       pb[q] = pack8(p);
       psum = sum8(pb[q], psum);
     }
@@ -389,7 +394,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // move the reference to the tile maximum where the sum overflowed, or where
   // nothing was accumulated yet and the sum underflowed; recompute P and
   // rescale the running state.
-  auto softmax_fix = [&](const f32x16* sc, bf16x8* pb, float& psum) {
+  auto softmax_fix = [&](const f32x16* sc, bf16x8* pb, float& psum) __attribute__((always_inline)) {
     const bool bad = !(psum <= a.sum_hi) || (l_run == 0.f && psum < kSumLo);
     if (__ballot(bad) == 0) return;
     float mt = -INFINITY;
@@ -401,17 +406,9 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     const float ps = psum + __shfl_xor(psum, 32);
     const float lc = l_run + __shfl_xor(l_run, 32);
     const bool upd = mt != -INFINITY && (!(ps <= a.sum_hi) || (lc == 0.f && ps < kSumLo));
-    const float m_new = upd ? round_to_bf16(m_ref + mt) : m_ref;
+    const float m_new = upd ? mt : m_ref;
     const float shift = m_new - m_ref;
-    psum = 0.f;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float p[8];
-#pragma unroll
-      for (int t = 0; t < 8; ++t) p[t] = fast_exp2(sc[q >> 1][8 * (q & 1) + t] - shift);
-      pb[q] = pack8(p);
-      psum = sum8(pb[q], psum);
-    }
+    psum = softmax(sc, m_new, pb);
     // a downward move only happens before anything was accumulated (lc == 0),
     // where 2^-shift may overflow and must not touch l and O
     const float alpha = lc == 0.f ? 1.f : fast_exp2(-shift);
@@ -421,46 +418,53 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
     l_run *= alpha;
     m_ref = m_new;
-    if (hl32 == 0) b_off[0] = (__bf16)(-m_new);
   };
 
-  // one visit of tile j in one view
-  auto step = [&](int j, auto seg1_tag, auto mask_tag) {
-    constexpr bool seg1 = decltype(seg1_tag)::value;
-    constexpr bool MASKED = decltype(mask_tag)::value;
-    const int k0 = (seg1 ? j : kt_l + (j - n_r)) * kPfBK;
-    const unsigned char* kb = smem + (j & 1) * 2 * kTileBytes;
-    const unsigned char* vb = kb + kTileBytes;
-    f32x16 sc[2];
+  // One pipelined visit: on entry `cur` holds the scores of tile j, this
+  // wave's copies of K(j+1) and V(j) are in flight.  The QK product of tile
+  // j+1 is issued next to the softmax of tile j, then PV of tile j; K(j+2)
+  // and V(j+1) are copied meanwhile.  For the last tile of a segment the
+  // QK product reads whatever the next K buffer holds and is discarded.
+  auto visit = [&](int j, f32x16* cur, f32x16* nxt) __attribute__((always_inline)) {
+    if (need_mask(j)) mask(j, cur);
+    wait_vmem();      // this wave's copies of K(j+1), V(j)
+    __syncthreads();  // everyone's; QK(j) and PV(j-1) are done everywhere
+    if (j + 2 < n_steps) issue_k(j + 2);
+    if (j + 1 < n_steps) issue_v(j + 1);
     bf16x8 pb[4];
-
-    wait_vmem();      // this wave's copies of tile j
-    __syncthreads();  // everyone's copies of tile j; buffer (j+1) & 1 is free
-    if (j + 1 < n_steps) issue(j + 1);
-    qk(kb, sc);
-    if (MASKED) mask(k0, seg1, sc);
-    float psum = softmax(sc, pb);
-    softmax_fix(sc, pb, psum);
+    qk(kbuf(j + 1), nxt);
+    float psum = softmax(cur, m_ref, pb);
+    softmax_fix(cur, pb, psum);
     l_run += psum;
-    pv(vb, pb);
+    pv(vbuf(j), pb);
+  };
+  // segment [j, jend): the first tile's scores are in sc_a on entry
+  auto segment = [&](int j, int jend) __attribute__((always_inline)) {
+    for (; j + 2 <= jend; j += 2) {
+      visit(j, sc_a, sc_b);
+      visit(j + 1, sc_b, sc_a);
+    }
+    if (j < jend) visit(j, sc_a, sc_b);
   };
 
-  auto run = [&](int j, auto seg1_tag) {
-    constexpr bool seg1 = decltype(seg1_tag)::value;
-    const int k0 = (seg1 ? j : kt_l + (j - n_r)) * kPfBK;
-    const bool need_mask = seg1 ? !(q0 - (k0 + kPfBK - 1) > w0)
-                                : !(q1 - k0 <= w0 && k0 + kPfBK - 1 <= q0);
-    if (need_mask)
-      step(j, seg1_tag, std::true_type{});
-    else
-      step(j, seg1_tag, std::false_type{});
-  };
+  // ---- prologue: the first view's query operand, K(0), V(0), K(1)
+  load_q_operand(qrow, hl32, a.table, (n_r > 0 || REMOTE2) ? remote_pos(qp, a.gdiv) : qp,
+                 a.q_scale, qop);
+  issue_k(0);
+  issue_v(0);
+  if (n_steps > 1) issue_k(1);
+  wait_vmem();
+  __syncthreads();
+  qk(kbuf(0), sc_a);
 
-  if (FUSED) {
-    for (int j = 0; j < n_r; ++j) run(j, std::true_type{});
-    if (n_r > 0) load_q_operand(qrow, hl32, a.table, qp, a.q_scale, qop);
+  if (FUSED && n_r > 0) {
+    segment(0, n_r);
+    // segment 2 in the base view: its first tile's K image (in buffer n_r & 1,
+    // not overwritten since) is scored again with the base-rotated operand
+    load_q_operand(qrow, hl32, a.table, qp, a.q_scale, qop);
+    qk(kbuf(n_r), sc_a);
   }
-  for (int j = n_r; j < n_steps; ++j) run(j, std::false_type{});
+  segment(n_r, n_steps);
 
   // ---- normalise and write
   const float l_tot = l_run + __shfl_xor(l_run, 32);
