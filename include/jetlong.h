@@ -196,9 +196,10 @@ int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_
 
 /*
  * Debug knob for tests, process-wide: the prefill kernels move a row's softmax
- * reference (and rescale the running output) when a key tile's row sum
- * exceeds 2^log2_bound; the default is 64, far from anything ordinary data
- * reaches.  A small bound (e.g. 3) makes the rescale path run on almost every
+ * reference (and rescale the running output) when a key tile's largest score
+ * in that row exceeds the reference by more than log2_bound (scores in log2
+ * units), or lies more than log2_bound below it before anything was
+ * accumulated; the default is 64, far from anything ordinary data reaches.  A small bound (e.g. 3) makes the rescale path run on almost every
  * tile of ordinary inputs, which tests use to check it.  Values outside
  * [1, 100] leave the setting unchanged.  Returns the previous value.  Not for
  * use while prefill calls are in flight.

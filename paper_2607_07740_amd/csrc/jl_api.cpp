@@ -20,12 +20,12 @@ namespace jl {
 size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L);
 hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                           uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
-                          int L, int G, int w0, float sum_hi, void* ws, hipStream_t stream,
+                          int L, int G, int w0, float slack, void* ws, hipStream_t stream,
                           hipEvent_t ev0, hipEvent_t ev1);
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L);
 hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                   uint16_t* o, float* lse, const float2* table, int B, int Hq,
-                                  int Hkv, int L, int G, int w0, float sum_hi, void* ws,
+                                  int Hkv, int L, int G, int w0, float slack, void* ws,
                                   hipStream_t stream);
 int prefill_rows_per_block();
 int prefill_block_q(int g);
@@ -47,8 +47,9 @@ namespace {
 
 constexpr int kHeadDim = 128;
 thread_local std::string t_detail;
-// log2 of the prefill row-sum bound that moves the softmax reference; the
-// debug entry lowers it so tests can drive the rescale path on ordinary data
+// how far (log2 units) a prefill tile's score maximum may lie from the softmax
+// reference before the reference moves; the debug entry lowers it so tests
+// can drive the rescale path on ordinary data
 std::atomic<double> g_rescale_log2{64.0};
 // benchmark timing hook: events recorded around the prefill attention kernel
 // ([0]) and the decode split kernel ([1]); null when unset
@@ -232,12 +233,12 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   // G == 1: f is the identity and the method is the base model (Sec. 3), so
   // the bifocal entry runs the vanilla kernel and matches it bit for bit.
   const bool use_bifocal = bifocal && G > 1;
-  const float sum_hi = (float)std::exp2(g_rescale_log2.load());
+  const float slack = (float)g_rescale_log2.load();
   if (literal) {
     if (use_bifocal) {
       hipError_t e = jl::launch_prefill_literal((const uint16_t*)q, (const uint16_t*)k,
                                                 (const uint16_t*)v, (uint16_t*)o, lse, table, B,
-                                                Hq, Hkv, L, G, w0, sum_hi, ws, s);
+                                                Hq, Hkv, L, G, w0, slack, ws, s);
       if (e != hipSuccess) return hip_fail(e, "literal prefill launch");
       return ok();
     }
@@ -250,7 +251,7 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   timing_events(0, &ev0, &ev1);
   hipError_t e = jl::launch_prefill(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,
                                     (const uint16_t*)v, (uint16_t*)o, lse, table, B, Hq, Hkv, L,
-                                    G, w0, sum_hi, scratch, s, ev0, ev1);
+                                    G, w0, slack, scratch, s, ev0, ev1);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   return ok();
 }

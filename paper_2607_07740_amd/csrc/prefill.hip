@@ -42,11 +42,13 @@
 // accumulator (4 x 16 fp32 per lane) stays in VGPRs, and each segment's loop
 // is unrolled twice so the two score buffers alternate without copies.
 //
-// Softmax runs in the log2 domain against a per-row reference m (initially 0):
-// the common path is subtract, exp2, convert and a dot product for the row
-// sum.  The reference moves only when a tile's sum leaves [2^-64, 2^64]
-// before anything was accumulated, or exceeds 2^64 later (a rare branch that
-// recomputes the tile against the new maximum and rescales the state).
+// Softmax runs in the log2 domain against a per-row reference m (initially 0)
+// that the QK product subtracts itself: its first k-step accumulates onto -m.
+// The common path is exp2, convert and a dot product for the row sum.  Before
+// a tile's softmax the reference is checked against the tile's largest score;
+// it moves only when that score lies more than 64 above it, or (before
+// anything was accumulated) more than 64 below it, a rare branch that re-bases
+// the tile and rescales the state.  So every probability stays below 2^64.
 #include <climits>
 #include <type_traits>
 
@@ -59,7 +61,6 @@ constexpr int kPfRows = 128;     // query rows per workgroup: 32 per wave
 constexpr int kPfBK = 64;        // keys per tile
 constexpr int kTileBytes = kPfBK * kHeadDim * 2;  // one K image or one V^T image: 16 KB
 constexpr int kSmemBytes = 2 * 2 * kTileBytes;    // double-buffered K + V^T: 64 KB
-constexpr float kSumLo = 5.421010862427522e-20f;    // 2^-64
 
 // Tile images (byte layout, also the LDS layout):
 //   K image:   key r (0..63) at r * 256; its 16-byte chunk c (d = 8c .. 8c+7)
@@ -173,7 +174,8 @@ struct PrefillArgs {
   int w0;         // local window; INT_MAX for the vanilla kernel and window B
   FastDiv gdiv;   // division by G (Eq. (3))
   float q_scale;  // log2(e) / sqrt(head_dim): scores come out in log2 units
-  float sum_hi;   // a tile's row sum above this moves the reference (2^64)
+  float slack;    // log2 units a tile maximum may lie above (or, before anything
+                  // was accumulated, below) the reference before it moves (64)
   float* o32;     // window passes: normalised fp32 O_X [B][L][Hq][128]
 };
 
@@ -307,32 +309,36 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   auto kbuf = [&](int j) __attribute__((always_inline)) { return (const unsigned char*)smem + (j & 1) * kTileBytes; };
   auto vbuf = [&](int j) __attribute__((always_inline)) { return (const unsigned char*)smem + (2 + (j & 1)) * kTileBytes; };
 
-  // ---- state.  Scores are log2-domain (q_scale folded into Q); the
-  // probabilities are exp2(s - m_ref) against a per-row reference m_ref that
-  // moves only on the rare path below.
+  // ---- state.  Scores are log2-domain (q_scale folded into Q) and come out
+  // of the MFMA already relative to a per-row reference m_ref: the first
+  // k-step of every QK product accumulates onto neg_m = -m_ref in each entry
+  // (all 16 accumulator entries of a lane belong to its query column).  The
+  // reference moves only on the rare path below.
   bf16x8 qop[8];
   f32x16 acc_o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) acc_o[i] = f32x16{};
   float m_ref = 0.f;
+  f32x16 neg_m = f32x16{};
   float l_run = 0.f;
   f32x16 sc_a[2], sc_b[2];
 
   const int kr_lane = lane & 31;
-  // S^T = K Q^T for one tile: 2 blocks of 32 keys x 8 k-steps, K operands
-  // read 4 MFMAs ahead
+  // S^T = K Q^T for one tile: 2 blocks of 32 keys x 8 k-steps.  The two
+  // blocks' accumulation chains alternate so that consecutive MFMAs are
+  // independent; K operands are read 4 MFMAs ahead.
   auto qk = [&](const unsigned char* kb, f32x16* sc) __attribute__((always_inline)) {
     auto kop = [&](int m) __attribute__((always_inline)) {
-      const int r = 32 * (m >> 3) + kr_lane;
-      return *(const bf16x8*)(kb + kimg_off(r, 2 * (m & 7) + hl32));
+      const int r = 32 * (m & 1) + kr_lane;
+      return *(const bf16x8*)(kb + kimg_off(r, 2 * (m >> 1) + hl32));
     };
     bf16x8 ring[4];
 #pragma unroll
     for (int m = 0; m < 4; ++m) ring[m] = kop(m);
 #pragma unroll
     for (int m = 0; m < 16; ++m) {
-      const int blk = m >> 3, s = m & 7;
-      sc[blk] = mfma32(ring[m & 3], qop[s], s == 0 ? f32x16{} : sc[blk]);
+      const int blk = m & 1, s = m >> 1;
+      sc[blk] = mfma32(ring[m & 3], qop[s], s == 0 ? neg_m : sc[blk]);
       if (m + 4 < 16) ring[m & 3] = kop(m + 4);
     }
   };
@@ -377,47 +383,50 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   };
 
   // P^T operands and their row sum (of the rounded probabilities that the PV
-  // product uses) against the reference m
-  auto softmax = [&](const f32x16* sc, float m, bf16x8* pb) __attribute__((always_inline)) {
+  // product uses); the scores are already relative to the reference
+  auto softmax = [&](const f32x16* sc, bf16x8* pb) __attribute__((always_inline)) {
     float psum = 0.f;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       float p[8];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) p[t] = fast_exp2(sc[q >> 1][8 * (q & 1) + t] - m);
+      for (int t = 0; t < 8; ++t) p[t] = fast_exp2(sc[q >> 1][8 * (q & 1) + t]);
       pb[q] = pack8(p);
       psum = sum8(pb[q], psum);
     }
     return psum;
   };
-  // Rare path: some column's sum left range.  Per column (both lane halves),
-  // move the reference to the tile maximum where the sum overflowed, or where
-  // nothing was accumulated yet and the sum underflowed; recompute P and
-  // rescale the running state.
-  auto softmax_fix = [&](const f32x16* sc, bf16x8* pb, float& psum) __attribute__((always_inline)) {
-    const bool bad = !(psum <= a.sum_hi) || (l_run == 0.f && psum < kSumLo);
-    if (__ballot(bad) == 0) return;
+  // Reference check, before the tile's softmax: the reference moves when
+  // the tile's largest (relative) score in a column exceeds it by more than
+  // the slack (exp2 could overflow), or, before anything was accumulated,
+  // lies more than the slack below it (everything could underflow).  The
+  // common path is a per-lane maximum and one ballot; the rare path settles
+  // each column (both lane halves), re-bases the tile's scores and rescales
+  // the running state.
+  auto ref_check = [&](f32x16* sc) __attribute__((always_inline)) {
     float mt = -INFINITY;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mt = fmaxf(mt, sc[blk][i]);
+    const bool bad = mt > a.slack || (l_run == 0.f && mt < -a.slack && mt != -INFINITY);
+    if (__ballot(bad) == 0) return;
     mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float ps = psum + __shfl_xor(psum, 32);
     const float lc = l_run + __shfl_xor(l_run, 32);
-    const bool upd = mt != -INFINITY && (!(ps <= a.sum_hi) || (lc == 0.f && ps < kSumLo));
-    const float m_new = upd ? mt : m_ref;
-    const float shift = m_new - m_ref;
-    psum = softmax(sc, m_new, pb);
-    // a downward move only happens before anything was accumulated (lc == 0),
-    // where 2^-shift may overflow and must not touch l and O
+    const bool upd = mt != -INFINITY && (mt > a.slack || (lc == 0.f && mt < -a.slack));
+    const float shift = upd ? mt : 0.f;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) sc[blk] -= shift;
+    // a downward move only happens before anything was accumulated (lc == 0)
     const float alpha = lc == 0.f ? 1.f : fast_exp2(-shift);
     if (__ballot(upd && lc != 0.f) != 0) {
 #pragma unroll
       for (int db = 0; db < 4; ++db) acc_o[db] *= alpha;
     }
     l_run *= alpha;
-    m_ref = m_new;
+    m_ref += shift;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) neg_m[i] = -m_ref;
   };
 
   // One pipelined visit: on entry `cur` holds the scores of tile j, this
@@ -427,15 +436,14 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // QK product reads whatever the next K buffer holds and is discarded.
   auto visit = [&](int j, f32x16* cur, f32x16* nxt) __attribute__((always_inline)) {
     if (need_mask(j)) mask(j, cur);
+    ref_check(cur);
     wait_vmem();      // this wave's copies of K(j+1), V(j)
     __syncthreads();  // everyone's; QK(j) and PV(j-1) are done everywhere
     if (j + 2 < n_steps) issue_k(j + 2);
     if (j + 1 < n_steps) issue_v(j + 1);
     bf16x8 pb[4];
     qk(kbuf(j + 1), nxt);
-    float psum = softmax(cur, m_ref, pb);
-    softmax_fix(cur, pb, psum);
-    l_run += psum;
+    l_run += softmax(cur, pb);
     pv(vbuf(j), pb);
   };
   // segment [j, jend): the first tile's scores are in sc_a on entry
@@ -580,7 +588,7 @@ static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v
   return hipGetLastError();
 }
 
-static void fill_geometry(PrefillArgs& a, int B, int Hq, int Hkv, int L, float sum_hi) {
+static void fill_geometry(PrefillArgs& a, int B, int Hq, int Hkv, int L, float slack) {
   a.B = B;
   a.Hq = Hq;
   a.Hkv = Hkv;
@@ -589,7 +597,7 @@ static void fill_geometry(PrefillArgs& a, int B, int Hq, int Hkv, int L, float s
   a.BQ = kPfRows / a.g;
   a.n_qblocks = (L + a.BQ - 1) / a.BQ;
   a.q_scale = 1.4426950408889634f / sqrtf((float)kHeadDim);
-  a.sum_hi = sum_hi;
+  a.slack = slack;
 }
 
 static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream) {
@@ -610,10 +618,10 @@ static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream
 // ev0 / ev1 (optional) are recorded on the stream around the attention kernel.
 hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                           uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
-                          int L, int G, int w0, float sum_hi, void* ws, hipStream_t stream,
+                          int L, int G, int w0, float slack, void* ws, hipStream_t stream,
                           hipEvent_t ev0, hipEvent_t ev1) {
   PrefillArgs a = {};
-  fill_geometry(a, B, Hq, Hkv, L, sum_hi);
+  fill_geometry(a, B, Hq, Hkv, L, slack);
   hipError_t e = launch_prep(bifocal, k, v, table, B, Hkv, L, G, ws, a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
@@ -629,7 +637,7 @@ hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, co
 // Eq. (7) taken literally: the three window passes, then the merge.
 hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                   uint16_t* o, float* lse, const float2* table, int B, int Hq,
-                                  int Hkv, int L, int G, int w0, float sum_hi, void* ws,
+                                  int Hkv, int L, int G, int w0, float slack, void* ws,
                                   hipStream_t stream) {
   const size_t rows = (size_t)B * L * Hq;
   float* o3 = (float*)ws;
@@ -637,7 +645,7 @@ hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const ui
   void* images = (unsigned char*)ws + 3 * rows * kHeadDim * sizeof(float) +
                  round256(3 * rows * sizeof(float));
   PrefillArgs a = {};
-  fill_geometry(a, B, Hq, Hkv, L, sum_hi);
+  fill_geometry(a, B, Hq, Hkv, L, slack);
   hipError_t e = launch_prep(true, k, v, table, B, Hkv, L, G, images, a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
