@@ -8,10 +8,10 @@
 // L = kv_len[b] (Eq. (2)), computed on the device, so one launch serves a
 // ragged batch whose sequences have different G.
 //
-// Split-K: workgroup (b, group of up to 4 kv heads, split) streams a chunk of
-// keys, one wave per kv head.  The g query heads of a kv head are rotated twice
-// (base and remote) and placed
-// in the 16 columns of a v_mfma_f32_16x16x32_bf16 B operand: columns 0..7 hold
+// Split-K: workgroup (b, group of up to 4 kv heads, split) streams every
+// n_split-th 16-key step of the sequence, two waves per kv head.  The g query
+// heads of a kv head are rotated twice (base and remote) and placed in the 16
+// columns of a v_mfma_f32_16x16x32_bf16 B operand: columns 0..7 hold
 // the base-rotated heads, 8..15 the remote-rotated ones.  Each key is rotated
 // once, to the view its distance selects (Eq. (1)), and scored against both
 // column groups; a column keeps only keys of its own view, so every column is
@@ -77,7 +77,9 @@ __device__ inline f32x4 mfma16k16(bf16x4 a, bf16x4 b, f32x4 c) {
                                                    __builtin_bit_cast(i16x4v, b), c, 0, 0, 0);
 }
 
-// Split-K workgroup (b, group of up to 4 kv heads, key chunk).  Every 16-key
+// Split-K workgroup (b, group of up to 4 kv heads, split): split s takes the
+// 16-key steps s, s + n_split, s + 2 n_split, ... of the sequence, so at any
+// moment all workgroups stream one narrow window of the cache.  Every 16-key
 // step copies the keys' contiguous head slices (K and V, one key's heads are
 // adjacent in the cache) straight into LDS.  Waves w and w + 4 serve kv head
 // 4 * group + w on the even and the odd steps, so two waves share each SIMD
@@ -117,14 +119,18 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   const int kvh = h0 + hw;
   const bool head_on = hw < Hg;
   const int kv_len = clamp_len(a.kv_lens[b], a.max_len);
-  const int c0 = split * a.chunk;
-  if (c0 >= kv_len) return;  // whole workgroup, before any barrier
-  const int c1 = min(c0 + a.chunk, kv_len);
+  // this split's steps: global 16-key steps split, split + n_split, ... below
+  // kv_len, so at any moment all splits read neighbouring parts of the cache
+  const int s_all = (kv_len + kDecTile - 1) / kDecTile;
+  if (split >= s_all) return;  // whole workgroup, before any barrier
+  const int c1 = kv_len;
+  const int kstride = a.n_split * kDecTile;
+  const int c0 = split * kDecTile;
   const int G = BIFOCAL ? group_size(kv_len, a.w_pre) : 1;
   const FastDiv gdiv = make_fastdiv((uint32_t)G);
   const int qpos = kv_len - 1;
   const int fq = BIFOCAL ? remote_pos(qpos, gdiv) : qpos;
-  const int n_steps = (c1 - c0 + kDecTile - 1) / kDecTile;
+  const int n_steps = (s_all - split + a.n_split - 1) / a.n_split;
   const int n_iter = (n_steps + 1) / 2;
 
   // ---- copies: a step's K image is 16 keys x Hg heads x 256 B = 4 Hg chunks
@@ -156,7 +162,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     cp_off[i] = h * 256 + 16 * (slot ^ (is_v ? 2 * (t & 7) : t));
   }
   auto issue = [&](int jb) {
-    const int k0 = c0 + min(jb, n_steps - 1) * kDecTile;
+    const int k0 = c0 + min(jb, n_steps - 1) * kstride;
     const uint32_t buf = smem_base + (jb % kDecBufs) * kDecBufBytes;
     {
       // the cos/sin rows that rotate the query columns for this step: q - k0
@@ -174,7 +180,8 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
       const uint32_t key = (uint32_t)min(k0 + (int)cp_t[i], c1 - 1);
       const uint32_t dst = real ? buf + (is_v ? kDecImgBytes + (n - 4 * Hg) * 1024 : n * 1024)
                                 : smem_base + kDecOffDummy;
-      dma16_s(is_v && real ? vseq : kseq, key * kv_row_bytes + cp_off[i], dst);
+      // K and V are read exactly once per call: nontemporal
+      dma16_s_nt(is_v && real ? vseq : kseq, key * kv_row_bytes + cp_off[i], dst);
     }
   };
 
@@ -216,7 +223,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     __syncthreads();  // everyone's copies (and the offset table)
     const int j = 2 * it + par;
     if (head_on && j < n_steps) {
-      const int k0 = c0 + j * kDecTile;
+      const int k0 = c0 + j * kstride;
       const unsigned char* sb = smem + (j % kDecBufs) * kDecBufBytes;
       const unsigned char* kb = sb + hw * 256;
       const unsigned char* vb = kb + kDecImgBytes;
@@ -277,7 +284,9 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
       mt = fmaxf(mt, __shfl_xor(mt, 32));
       const float m_new = fmaxf(m_run, mt);
       const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run - m_use);
+      // 1 unless the maximum moved (a column with no key of its view yet
+      // keeps m = -inf and must not take the rescale branch every step)
+      const float alpha = m_new == m_run ? 1.f : fast_exp2(m_run - m_use);
       f32x4 p;
 #pragma unroll
       for (int i = 0; i < 4; ++i) p[i] = fast_exp2(sv[i] - m_use);
@@ -379,7 +388,7 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
   const int b = bh / a.Hq;
   const int tid = threadIdx.x;
   const int kv_len = clamp_len(a.kv_lens[b], a.max_len);
-  const int ns = (kv_len + a.chunk - 1) / a.chunk;
+  const int ns = min(a.n_split, (kv_len + kDecTile - 1) / kDecTile);  // splits with keys
   const float* base = a.ws + (size_t)bh * a.n_split * kStateFloats;
   const int c = tid & 7;
   const int grp = tid >> 3;
@@ -435,16 +444,16 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
 void decode_geometry(int B, int Hkv, int max_len, int* chunk, int* n_split) {
   // about one workgroup per CU (256 CUs; each holds 144 KB of LDS): enough
   // copies in flight to stream at full bandwidth while keeping few split
-  // states for the reduce (at most kRedGroups * kRedPerGroup per head);
-  // chunks are multiples of one 16-key step
+  // states for the reduce (at most kRedGroups * kRedPerGroup per head).
+  // Split s takes the 16-key steps s, s + n_split, ...; *chunk is the most
+  // keys one split covers.
   const long long groups = (long long)B * ((Hkv + kDecHeads - 1) / kDecHeads);
   long long want = (256 + groups - 1) / groups;
   if (want > kRedGroups * kRedPerGroup) want = kRedGroups * kRedPerGroup;
-  long long ch = ((long long)max_len + want - 1) / want;
-  ch = (ch + kDecTile - 1) / kDecTile * kDecTile;
-  if (ch < 128) ch = 128;
-  *chunk = (int)ch;
-  *n_split = (int)((max_len + ch - 1) / ch);
+  const long long steps = ((long long)max_len + kDecTile - 1) / kDecTile;
+  if (want > steps) want = steps;
+  *n_split = (int)want;
+  *chunk = (int)((steps + want - 1) / want * kDecTile);
 }
 
 size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len) {

@@ -181,6 +181,14 @@ __device__ inline void dma16_s(const void* sbase, uint32_t voff, uint32_t lds_ba
                : "v"(voff), "s"(sbase), "i"(imm), "{m0}"(lds_base)
                : "memory");
 }
+// The same copy with the nontemporal hint, for data that is read exactly once.
+template <int imm = 0>
+__device__ inline void dma16_s_nt(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 offset:%2 nt"
+               :
+               : "v"(voff), "s"(sbase), "i"(imm), "{m0}"(lds_base)
+               : "memory");
+}
 __device__ inline void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 // Wait until at most N of this wave's vector-memory operations are in flight
 // (they complete in issue order, so everything older than the last N is done).
