@@ -113,6 +113,9 @@ def main() -> int:
                     help="decode calls per timed batch")
     ap.add_argument("--literal-reps", type=int, default=2,
                     help="timed calls of the literal three-pass prefill (0 skips it)")
+    ap.add_argument("--freq-reps", type=int, default=1,
+                    help="timed calls of the prefill with the frequency-interpolation remote map "
+                         "(0 skips it)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -272,6 +275,16 @@ def main() -> int:
                "literal_throughput_vs_vanilla": round(med(pv) / med(lt), 4),
                "fused_speedup_vs_literal": round(med(lt) / med(pb), 4)}
 
+    # ---- the Sec. 4.5 ablation's remote view: frequency interpolation
+    fm = {}
+    if args.freq_reps > 0:
+        def freq_map():
+            api.bifocal_prefill(q, k, v, w_pretrained=wp.w_pretrained, w_local=wp.w_local,
+                                rope_theta=wp.theta, out=out, stream=stream, remote_map="freq")
+        freq_map()
+        ft = [timed(freq_map) for _ in range(args.freq_reps)]
+        fm = {"freq_map_prefill_ms": round(med(ft), 3)}
+
     traffic = _traffic_from_profile()
     line = {
         "metric": METRIC,
@@ -307,6 +320,7 @@ def main() -> int:
         "vanilla_prefill_ms": round(med(pv), 3),
         "vanilla_decode_us": round(med(dv_) * 1e3, 2),
         **lit,
+        **fm,
         "roofline": {
             "bound": "mfma",
             "kernel": "prefill_kernel<fused>",

@@ -86,6 +86,35 @@ int jl_bifocal_prefill(const void* q, const void* k, const void* v, void* o, flo
                        int Hq, int Hkv, int L, int head_dim, double rope_theta, int w_pretrained,
                        int w_local, void* stream);
 
+/* Remote-view maps for jl_bifocal_prefill_map. */
+enum {
+  JL_REMOTE_ALIAS = 0, /* Eq. (3): remote positions f(x) = floor(x / G), base frequencies */
+  JL_REMOTE_FREQ = 1   /* Sec. 4.5 / Table 6 ablation: positions kept, frequencies rescaled */
+};
+
+/*
+ * jl_bifocal_prefill with a choice of remote view (Sec. 4.5, Table 6, the
+ * ablation that replaces position aliasing by frequency interpolation).
+ *   remote_map = JL_REMOTE_ALIAS  identical to jl_bifocal_prefill;
+ *   remote_map = JL_REMOTE_FREQ   the remote view keeps each query and key at
+ *     its own position and rotates it with rescaled frequencies omega'_i: with
+ *     s = max(1, L / w_pretrained) and r_i = w_pretrained * omega_i / (2 pi) the
+ *     number of turns pair i completes over the pretraining window,
+ *     gamma_i = clamp((r_i - 1) / 31, 0, 1) and
+ *     omega'_i = (1 - gamma_i) omega_i / s + gamma_i omega_i (YaRN's per-pair
+ *     ramp, alpha = 1, beta = 32; no attention temperature).  The local window,
+ *     the masks and the Eq. (7) merge are unchanged.
+ * When L <= w_pretrained (s = 1, G = 1) both maps run the vanilla kernel.
+ * The frequency map keeps one library-owned table of cos/sin(p * omega'_i),
+ * L x 512 bytes per device, for the last (rope_theta, L, w_pretrained) used;
+ * a new configuration builds a new table (waiting for the stream) and keeps
+ * the old one until jl_release_caches.  Other arguments, scratch and errors
+ * as in jl_bifocal_prefill; remote_map outside {0, 1} -> JL_ERR_INVALID_ARG.
+ */
+int jl_bifocal_prefill_map(const void* q, const void* k, const void* v, void* o, float* lse,
+                           int B, int Hq, int Hkv, int L, int head_dim, double rope_theta,
+                           int w_pretrained, int w_local, int remote_map, void* stream);
+
 /*
  * Vanilla causal RoPE attention with the same tiling and RoPE of raw Q/K at
  * base positions: the base model of Sec. 3 and the denominator of the

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(HERE, "libjetlong.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "jetlong.h")
 
 JL_OK, JL_ERR_INVALID_ARG, JL_ERR_UNSUPPORTED, JL_ERR_WORKSPACE, JL_ERR_HIP = range(5)
+REMOTE_MAPS = {"alias": 0, "freq": 1}  # JL_REMOTE_ALIAS, JL_REMOTE_FREQ
 TILE_SKIP, TILE_LOCAL, TILE_REMOTE, TILE_MIXED = range(4)
 
 _lib = None
@@ -47,6 +48,9 @@ def lib() -> ctypes.CDLL:
         L.jl_bifocal_prefill.restype = i32
         L.jl_bifocal_prefill.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl, i32,
                                          i32, vp]
+        L.jl_bifocal_prefill_map.restype = i32
+        L.jl_bifocal_prefill_map.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl,
+                                             i32, i32, i32, vp]
         L.jl_rope_attention.restype = i32
         L.jl_rope_attention.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl, vp]
         L.jl_prefill_literal_workspace_bytes.restype = sz
@@ -113,7 +117,8 @@ def group_size(L: int, w_pretrained: int) -> int:
     return int(lib().jl_group_size(L, w_pretrained))
 
 
-def _prefill(bifocal, q, k, v, w_pretrained, w_local, rope_theta, out, lse, want_lse, stream):
+def _prefill(bifocal, q, k, v, w_pretrained, w_local, rope_theta, out, lse, want_lse, stream,
+             remote_map="alias"):
     import torch
     B, L, Hq, D = q.shape
     Hkv = k.shape[2]
@@ -127,7 +132,10 @@ def _prefill(bifocal, q, k, v, w_pretrained, w_local, rope_theta, out, lse, want
             _dev(v, "v", torch.bfloat16), _dev(out, "out", torch.bfloat16),
             _dev(lse, "lse", torch.float32) if lse is not None else None, B, Hq, Hkv, L, D,
             float(rope_theta)]
-    if bifocal:
+    if bifocal and remote_map != "alias":
+        _check(lib().jl_bifocal_prefill_map(*args, int(w_pretrained), int(w_local),
+                                            REMOTE_MAPS[remote_map], _stream(stream)))
+    elif bifocal:
         _check(lib().jl_bifocal_prefill(*args, int(w_pretrained), int(w_local), _stream(stream)))
     else:
         _check(lib().jl_rope_attention(*args, _stream(stream)))
@@ -135,10 +143,14 @@ def _prefill(bifocal, q, k, v, w_pretrained, w_local, rope_theta, out, lse, want
 
 
 def bifocal_prefill(q, k, v, *, w_pretrained: int, w_local: int, rope_theta: float = 1e6,
-                    out=None, lse=None, want_lse: bool = False, stream=None):
-    """jl_bifocal_prefill: q [B, L, Hq, 128], k/v [B, L, Hkv, 128] raw bf16 -> out bf16."""
+                    out=None, lse=None, want_lse: bool = False, stream=None,
+                    remote_map: str = "alias"):
+    """jl_bifocal_prefill: q [B, L, Hq, 128], k/v [B, L, Hkv, 128] raw bf16 -> out bf16.
+    remote_map "freq" calls jl_bifocal_prefill_map with JL_REMOTE_FREQ (Sec. 4.5)."""
+    if remote_map not in REMOTE_MAPS:
+        raise ValueError("remote_map must be one of %s" % sorted(REMOTE_MAPS))
     return _prefill(True, q, k, v, w_pretrained, w_local, rope_theta, out, lse,
-                    want_lse or lse is not None, stream)
+                    want_lse or lse is not None, stream, remote_map)
 
 
 def rope_attention(q, k, v, *, rope_theta: float = 1e6, out=None, lse=None,

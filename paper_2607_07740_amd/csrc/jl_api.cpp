@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 #include <string>
@@ -19,13 +20,14 @@ namespace jl {
 // kernels (prefill.hip, decode.hip, aux.hip)
 size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L);
 hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                          uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
-                          int L, int G, int w0, float slack, void* ws, hipStream_t stream,
-                          hipEvent_t ev0, hipEvent_t ev1);
+                          uint16_t* o, float* lse, const float2* table, const float2* rtable,
+                          int freq_map, int B, int Hq, int Hkv, int L, int G, int w0, float slack,
+                          void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L);
 hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                                  uint16_t* o, float* lse, const float2* table, int B, int Hq,
-                                  int Hkv, int L, int G, int w0, float slack, void* ws,
+                                  uint16_t* o, float* lse, const float2* table,
+                                  const float2* rtable, int freq_map, int B, int Hq, int Hkv,
+                                  int L, int G, int w0, float slack, void* ws,
                                   hipStream_t stream);
 int prefill_rows_per_block();
 int prefill_block_q(int g);
@@ -134,6 +136,69 @@ int get_table(double theta, int n_pos, hipStream_t stream, const float2** out) {
   return JL_OK;
 }
 
+// Remote-view frequencies of the frequency-interpolation map (Sec. 4.5, the
+// ablation that keeps positions and rescales frequencies, YaRN style): with
+// s = max(1, L / w_pretrained), pair i of wavelength lambda_i = 2 pi / omega_i
+// completes r_i = w_pretrained / lambda_i turns over the pretraining window;
+// gamma_i = clamp((r_i - 1) / (32 - 1), 0, 1) and
+// omega'_i = (1 - gamma_i) omega_i / s + gamma_i omega_i.  Fast pairs keep
+// their frequency, slow pairs are divided by s.
+void freq_map_omegas(double theta, int L, int w_pre, double* out) {
+  const double kAlpha = 1.0, kBeta = 32.0;
+  const double s = std::max(1.0, (double)L / (double)w_pre);
+  const double two_pi = 2.0 * std::acos(-1.0);
+  for (int i = 0; i < 64; ++i) {
+    const double omega = std::pow(theta, -2.0 * i / (double)kHeadDim);
+    const double r = (double)w_pre / (two_pi / omega);
+    const double gamma = std::min(1.0, std::max(0.0, (r - kAlpha) / (kBeta - kAlpha)));
+    out[i] = (1.0 - gamma) * omega / s + gamma * omega;
+  }
+}
+
+// One frequency-map table per device, for the last (theta, L, w_pretrained)
+// used: [L][64] (cos, sin) of p * omega'_i, rebuilt when the configuration
+// changes (the old one is retired, not freed, while calls may still read it).
+struct FreqTable {
+  int device;
+  double theta;
+  int L, w_pre;
+  float2* ptr;
+};
+std::vector<FreqTable> g_freq_tables;
+
+int get_freq_table(double theta, int L, int w_pre, hipStream_t stream, const float2** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_mu);
+  FreqTable* found = nullptr;
+  for (auto& t : g_freq_tables)
+    if (t.device == dev) found = &t;
+  if (found && found->theta == theta && found->L == L && found->w_pre == w_pre) {
+    *out = found->ptr;
+    return JL_OK;
+  }
+  float2* p = nullptr;
+  e = hipMalloc(&p, (size_t)L * 64 * sizeof(float2));
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc(frequency-map table)");
+  double omega[64];
+  freq_map_omegas(theta, L, w_pre, omega);
+  e = jl::launch_build_table(p, L, omega, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) {
+    (void)hipFree(p);
+    return hip_fail(e, "building frequency-map table");
+  }
+  if (found) {
+    g_retired.emplace_back(found->device, found->ptr);
+    *found = FreqTable{dev, theta, L, w_pre, p};
+  } else {
+    g_freq_tables.push_back(FreqTable{dev, theta, L, w_pre, p});
+  }
+  *out = p;
+  return JL_OK;
+}
+
 // ------------------------------------------- prefill scratch, per stream
 // The prefill writes each call's rotated K (one image per view) and
 // transposed V to scratch before its attention kernel reads them.  One buffer
@@ -201,9 +266,13 @@ int check_common(int B, int Hq, int Hkv, int head_dim, double theta) {
 // library scratch.
 int prefill_common(bool bifocal, const void* q, const void* k, const void* v, void* o, float* lse,
                    int B, int Hq, int Hkv, int L, int head_dim, double theta, int w_pre, int w0,
-                   void* stream, bool literal = false, void* ws = nullptr, size_t ws_bytes = 0) {
+                   void* stream, bool literal = false, void* ws = nullptr, size_t ws_bytes = 0,
+                   int remote_map = JL_REMOTE_ALIAS) {
   int st = check_common(B, Hq, Hkv, head_dim, theta);
   if (st != JL_OK) return st;
+  if (remote_map != JL_REMOTE_ALIAS && remote_map != JL_REMOTE_FREQ)
+    return fail(JL_ERR_INVALID_ARG, "remote_map must be JL_REMOTE_ALIAS or JL_REMOTE_FREQ (got %d)",
+                remote_map);
   if (L < 1) return fail(JL_ERR_INVALID_ARG, "L must be >= 1 (got %d)", L);
   if (bifocal && w_pre < 1)
     return fail(JL_ERR_INVALID_ARG, "w_pretrained must be >= 1 (got %d)", w_pre);
@@ -232,13 +301,21 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   if (st != JL_OK) return st;
   // G == 1: f is the identity and the method is the base model (Sec. 3), so
   // the bifocal entry runs the vanilla kernel and matches it bit for bit.
+  // The frequency map's factor s = L / w_pretrained is 1 exactly then too.
   const bool use_bifocal = bifocal && G > 1;
+  const int freq_map = remote_map == JL_REMOTE_FREQ ? 1 : 0;
+  const float2* rtable = nullptr;
+  if (use_bifocal && freq_map) {
+    st = get_freq_table(theta, L, w_pre, s, &rtable);
+    if (st != JL_OK) return st;
+  }
   const float slack = (float)g_rescale_log2.load();
   if (literal) {
     if (use_bifocal) {
       hipError_t e = jl::launch_prefill_literal((const uint16_t*)q, (const uint16_t*)k,
-                                                (const uint16_t*)v, (uint16_t*)o, lse, table, B,
-                                                Hq, Hkv, L, G, w0, slack, ws, s);
+                                                (const uint16_t*)v, (uint16_t*)o, lse, table,
+                                                rtable, freq_map, B, Hq, Hkv, L, G, w0, slack,
+                                                ws, s);
       if (e != hipSuccess) return hip_fail(e, "literal prefill launch");
       return ok();
     }
@@ -250,8 +327,8 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   hipEvent_t ev0, ev1;
   timing_events(0, &ev0, &ev1);
   hipError_t e = jl::launch_prefill(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,
-                                    (const uint16_t*)v, (uint16_t*)o, lse, table, B, Hq, Hkv, L,
-                                    G, w0, slack, scratch, s, ev0, ev1);
+                                    (const uint16_t*)v, (uint16_t*)o, lse, table, rtable, freq_map,
+                                    B, Hq, Hkv, L, G, w0, slack, scratch, s, ev0, ev1);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   return ok();
 }
@@ -325,6 +402,13 @@ int jl_rope_attention(const void* q, const void* k, const void* v, void* o, floa
                       int Hq, int Hkv, int L, int head_dim, double rope_theta, void* stream) {
   return prefill_common(false, q, k, v, o, lse, B, Hq, Hkv, L, head_dim, rope_theta, 1, 0,
                         stream);
+}
+
+int jl_bifocal_prefill_map(const void* q, const void* k, const void* v, void* o, float* lse,
+                           int B, int Hq, int Hkv, int L, int head_dim, double rope_theta,
+                           int w_pretrained, int w_local, int remote_map, void* stream) {
+  return prefill_common(true, q, k, v, o, lse, B, Hq, Hkv, L, head_dim, rope_theta, w_pretrained,
+                        w_local, stream, false, nullptr, 0, remote_map);
 }
 
 size_t jl_prefill_literal_workspace_bytes(int B, int Hq, int Hkv, int L, int head_dim) {
@@ -430,6 +514,9 @@ void jl_release_caches(void) {
   for (auto& r : g_retired) {
     if (hipSetDevice(r.first) == hipSuccess) (void)hipFree(r.second);
   }
+  for (auto& t : g_freq_tables) {
+    if (hipSetDevice(t.device) == hipSuccess) (void)hipFree(t.ptr);
+  }
   for (auto& sc : g_scratch) {
     if (hipSetDevice(sc.device) == hipSuccess) {
       (void)hipStreamSynchronize(sc.stream);
@@ -437,6 +524,7 @@ void jl_release_caches(void) {
     }
   }
   g_tables.clear();
+  g_freq_tables.clear();
   g_retired.clear();
   g_scratch.clear();
   if (have_cur) (void)hipSetDevice(cur);

@@ -81,7 +81,9 @@ struct PrepArgs {
   uint16_t* krem;  // same, remote view (bifocal only)
   uint16_t* vt;    // [B][Hkv][n_tiles] V^T images
   const float2* table;
+  const float2* rtable;  // remote view: table at f(p) (aliasing map) or rtable at p (frequency map)
   int B, Hkv, L, n_tiles;
+  int freq_map;          // 0: Eq. (3) aliasing, 1: Sec. 4.5 frequency interpolation
   FastDiv gdiv;
 };
 
@@ -124,8 +126,10 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
       unpack8(valid ? load16(kseq + (size_t)key * row + 8 * c + kHalf) : u32x4{0, 0, 0, 0}, hi);
 #pragma unroll
       for (int view = 0; view < (BIFOCAL ? 2 : 1); ++view) {
-        const int pos = view == 0 ? (valid ? key : 0) : remote_pos(valid ? key : 0, a.gdiv);
-        const float4* c4 = (const float4*)(a.table + (size_t)pos * kHalf + 8 * c);
+        const int kp = valid ? key : 0;
+        const int pos = view == 0 || a.freq_map ? kp : remote_pos(kp, a.gdiv);
+        const float2* tab = view == 0 ? a.table : a.rtable;
+        const float4* c4 = (const float4*)(tab + (size_t)pos * kHalf + 8 * c);
         float ylo[8], yhi[8];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -166,6 +170,8 @@ struct PrefillArgs {
   uint16_t* o;
   float* lse;
   const float2* table;   // [positions][64] (cos, sin) of p * omega_i
+  const float2* rtable;  // remote view: table read at f(p), or the frequency map's table at p
+  int freq_map;          // 0: Eq. (3) aliasing, 1: Sec. 4.5 frequency interpolation
   const uint16_t* kloc;  // tile images from prep_kernel
   const uint16_t* krem;
   const uint16_t* vt;
@@ -456,8 +462,9 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   };
 
   // ---- prologue: the first view's query operand, K(0), V(0), K(1)
-  load_q_operand(qrow, hl32, a.table, (n_r > 0 || REMOTE2) ? remote_pos(qp, a.gdiv) : qp,
-                 a.q_scale, qop);
+  const bool q_remote = n_r > 0 || REMOTE2;
+  load_q_operand(qrow, hl32, q_remote ? a.rtable : a.table,
+                 q_remote && !a.freq_map ? remote_pos(qp, a.gdiv) : qp, a.q_scale, qop);
   issue_k(0);
   issue_v(0);
   if (n_steps > 1) issue_k(1);
@@ -556,9 +563,12 @@ size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L) {
          prefill_workspace_bytes(true, B, Hkv, L);
 }
 
+// rtable: the remote view's table, nullptr for the aliasing map (then the
+// base table is read at f(p)); with freq_map it is read at p.
 static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v,
-                              const float2* table, int B, int Hkv, int L, int G, void* images,
-                              PrefillArgs& a, hipStream_t stream) {
+                              const float2* table, const float2* rtable, int freq_map, int B,
+                              int Hkv, int L, int G, void* images, PrefillArgs& a,
+                              hipStream_t stream) {
   const int n_tiles = (L + kPfBK - 1) / kPfBK;
   const size_t img = (size_t)B * Hkv * n_tiles * (kTileBytes / 2);  // bf16 elements per image set
   a.kloc = (const uint16_t*)images;
@@ -566,6 +576,8 @@ static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v
   a.krem = bifocal ? a.vt + img : nullptr;
   a.n_tiles = n_tiles;
   a.table = table;
+  a.rtable = freq_map ? rtable : table;
+  a.freq_map = freq_map;
   a.gdiv = make_fastdiv((uint32_t)G);
 
   PrepArgs p;
@@ -575,6 +587,8 @@ static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v
   p.krem = (uint16_t*)a.krem;
   p.vt = (uint16_t*)a.vt;
   p.table = table;
+  p.rtable = a.rtable;
+  p.freq_map = freq_map;
   p.B = B;
   p.Hkv = Hkv;
   p.L = L;
@@ -617,12 +631,12 @@ static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream
 
 // ev0 / ev1 (optional) are recorded on the stream around the attention kernel.
 hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                          uint16_t* o, float* lse, const float2* table, int B, int Hq, int Hkv,
-                          int L, int G, int w0, float slack, void* ws, hipStream_t stream,
-                          hipEvent_t ev0, hipEvent_t ev1) {
+                          uint16_t* o, float* lse, const float2* table, const float2* rtable,
+                          int freq_map, int B, int Hq, int Hkv, int L, int G, int w0, float slack,
+                          void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
   PrefillArgs a = {};
   fill_geometry(a, B, Hq, Hkv, L, slack);
-  hipError_t e = launch_prep(bifocal, k, v, table, B, Hkv, L, G, ws, a, stream);
+  hipError_t e = launch_prep(bifocal, k, v, table, rtable, freq_map, B, Hkv, L, G, ws, a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
   a.o = o;
@@ -636,8 +650,9 @@ hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, co
 
 // Eq. (7) taken literally: the three window passes, then the merge.
 hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                                  uint16_t* o, float* lse, const float2* table, int B, int Hq,
-                                  int Hkv, int L, int G, int w0, float slack, void* ws,
+                                  uint16_t* o, float* lse, const float2* table,
+                                  const float2* rtable, int freq_map, int B, int Hq, int Hkv,
+                                  int L, int G, int w0, float slack, void* ws,
                                   hipStream_t stream) {
   const size_t rows = (size_t)B * L * Hq;
   float* o3 = (float*)ws;
@@ -646,7 +661,7 @@ hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const ui
                  round256(3 * rows * sizeof(float));
   PrefillArgs a = {};
   fill_geometry(a, B, Hq, Hkv, L, slack);
-  hipError_t e = launch_prep(true, k, v, table, B, Hkv, L, G, images, a, stream);
+  hipError_t e = launch_prep(true, k, v, table, rtable, freq_map, B, Hkv, L, G, images, a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
   const int modes[3] = {kModeWinA, kModeWinB, kModeWinC};

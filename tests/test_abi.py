@@ -70,6 +70,17 @@ def test_prefill_rejects_before_launch(kw, code):
     assert api.lib().jl_last_error().decode() != ""
 
 
+@pytest.mark.parametrize("remote_map", [-1, 2, 7])
+def test_prefill_map_rejects_unknown_remote_map(remote_map):
+    L = api.lib()
+    assert L.jl_bifocal_prefill_map(A, A, A, A, None, 1, 4, 2, 64, 128, 1e6, 16, 4, remote_map,
+                                    None) == api.JL_ERR_INVALID_ARG
+    assert "remote_map" in L.jl_last_error().decode()
+    # the usual checks still apply to a valid map
+    assert L.jl_bifocal_prefill_map(A, A, A, A, None, 1, 4, 2, 0, 128, 1e6, 16, 4, 1,
+                                    None) == api.JL_ERR_INVALID_ARG
+
+
 def test_rope_attention_rejects_before_launch():
     L = api.lib()
     assert L.jl_rope_attention(A, A, A, A, None, 1, 4, 2, 0, 128, 1e6, None) == api.JL_ERR_INVALID_ARG
