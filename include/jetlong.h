@@ -116,6 +116,35 @@ int jl_bifocal_prefill_map(const void* q, const void* k, const void* v, void* o,
                            int w_pretrained, int w_local, int remote_map, void* stream);
 
 /*
+ * Continued (chunked) prefill over an existing raw cache (Sec. 3.2: the cache
+ * keeps keys at base coordinates and is never rewritten when G changes).
+ *   q       bf16 [B, n_queries, Hq, head_dim]  raw queries at positions
+ *                                              q_start .. q_start + n_queries - 1
+ *   k_cache bf16 [B, max_len, Hkv, head_dim]   raw keys; rows [0, q_start + n_queries)
+ *   v_cache bf16 [B, max_len, Hkv, head_dim]   must hold the chunk's own keys too
+ *   o       bf16 [B, n_queries, Hq, head_dim]  output (written)
+ *   lse     fp32 [B, Hq, n_queries] or NULL
+ * The call's sequence length is L = q_start + n_queries: G = max(1,
+ * ceil(L / w_pretrained)) for every query of the chunk, as in a prefill of
+ * length L, so the output equals rows q_start .. L - 1 of
+ * jl_bifocal_prefill over the first L cache rows.  The caches are only read.
+ * Each call rotates keys [0, L) once per view into the library scratch (as
+ * jl_bifocal_prefill does for its L), so a chunk costs O(L) extra work on top
+ * of its attention.  Requires 0 <= q_start, n_queries >= 1,
+ * q_start + n_queries <= max_len; other requirements and errors as in
+ * jl_bifocal_prefill.
+ */
+int jl_bifocal_prefill_chunk(const void* q, const void* k_cache, const void* v_cache, void* o,
+                             float* lse, int B, int Hq, int Hkv, int q_start, int n_queries,
+                             int max_len, int head_dim, double rope_theta, int w_pretrained,
+                             int w_local, void* stream);
+
+/* The vanilla counterpart of jl_bifocal_prefill_chunk (base rotation only). */
+int jl_rope_attention_chunk(const void* q, const void* k_cache, const void* v_cache, void* o,
+                            float* lse, int B, int Hq, int Hkv, int q_start, int n_queries,
+                            int max_len, int head_dim, double rope_theta, void* stream);
+
+/*
  * Vanilla causal RoPE attention with the same tiling and RoPE of raw Q/K at
  * base positions: the base model of Sec. 3 and the denominator of the
  * overhead measurements.  Arguments and scratch as in jl_bifocal_prefill

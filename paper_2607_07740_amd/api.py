@@ -51,6 +51,12 @@ def lib() -> ctypes.CDLL:
         L.jl_bifocal_prefill_map.restype = i32
         L.jl_bifocal_prefill_map.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl,
                                              i32, i32, i32, vp]
+        L.jl_bifocal_prefill_chunk.restype = i32
+        L.jl_bifocal_prefill_chunk.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
+                                               i32, dbl, i32, i32, vp]
+        L.jl_rope_attention_chunk.restype = i32
+        L.jl_rope_attention_chunk.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
+                                              i32, dbl, vp]
         L.jl_rope_attention.restype = i32
         L.jl_rope_attention.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl, vp]
         L.jl_prefill_literal_workspace_bytes.restype = sz
@@ -158,6 +164,33 @@ def rope_attention(q, k, v, *, rope_theta: float = 1e6, out=None, lse=None,
     """jl_rope_attention: vanilla causal RoPE attention with the same kernel."""
     return _prefill(False, q, k, v, 1, 0, rope_theta, out, lse, want_lse or lse is not None,
                     stream)
+
+
+def prefill_chunk(q, k_cache, v_cache, *, q_start: int, w_pretrained: int = 1, w_local: int = 0,
+                  rope_theta: float = 1e6, bifocal: bool = True, out=None, lse=None,
+                  want_lse: bool = False, stream=None):
+    """jl_bifocal_prefill_chunk / jl_rope_attention_chunk: q [B, n, Hq, 128] raw queries at
+    positions q_start .. q_start + n - 1 over the raw caches [B, max_len, Hkv, 128]."""
+    import torch
+    B, n, Hq, D = q.shape
+    _, max_len, Hkv, _ = k_cache.shape
+    if k_cache.shape != (B, max_len, Hkv, D) or v_cache.shape != k_cache.shape:
+        raise ValueError("caches must be [B, max_len, Hkv, D] matching q [B, n, Hq, D]")
+    if out is None:
+        out = torch.empty_like(q)
+    want_lse = want_lse or lse is not None
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, n), dtype=torch.float32, device=q.device)
+    args = [_dev(q, "q", torch.bfloat16), _dev(k_cache, "k_cache", torch.bfloat16),
+            _dev(v_cache, "v_cache", torch.bfloat16), _dev(out, "out", torch.bfloat16),
+            _dev(lse, "lse", torch.float32) if lse is not None else None, B, Hq, Hkv,
+            int(q_start), n, max_len, D, float(rope_theta)]
+    if bifocal:
+        _check(lib().jl_bifocal_prefill_chunk(*args, int(w_pretrained), int(w_local),
+                                              _stream(stream)))
+    else:
+        _check(lib().jl_rope_attention_chunk(*args, _stream(stream)))
+    return (out, lse) if want_lse else out
 
 
 def prefill_literal_workspace_bytes(B: int, Hq: int, Hkv: int, L: int,

@@ -23,6 +23,11 @@ hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, co
                           uint16_t* o, float* lse, const float2* table, const float2* rtable,
                           int freq_map, int B, int Hq, int Hkv, int L, int G, int w0, float slack,
                           void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
+hipError_t launch_prefill_chunk(bool bifocal, const uint16_t* q, const uint16_t* k,
+                                const uint16_t* v, uint16_t* o, float* lse, const float2* table,
+                                const float2* rtable, int freq_map, int B, int Hq, int Hkv, int L,
+                                int q_start, int Lq, int kv_stride, int G, int w0, float slack,
+                                void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L);
 hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                   uint16_t* o, float* lse, const float2* table,
@@ -267,7 +272,12 @@ int check_common(int B, int Hq, int Hkv, int head_dim, double theta) {
 int prefill_common(bool bifocal, const void* q, const void* k, const void* v, void* o, float* lse,
                    int B, int Hq, int Hkv, int L, int head_dim, double theta, int w_pre, int w0,
                    void* stream, bool literal = false, void* ws = nullptr, size_t ws_bytes = 0,
-                   int remote_map = JL_REMOTE_ALIAS) {
+                   int remote_map = JL_REMOTE_ALIAS, int q_start = 0, int Lq = -1,
+                   int kv_stride = -1) {
+  // a chunk: queries q_start .. q_start + Lq - 1 over keys [0, L) of a cache
+  // with kv_stride rows per sequence; the full prefill has Lq = kv_stride = L
+  if (Lq < 0) Lq = L;
+  if (kv_stride < 0) kv_stride = L;
   int st = check_common(B, Hq, Hkv, head_dim, theta);
   if (st != JL_OK) return st;
   if (remote_map != JL_REMOTE_ALIAS && remote_map != JL_REMOTE_FREQ)
@@ -284,7 +294,7 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   const int rows = jl::prefill_rows_per_block();
   if (rows % g != 0)
     return fail(JL_ERR_UNSUPPORTED, "GQA group Hq/Hkv = %d must divide %d", g, rows);
-  const long long nqb = (L + (rows / g) - 1) / (rows / g);
+  const long long nqb = (Lq + (rows / g) - 1) / (rows / g);
   if (nqb * B * Hkv > 0x7fffffffLL) return fail(JL_ERR_INVALID_ARG, "problem too large");
   if ((long long)B * Hkv > 65535) return fail(JL_ERR_INVALID_ARG, "B * Hkv too large");
   if (literal) {
@@ -326,9 +336,10 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   if (st != JL_OK) return st;
   hipEvent_t ev0, ev1;
   timing_events(0, &ev0, &ev1);
-  hipError_t e = jl::launch_prefill(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,
-                                    (const uint16_t*)v, (uint16_t*)o, lse, table, rtable, freq_map,
-                                    B, Hq, Hkv, L, G, w0, slack, scratch, s, ev0, ev1);
+  hipError_t e = jl::launch_prefill_chunk(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,
+                                          (const uint16_t*)v, (uint16_t*)o, lse, table, rtable,
+                                          freq_map, B, Hq, Hkv, L, q_start, Lq, kv_stride, G, w0,
+                                          slack, scratch, s, ev0, ev1);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   return ok();
 }
@@ -409,6 +420,35 @@ int jl_bifocal_prefill_map(const void* q, const void* k, const void* v, void* o,
                            int w_pretrained, int w_local, int remote_map, void* stream) {
   return prefill_common(true, q, k, v, o, lse, B, Hq, Hkv, L, head_dim, rope_theta, w_pretrained,
                         w_local, stream, false, nullptr, 0, remote_map);
+}
+
+static int prefill_chunk(bool bifocal, const void* q, const void* k_cache, const void* v_cache,
+                         void* o, float* lse, int B, int Hq, int Hkv, int q_start, int n_queries,
+                         int max_len, int head_dim, double theta, int w_pre, int w0,
+                         void* stream) {
+  if (q_start < 0) return fail(JL_ERR_INVALID_ARG, "q_start must be >= 0 (got %d)", q_start);
+  if (n_queries < 1) return fail(JL_ERR_INVALID_ARG, "n_queries must be >= 1 (got %d)", n_queries);
+  if ((long long)q_start + n_queries > max_len)
+    return fail(JL_ERR_INVALID_ARG, "q_start + n_queries (%lld) exceeds max_len (%d)",
+                (long long)q_start + n_queries, max_len);
+  return prefill_common(bifocal, q, k_cache, v_cache, o, lse, B, Hq, Hkv, q_start + n_queries,
+                        head_dim, theta, w_pre, w0, stream, false, nullptr, 0, JL_REMOTE_ALIAS,
+                        q_start, n_queries, max_len);
+}
+
+int jl_bifocal_prefill_chunk(const void* q, const void* k_cache, const void* v_cache, void* o,
+                             float* lse, int B, int Hq, int Hkv, int q_start, int n_queries,
+                             int max_len, int head_dim, double rope_theta, int w_pretrained,
+                             int w_local, void* stream) {
+  return prefill_chunk(true, q, k_cache, v_cache, o, lse, B, Hq, Hkv, q_start, n_queries, max_len,
+                       head_dim, rope_theta, w_pretrained, w_local, stream);
+}
+
+int jl_rope_attention_chunk(const void* q, const void* k_cache, const void* v_cache, void* o,
+                            float* lse, int B, int Hq, int Hkv, int q_start, int n_queries,
+                            int max_len, int head_dim, double rope_theta, void* stream) {
+  return prefill_chunk(false, q, k_cache, v_cache, o, lse, B, Hq, Hkv, q_start, n_queries,
+                       max_len, head_dim, rope_theta, 1, 0, stream);
 }
 
 size_t jl_prefill_literal_workspace_bytes(int B, int Hq, int Hkv, int L, int head_dim) {

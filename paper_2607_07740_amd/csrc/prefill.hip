@@ -82,8 +82,9 @@ struct PrepArgs {
   uint16_t* vt;    // [B][Hkv][n_tiles] V^T images
   const float2* table;
   const float2* rtable;  // remote view: table at f(p) (aliasing map) or rtable at p (frequency map)
-  int B, Hkv, L, n_tiles;
-  int freq_map;          // 0: Eq. (3) aliasing, 1: Sec. 4.5 frequency interpolation
+  int B, Hkv, L, n_tiles;  // L: keys [0, L) are valid
+  int kv_stride;           // rows per sequence in k and v (>= L)
+  int freq_map;            // 0: Eq. (3) aliasing, 1: Sec. 4.5 frequency interpolation
   FastDiv gdiv;
 };
 
@@ -97,8 +98,8 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
   const int t = threadIdx.x;
   const int k0 = tile * kPfBK;
   const size_t row = (size_t)a.Hkv * kHeadDim;
-  const uint16_t* kseq = a.k + ((size_t)b * a.L * a.Hkv + kvh) * kHeadDim;
-  const uint16_t* vseq = a.v + ((size_t)b * a.L * a.Hkv + kvh) * kHeadDim;
+  const uint16_t* kseq = a.k + ((size_t)b * a.kv_stride * a.Hkv + kvh) * kHeadDim;
+  const uint16_t* vseq = a.v + ((size_t)b * a.kv_stride * a.Hkv + kvh) * kHeadDim;
   const size_t img = ((size_t)bh * a.n_tiles + tile) * (kTileBytes / 2);
 
   // V tile -> LDS, zeros past L
@@ -175,7 +176,8 @@ struct PrefillArgs {
   const uint16_t* kloc;  // tile images from prep_kernel
   const uint16_t* krem;
   const uint16_t* vt;
-  int B, Hq, Hkv, L, n_tiles;
+  int B, Hq, Hkv, L, n_tiles;  // L: keys [0, L), the call's sequence length (G follows it)
+  int q_start, Lq;              // query rows: positions q_start .. q_start + Lq - 1 (= L - Lq ..)
   int g, BQ, n_qblocks;
   int w0;         // local window; INT_MAX for the vanilla kernel and window B
   FastDiv gdiv;   // division by G (Eq. (3))
@@ -266,19 +268,20 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   }
   const int b = group / a.Hkv;
   const int kvh = group - b * a.Hkv;
-  const int L = a.L;
+  const int q_end = a.q_start + a.Lq;  // one past the last query position
   const int w0 = a.w0;
-  const int q0 = qblk * a.BQ;
-  const int q1 = min(q0 + a.BQ, L) - 1;
+  const int q0 = a.q_start + qblk * a.BQ;
+  const int q1 = min(q0 + a.BQ, q_end) - 1;
 
   // ---- this lane's query row: column (lane & 31) of the wave's 32
   const int row = 32 * wave + (lane & 31);
   const int hl = row / a.BQ;
   const int qpos = q0 + (row - hl * a.BQ);
-  const bool row_valid = qpos < L;
-  const int qp = row_valid ? qpos : L - 1;
+  const bool row_valid = qpos < q_end;
+  const int qp = row_valid ? qpos : q_end - 1;
   const int hd = kvh * a.g + hl;
-  const uint16_t* qrow = a.q + (((size_t)b * L + qp) * a.Hq + hd) * kHeadDim;
+  const int qr = qp - a.q_start;  // row of this query in q, o and lse
+  const uint16_t* qrow = a.q + (((size_t)b * a.Lq + qr) * a.Hq + hd) * kHeadDim;
 
   // ---- visit list: segment 1 = tiles [0, n_r), segment 2 = tiles [kt_l, n_kt)
   const VisitRanges vr = visit_ranges(q0, q1, w0, kPfBK);
@@ -485,7 +488,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (row_valid) {
     const float inv = 1.f / l_tot;
-    const size_t orow_off = (((size_t)b * L + qp) * a.Hq + hd) * kHeadDim;
+    const size_t orow_off = (((size_t)b * a.Lq + qr) * a.Hq + hd) * kHeadDim;
 #pragma unroll
     for (int db = 0; db < 4; ++db) {
 #pragma unroll
@@ -501,7 +504,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       }
     }
     if (a.lse != nullptr && hl32 == 0)
-      a.lse[((size_t)b * a.Hq + hd) * L + qp] = (m_ref + log2f(l_tot)) * 0.69314718055994531f;
+      a.lse[((size_t)b * a.Hq + hd) * a.Lq + qr] = (m_ref + log2f(l_tot)) * 0.69314718055994531f;
   }
 }
 
@@ -567,7 +570,7 @@ size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L) {
 // base table is read at f(p)); with freq_map it is read at p.
 static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v,
                               const float2* table, const float2* rtable, int freq_map, int B,
-                              int Hkv, int L, int G, void* images, PrefillArgs& a,
+                              int Hkv, int L, int kv_stride, int G, void* images, PrefillArgs& a,
                               hipStream_t stream) {
   const int n_tiles = (L + kPfBK - 1) / kPfBK;
   const size_t img = (size_t)B * Hkv * n_tiles * (kTileBytes / 2);  // bf16 elements per image set
@@ -592,6 +595,7 @@ static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v
   p.B = B;
   p.Hkv = Hkv;
   p.L = L;
+  p.kv_stride = kv_stride;
   p.n_tiles = n_tiles;
   p.gdiv = a.gdiv;
   if ((long long)B * Hkv > 65535) return hipErrorInvalidConfiguration;
@@ -602,14 +606,18 @@ static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v
   return hipGetLastError();
 }
 
-static void fill_geometry(PrefillArgs& a, int B, int Hq, int Hkv, int L, float slack) {
+// L: keys of the call; the queries are rows q_start .. q_start + Lq - 1
+static void fill_geometry(PrefillArgs& a, int B, int Hq, int Hkv, int L, int q_start, int Lq,
+                          float slack) {
   a.B = B;
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.L = L;
+  a.q_start = q_start;
+  a.Lq = Lq;
   a.g = Hq / Hkv;
   a.BQ = kPfRows / a.g;
-  a.n_qblocks = (L + a.BQ - 1) / a.BQ;
+  a.n_qblocks = (Lq + a.BQ - 1) / a.BQ;
   a.q_scale = 1.4426950408889634f / sqrtf((float)kHeadDim);
   a.slack = slack;
 }
@@ -629,14 +637,19 @@ static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream
   return hipGetLastError();
 }
 
-// ev0 / ev1 (optional) are recorded on the stream around the attention kernel.
-hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                          uint16_t* o, float* lse, const float2* table, const float2* rtable,
-                          int freq_map, int B, int Hq, int Hkv, int L, int G, int w0, float slack,
-                          void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+// Queries at positions q_start .. q_start + Lq - 1 (q, o: [B][Lq][Hq][128],
+// lse [B][Hq][Lq]) over keys [0, L) of k, v ([B][kv_stride][Hkv][128]); the
+// full prefill is q_start = 0, Lq = kv_stride = L.  ev0 / ev1 (optional) are
+// recorded on the stream around the attention kernel.
+hipError_t launch_prefill_chunk(bool bifocal, const uint16_t* q, const uint16_t* k,
+                                const uint16_t* v, uint16_t* o, float* lse, const float2* table,
+                                const float2* rtable, int freq_map, int B, int Hq, int Hkv, int L,
+                                int q_start, int Lq, int kv_stride, int G, int w0, float slack,
+                                void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
   PrefillArgs a = {};
-  fill_geometry(a, B, Hq, Hkv, L, slack);
-  hipError_t e = launch_prep(bifocal, k, v, table, rtable, freq_map, B, Hkv, L, G, ws, a, stream);
+  fill_geometry(a, B, Hq, Hkv, L, q_start, Lq, slack);
+  hipError_t e = launch_prep(bifocal, k, v, table, rtable, freq_map, B, Hkv, L, kv_stride, G, ws,
+                             a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
   a.o = o;
@@ -646,6 +659,14 @@ hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, co
   e = launch_attn(bifocal ? kModeFused : kModeVanilla, a, stream);
   if (e == hipSuccess && ev1 != nullptr) e = hipEventRecord(ev1, stream);
   return e;
+}
+
+hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                          uint16_t* o, float* lse, const float2* table, const float2* rtable,
+                          int freq_map, int B, int Hq, int Hkv, int L, int G, int w0, float slack,
+                          void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+  return launch_prefill_chunk(bifocal, q, k, v, o, lse, table, rtable, freq_map, B, Hq, Hkv, L, 0,
+                              L, L, G, w0, slack, ws, stream, ev0, ev1);
 }
 
 // Eq. (7) taken literally: the three window passes, then the merge.
@@ -660,8 +681,9 @@ hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const ui
   void* images = (unsigned char*)ws + 3 * rows * kHeadDim * sizeof(float) +
                  round256(3 * rows * sizeof(float));
   PrefillArgs a = {};
-  fill_geometry(a, B, Hq, Hkv, L, slack);
-  hipError_t e = launch_prep(true, k, v, table, rtable, freq_map, B, Hkv, L, G, images, a, stream);
+  fill_geometry(a, B, Hq, Hkv, L, 0, L, slack);
+  hipError_t e = launch_prep(true, k, v, table, rtable, freq_map, B, Hkv, L, L, G, images, a,
+                             stream);
   if (e != hipSuccess) return e;
   a.q = q;
   const int modes[3] = {kModeWinA, kModeWinB, kModeWinC};

@@ -81,6 +81,18 @@ def test_prefill_map_rejects_unknown_remote_map(remote_map):
                                     None) == api.JL_ERR_INVALID_ARG
 
 
+@pytest.mark.parametrize("q_start,n,max_len", [(-1, 16, 64), (0, 0, 64), (60, 16, 64),
+                                                (0, 65, 64)])
+def test_prefill_chunk_rejects_bad_ranges(q_start, n, max_len):
+    L = api.lib()
+    for rc in (L.jl_bifocal_prefill_chunk(A, A, A, A, None, 1, 4, 2, q_start, n, max_len, 128,
+                                          1e6, 16, 4, None),
+               L.jl_rope_attention_chunk(A, A, A, A, None, 1, 4, 2, q_start, n, max_len, 128, 1e6,
+                                         None)):
+        assert rc == api.JL_ERR_INVALID_ARG
+        assert L.jl_last_error().decode() != ""
+
+
 def test_rope_attention_rejects_before_launch():
     L = api.lib()
     assert L.jl_rope_attention(A, A, A, A, None, 1, 4, 2, 0, 128, 1e6, None) == api.JL_ERR_INVALID_ARG
