@@ -226,6 +226,32 @@ int jl_rope_attention_decode(const void* q, const void* k_cache, const void* v_c
                              size_t workspace_bytes, void* stream);
 
 /*
+ * jl_bifocal_decode on a paged cache: keys and values live in pools of
+ * fixed-size pages and each sequence lists its pages in a block table.
+ *   k_pages, v_pages bf16 [n_pages, page_size, Hkv, head_dim] raw pools
+ *   block_table      int32 [B, max_pages] DEVICE array: key k of sequence b
+ *                    is row k % page_size of page block_table[b][k / page_size]
+ *   kv_lens          int32 [B] DEVICE array, 1 <= kv_lens[b] <= max_pages * page_size
+ * page_size is a power of two, at least 16 (a 16-key step of the kernel never
+ * straddles two pages).  Page indices outside [0, n_pages) are clamped into
+ * the pool, so a bad table gives wrong values, never an out-of-bounds read.
+ * Workspace as for jl_bifocal_decode with max_len = max_pages * page_size.
+ * Other arguments, requirements and errors as in jl_bifocal_decode.
+ */
+int jl_bifocal_decode_paged(const void* q, const void* k_pages, const void* v_pages,
+                            const int32_t* block_table, int max_pages, int page_size, int n_pages,
+                            const int32_t* kv_lens, void* o, int B, int Hq, int Hkv,
+                            int head_dim, double rope_theta, int w_pretrained, int w_local,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/* The vanilla counterpart of jl_bifocal_decode_paged. */
+int jl_rope_attention_decode_paged(const void* q, const void* k_pages, const void* v_pages,
+                                   const int32_t* block_table, int max_pages, int page_size,
+                                   int n_pages, const int32_t* kv_lens, void* o, int B, int Hq,
+                                   int Hkv, int head_dim, double rope_theta, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
+/*
  * Debug view of the schedule as the device computes it (Eqs. (2), (3), (5)),
  * for bit-exact tests.  All pointers are device pointers.
  *   lengths    int32 [n_lengths]              sequence lengths L (>= 1)

@@ -72,6 +72,12 @@ def lib() -> ctypes.CDLL:
         L.jl_rope_attention_decode.restype = i32
         L.jl_rope_attention_decode.argtypes = [vp, vp, vp, vp, i32, vp, i32, i32, i32, i32, dbl,
                                                vp, sz, vp]
+        L.jl_bifocal_decode_paged.restype = i32
+        L.jl_bifocal_decode_paged.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, i32, i32, i32,
+                                              i32, dbl, i32, i32, vp, sz, vp]
+        L.jl_rope_attention_decode_paged.restype = i32
+        L.jl_rope_attention_decode_paged.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, i32,
+                                                     i32, i32, i32, dbl, vp, sz, vp]
         L.jl_debug_schedule.restype = i32
         L.jl_debug_schedule.argtypes = [vp, i32, vp, i32, i32, vp, vp, vp, vp]
         L.jl_debug_prefill_tiles.restype = i32
@@ -278,6 +284,40 @@ def rope_attention_decode(q, k_cache, v_cache, kv_lens, *, rope_theta: float = 1
                           workspace=None, stream=None):
     """jl_rope_attention_decode: vanilla RoPE decode with the same kernels."""
     return _decode(False, q, k_cache, v_cache, kv_lens, 1, 0, rope_theta, out, workspace, stream)
+
+
+def decode_paged(q, k_pages, v_pages, block_table, kv_lens, *, w_pretrained: int = 1,
+                 w_local: int = 0, rope_theta: float = 1e6, bifocal: bool = True, out=None,
+                 workspace=None, stream=None):
+    """jl_bifocal_decode_paged / jl_rope_attention_decode_paged: q [B, Hq, 128] raw,
+    pools [n_pages, page_size, Hkv, 128] raw, block_table int32 [B, max_pages],
+    kv_lens int32 [B]."""
+    import torch
+    B, Hq, D = q.shape
+    n_pages, page_size, Hkv, _ = k_pages.shape
+    if k_pages.shape != (n_pages, page_size, Hkv, D) or v_pages.shape != k_pages.shape:
+        raise ValueError("page pools must be [n_pages, page_size, Hkv, D]")
+    if block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError("block_table must be [B, max_pages]")
+    if kv_lens.shape != (B,):
+        raise ValueError("kv_lens must be [B]")
+    max_pages = block_table.shape[1]
+    if out is None:
+        out = torch.empty_like(q)
+    need = decode_workspace_bytes(B, Hq, Hkv, max_pages * page_size, D)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    args = [_dev(q, "q", torch.bfloat16), _dev(k_pages, "k_pages", torch.bfloat16),
+            _dev(v_pages, "v_pages", torch.bfloat16), _dev(block_table, "block_table", torch.int32),
+            max_pages, page_size, n_pages, _dev(kv_lens, "kv_lens", torch.int32),
+            _dev(out, "out", torch.bfloat16), B, Hq, Hkv, D, float(rope_theta)]
+    ws = [_dev(workspace, "workspace"), workspace.numel() * workspace.element_size()]
+    if bifocal:
+        _check(lib().jl_bifocal_decode_paged(*args, int(w_pretrained), int(w_local), *ws,
+                                             _stream(stream)))
+    else:
+        _check(lib().jl_rope_attention_decode_paged(*args, *ws, _stream(stream)))
+    return out
 
 
 def debug_schedule(lengths, positions, w_pretrained: int, stream=None):

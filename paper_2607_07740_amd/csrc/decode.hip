@@ -43,7 +43,12 @@ struct DecodeArgs {
   const int32_t* kv_lens;
   float* ws;
   const float2* table;
-  int B, Hq, Hkv, g, max_len;
+  int B, Hq, Hkv, g, max_len;  // max_len: most keys a sequence can hold
+  // paged caches: kc, vc are pools [n_pages][page_size][Hkv][128] and key k of
+  // sequence b sits in page block_table[b][k >> page_shift]; nullptr: dense
+  // caches [B][max_len][Hkv][128]
+  const int32_t* block_table;
+  int max_pages, n_pages, page_shift;
   int chunk, n_split, n_hgroups;
   int w_pre, w0;
   float q_scale;
@@ -141,11 +146,23 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   // holds (keys past the chunk read the chunk's last key).
   const uint32_t row_bytes = (uint32_t)Hg * 256;
   const uint32_t smem_base = lds_addr(smem);
-  const unsigned char* kseq =
-      (const unsigned char*)(a.kc + ((size_t)b * a.max_len * a.Hkv + h0) * kHeadDim);
-  const unsigned char* vseq =
-      (const unsigned char*)(a.vc + ((size_t)b * a.max_len * a.Hkv + h0) * kHeadDim);
+  const unsigned char* kbase = (const unsigned char*)(a.kc + (size_t)h0 * kHeadDim);
+  const unsigned char* vbase = (const unsigned char*)(a.vc + (size_t)h0 * kHeadDim);
   const uint32_t kv_row_bytes = (uint32_t)a.Hkv * 256;
+  // cache row of step jb's first key: a step's 16 keys are consecutive rows
+  // (pages hold a multiple of 16 keys); page indices are clamped to the pool
+  auto step_row = [&](int jb) {
+    const int k0 = c0 + min(jb, n_steps - 1) * kstride;
+    if (a.block_table == nullptr) return (size_t)b * a.max_len + k0;
+    // the table is read-only for the kernel: read it through the constant
+    // address space, so the load is a scalar one and its wait does not
+    // drain the outstanding copies
+    typedef __attribute__((address_space(4))) const int32_t const_i32;
+    const const_i32* bt = (const const_i32*)a.block_table;
+    int pg = bt[(size_t)b * a.max_pages + (k0 >> a.page_shift)];
+    pg = min(max(pg, 0), a.n_pages - 1);
+    return ((size_t)pg << a.page_shift) + (k0 & ((1 << a.page_shift) - 1));
+  };
   // per copy i of this lane: the key row t it serves and the byte offset of its
   // chunk inside that key's slice of the cache (the same for every step)
   uint32_t cp_t[kDecCopies - 1], cp_off[kDecCopies - 1];
@@ -161,9 +178,11 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     cp_t[i] = t;
     cp_off[i] = h * 256 + 16 * (slot ^ (is_v ? 2 * (t & 7) : t));
   }
-  auto issue = [&](int jb) {
+  auto issue = [&](int jb, size_t row0) {
     const int k0 = c0 + min(jb, n_steps - 1) * kstride;
     const uint32_t buf = smem_base + (jb % kDecBufs) * kDecBufBytes;
+    const unsigned char* kstep = kbase + row0 * kv_row_bytes;
+    const unsigned char* vstep = vbase + row0 * kv_row_bytes;
     {
       // the cos/sin rows that rotate the query columns for this step: q - k0
       // (lanes 0..31) and f(q) - f(k0) (lanes 32..63); one copy, by wave 0
@@ -177,11 +196,11 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
       const int n = wave + kDecWaves * i;  // wave-uniform
       const bool is_v = n >= 4 * Hg;
       const bool real = n < 8 * Hg;
-      const uint32_t key = (uint32_t)min(k0 + (int)cp_t[i], c1 - 1);
+      const uint32_t t = (uint32_t)(min(k0 + (int)cp_t[i], c1 - 1) - k0);  // < 16
       const uint32_t dst = real ? buf + (is_v ? kDecImgBytes + (n - 4 * Hg) * 1024 : n * 1024)
                                 : smem_base + kDecOffDummy;
       // K and V are read exactly once per call: nontemporal
-      dma16_s_nt(is_v && real ? vseq : kseq, key * kv_row_bytes + cp_off[i], dst);
+      dma16_s_nt(is_v && real ? vstep : kstep, t * kv_row_bytes + cp_off[i], dst);
     }
   };
 
@@ -211,7 +230,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   // the plain loads above complete before the first copy is requested, so the
   // compiler's waits for them never hold back the copies
   wait_vmem();
-  for (int jb = 0; jb < 4; ++jb) issue(jb);
+  for (int jb = 0; jb < 4; ++jb) issue(jb, step_row(jb));
 
   f32x4 acc_o[8];
 #pragma unroll
@@ -219,6 +238,9 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   float m_run = -INFINITY, l_run = 0.f;
 
   for (int it = 0; it < n_iter; ++it) {
+    // cache rows of the steps copied at the end of this iteration, looked up
+    // now so the block-table reads are long done by then
+    const size_t row4 = step_row(2 * it + 4), row5 = step_row(2 * it + 5);
     wait_vmem_n<2 * kDecCopies>();  // this wave's copies of steps 2it, 2it+1 (the next pair may fly)
     __syncthreads();  // everyone's copies (and the offset table)
     const int j = 2 * it + par;
@@ -311,8 +333,8 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
       }
     }
     __syncthreads();  // steps 2it, 2it+1 consumed: their buffers take steps 2it+4, 2it+5
-    issue(2 * it + 4);
-    issue(2 * it + 5);
+    issue(2 * it + 4, row4);
+    issue(2 * it + 5, row5);
   }
   wait_vmem();  // copies requested past the last step
   __syncthreads();  // every buffer is free again
@@ -462,10 +484,13 @@ size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len) {
   return (size_t)B * Hq * n_split * kStateFloats * sizeof(float);
 }
 
+// block_table == nullptr: dense caches [B][max_len][Hkv][128]; otherwise
+// pools [n_pages][1 << page_shift][Hkv][128] and max_len = max_pages << page_shift.
 hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                          const int32_t* kv_lens, int max_len, uint16_t* o, const float2* table,
                          int B, int Hq, int Hkv, int w_pre, int w0, float* ws,
-                         hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+                         hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1,
+                         const int32_t* block_table, int max_pages, int n_pages, int page_shift) {
   DecodeArgs a;
   a.q = q;
   a.kc = kc;
@@ -478,6 +503,10 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
   a.Hkv = Hkv;
   a.g = Hq / Hkv;
   a.max_len = max_len;
+  a.block_table = block_table;
+  a.max_pages = max_pages;
+  a.n_pages = n_pages;
+  a.page_shift = page_shift;
   decode_geometry(B, Hkv, max_len, &a.chunk, &a.n_split);
   a.n_hgroups = (Hkv + kDecHeads - 1) / kDecHeads;
   a.w_pre = w_pre;

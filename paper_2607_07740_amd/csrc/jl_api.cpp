@@ -41,7 +41,8 @@ size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len);
 hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                          const int32_t* kv_lens, int max_len, uint16_t* o, const float2* table,
                          int B, int Hq, int Hkv, int w_pre, int w0, float* ws,
-                         hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
+                         hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1,
+                         const int32_t* block_table, int max_pages, int n_pages, int page_shift);
 hipError_t launch_build_table(float2* table, int n_pos, const double* omega, hipStream_t stream);
 hipError_t launch_debug_schedule(const int32_t* lengths, int nl, const int32_t* positions, int np,
                                  int w, int32_t* gout, int32_t* fout, int32_t* dout,
@@ -344,10 +345,28 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   return ok();
 }
 
+// block_table != nullptr: paged pools (kc, vc [n_pages][page_size][Hkv][128],
+// max_len = max_pages * page_size); else dense caches [B][max_len][Hkv][128]
 int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
                   const int32_t* kv_lens, int max_len, void* o, int B, int Hq, int Hkv,
                   int head_dim, double theta, int w_pre, int w0, void* ws, size_t ws_bytes,
-                  void* stream) {
+                  void* stream, const int32_t* block_table = nullptr, int max_pages = 0,
+                  int page_size = 0, int n_pages = 0) {
+  int page_shift = 0;
+  if (block_table != nullptr) {
+    if (!aligned4(block_table))
+      return fail(JL_ERR_INVALID_ARG, "block_table must be 4-byte aligned");
+    if (page_size < 16 || page_size > (1 << 20) || (page_size & (page_size - 1)) != 0)
+      return fail(JL_ERR_INVALID_ARG, "page_size must be a power of two in [16, 2^20] (got %d)",
+                  page_size);
+    if (max_pages < 1 || n_pages < 1)
+      return fail(JL_ERR_INVALID_ARG, "max_pages and n_pages must be >= 1 (got %d, %d)",
+                  max_pages, n_pages);
+    if ((long long)max_pages * page_size > 0x7fffffffLL)
+      return fail(JL_ERR_INVALID_ARG, "max_pages * page_size too large");
+    while ((1 << page_shift) < page_size) ++page_shift;
+    max_len = max_pages * page_size;
+  }
   int st = check_common(B, Hq, Hkv, head_dim, theta);
   if (st != JL_OK) return st;
   if (max_len < 1) return fail(JL_ERR_INVALID_ARG, "max_len must be >= 1 (got %d)", max_len);
@@ -358,8 +377,6 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
     return fail(JL_ERR_INVALID_ARG, "q, k_cache, v_cache, o must be non-null and 16-byte aligned");
   if (!aligned4(kv_lens)) return fail(JL_ERR_INVALID_ARG, "kv_lens must be non-null and aligned");
   if (Hq / Hkv > 8) return fail(JL_ERR_UNSUPPORTED, "decode GQA group %d > 8", Hq / Hkv);
-  if ((long long)max_len * Hkv * kHeadDim * 2 >= (1LL << 32))
-    return fail(JL_ERR_UNSUPPORTED, "one sequence of the cache must stay under 4 GiB");
   const size_t need = jl::decode_workspace_bytes(B, Hq, Hkv, max_len);
   if (ws == nullptr || ws_bytes < need)
     return fail(JL_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
@@ -372,7 +389,8 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
   timing_events(1, &ev0, &ev1);
   hipError_t e = jl::launch_decode(bifocal, (const uint16_t*)q, (const uint16_t*)kc,
                                    (const uint16_t*)vc, kv_lens, max_len, (uint16_t*)o, table, B,
-                                   Hq, Hkv, w_pre, w0, (float*)ws, s, ev0, ev1);
+                                   Hq, Hkv, w_pre, w0, (float*)ws, s, ev0, ev1, block_table,
+                                   max_pages, n_pages, page_shift);
   if (e != hipSuccess) return hip_fail(e, "decode launch");
   return ok();
 }
@@ -483,6 +501,28 @@ int jl_rope_attention_decode(const void* q, const void* k_cache, const void* v_c
                              size_t workspace_bytes, void* stream) {
   return decode_common(false, q, k_cache, v_cache, kv_lens, max_len, o, B, Hq, Hkv, head_dim,
                        rope_theta, 1, 0, workspace, workspace_bytes, stream);
+}
+
+int jl_bifocal_decode_paged(const void* q, const void* k_pages, const void* v_pages,
+                            const int32_t* block_table, int max_pages, int page_size, int n_pages,
+                            const int32_t* kv_lens, void* o, int B, int Hq, int Hkv,
+                            int head_dim, double rope_theta, int w_pretrained, int w_local,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  if (block_table == nullptr) return fail(JL_ERR_INVALID_ARG, "block_table must be non-null");
+  return decode_common(true, q, k_pages, v_pages, kv_lens, 0, o, B, Hq, Hkv, head_dim,
+                       rope_theta, w_pretrained, w_local, workspace, workspace_bytes, stream,
+                       block_table, max_pages, page_size, n_pages);
+}
+
+int jl_rope_attention_decode_paged(const void* q, const void* k_pages, const void* v_pages,
+                                   const int32_t* block_table, int max_pages, int page_size,
+                                   int n_pages, const int32_t* kv_lens, void* o, int B, int Hq,
+                                   int Hkv, int head_dim, double rope_theta, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  if (block_table == nullptr) return fail(JL_ERR_INVALID_ARG, "block_table must be non-null");
+  return decode_common(false, q, k_pages, v_pages, kv_lens, 0, o, B, Hq, Hkv, head_dim,
+                       rope_theta, 1, 0, workspace, workspace_bytes, stream, block_table,
+                       max_pages, page_size, n_pages);
 }
 
 int jl_debug_schedule(const int32_t* lengths, int n_lengths, const int32_t* positions,

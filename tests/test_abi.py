@@ -93,6 +93,22 @@ def test_prefill_chunk_rejects_bad_ranges(q_start, n, max_len):
         assert L.jl_last_error().decode() != ""
 
 
+@pytest.mark.parametrize("kw", [dict(page_size=8), dict(page_size=48), dict(page_size=0),
+                                dict(max_pages=0), dict(n_pages=0), dict(table=None),
+                                dict(table=P(0x1002))])
+def test_decode_paged_rejects_bad_pages(kw):
+    a = dict(table=A2, max_pages=4, page_size=64, n_pages=10)
+    a.update(kw)
+    L = api.lib()
+    rc = L.jl_bifocal_decode_paged(A, A, A, a["table"], a["max_pages"], a["page_size"],
+                                   a["n_pages"], A2, A, 1, 8, 2, 128, 1e6, 64, 8, A, 1 << 20, None)
+    assert rc == api.JL_ERR_INVALID_ARG
+    rc = L.jl_rope_attention_decode_paged(A, A, A, a["table"], a["max_pages"], a["page_size"],
+                                          a["n_pages"], A2, A, 1, 8, 2, 128, 1e6, A, 1 << 20,
+                                          None)
+    assert rc == api.JL_ERR_INVALID_ARG
+
+
 def test_rope_attention_rejects_before_launch():
     L = api.lib()
     assert L.jl_rope_attention(A, A, A, A, None, 1, 4, 2, 0, 128, 1e6, None) == api.JL_ERR_INVALID_ARG
