@@ -113,6 +113,8 @@ def main() -> int:
                     help="decode calls per timed batch")
     ap.add_argument("--literal-reps", type=int, default=2,
                     help="timed calls of the literal three-pass prefill (0 skips it)")
+    ap.add_argument("--paged-reps", type=int, default=3,
+                    help="timed batches of decode calls on a paged copy of the cache (0 skips)")
     ap.add_argument("--freq-reps", type=int, default=1,
                     help="timed calls of the prefill with the frequency-interpolation remote map "
                          "(0 skips it)")
@@ -275,6 +277,29 @@ def main() -> int:
                "literal_throughput_vs_vanilla": round(med(pv) / med(lt), 4),
                "fused_speedup_vs_literal": round(med(lt) / med(pb), 4)}
 
+    # ---- the same decode on a paged cache: 256-key pages in shuffled order
+    pg = {}
+    if args.paged_reps > 0:
+        page = 256
+        n_pg = (wd.L + page - 1) // page
+        perm = torch.randperm(wd.B * n_pg, generator=torch.Generator().manual_seed(0))
+        kc0, vc0 = caches[0]
+        kpool = torch.empty((wd.B * n_pg, page, wd.Hkv, wd.d), dtype=torch.bfloat16, device="cuda")
+        vpool = torch.empty_like(kpool)
+        kpool[perm] = kc0[:, :n_pg * page].reshape(wd.B * n_pg, page, wd.Hkv, wd.d)
+        vpool[perm] = vc0[:, :n_pg * page].reshape(wd.B * n_pg, page, wd.Hkv, wd.d)
+        table = perm.to(torch.int32).reshape(wd.B, n_pg).cuda()
+
+        def paged_batch():
+            for _ in range(args.decode_batch):
+                api.decode_paged(dqd, kpool, vpool, table, lens_d, w_pretrained=wd.w_pretrained,
+                                 w_local=wd.w_local, rope_theta=wd.theta, out=dout, workspace=ws,
+                                 stream=stream)
+        paged_batch()
+        pt = [timed(paged_batch) / args.decode_batch for _ in range(args.paged_reps)]
+        pg = {"decode_paged_us": round(med(pt) * 1e3, 2)}
+        del kpool, vpool
+
     # ---- the Sec. 4.5 ablation's remote view: frequency interpolation
     fm = {}
     if args.freq_reps > 0:
@@ -321,6 +346,7 @@ def main() -> int:
         "vanilla_decode_us": round(med(dv_) * 1e3, 2),
         **lit,
         **fm,
+        **pg,
         "roofline": {
             "bound": "mfma",
             "kernel": "prefill_kernel<fused>",

@@ -32,7 +32,9 @@ constexpr int kDecImgBytes = kDecTile * kDecHeads * kHeadDim * 2;  // K or V of 
 constexpr int kDecBufBytes = 2 * kDecImgBytes + 1024;  // K, V and the step's two query cos/sin rows
 constexpr int kDecOffTab = kDecBufs * kDecBufBytes;
 constexpr int kDecOffDummy = kDecOffTab + kDecTile * kHalf * 8;     // + 16 offset rows (8 KB)
-constexpr int kDecSmem = kDecOffDummy + 1024;                      // + landing slot for padding copies
+constexpr int kDecOffPages = kDecOffDummy + 1024;                  // + landing slot for padding copies
+constexpr int kDecPageCap = 4096;  // paged caches: page indices of up to this many steps in LDS
+constexpr int kDecSmem = kDecOffPages + kDecPageCap * 4;
 constexpr int kDecCopies = 5;  // copies per wave and step (padded to a fixed count)
 constexpr int kStateFloats = 132;  // m, l, 2 pad, O[128]
 
@@ -150,16 +152,26 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   const unsigned char* vbase = (const unsigned char*)(a.vc + (size_t)h0 * kHeadDim);
   const uint32_t kv_row_bytes = (uint32_t)a.Hkv * 256;
   // cache row of step jb's first key: a step's 16 keys are consecutive rows
-  // (pages hold a multiple of 16 keys); page indices are clamped to the pool
-  auto step_row = [&](int jb) {
+  // (pages hold a multiple of 16 keys).  The page index is read first
+  // (step_page) and turned into a row where the copies are issued (step_row),
+  // so the table read overlaps the compute in between; page indices are
+  // clamped to the pool.
+  int32_t* pages_lds = (int32_t*)(smem + kDecOffPages);
+  const bool pages_in_lds = a.block_table != nullptr && n_steps <= kDecPageCap;
+  auto step_page = [&](int jb) {
+    if (a.block_table == nullptr) return 0;
+    if (pages_in_lds) return (int)pages_lds[min(jb, n_steps - 1)];
     const int k0 = c0 + min(jb, n_steps - 1) * kstride;
-    if (a.block_table == nullptr) return (size_t)b * a.max_len + k0;
     // the table is read-only for the kernel: read it through the constant
     // address space, so the load is a scalar one and its wait does not
     // drain the outstanding copies
     typedef __attribute__((address_space(4))) const int32_t const_i32;
     const const_i32* bt = (const const_i32*)a.block_table;
-    int pg = bt[(size_t)b * a.max_pages + (k0 >> a.page_shift)];
+    return (int)bt[(size_t)b * a.max_pages + (k0 >> a.page_shift)];
+  };
+  auto step_row = [&](int jb, int pg) {
+    const int k0 = c0 + min(jb, n_steps - 1) * kstride;
+    if (a.block_table == nullptr) return (size_t)b * a.max_len + k0;
     pg = min(max(pg, 0), a.n_pages - 1);
     return ((size_t)pg << a.page_shift) + (k0 & ((1 << a.page_shift) - 1));
   };
@@ -227,10 +239,19 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     for (int s = 0; s < 4; ++s) qraw[s] = load16(qrow + 32 * s + 8 * g4);
   }
 
+  // paged caches: the page index of every step of this split, into LDS
+  if (pages_in_lds) {
+    for (int j = threadIdx.x; j < n_steps; j += kDecThreads) {
+      const int k0 = c0 + j * kstride;
+      pages_lds[j] = a.block_table[(size_t)b * a.max_pages + (k0 >> a.page_shift)];
+    }
+    __syncthreads();
+  }
+
   // the plain loads above complete before the first copy is requested, so the
   // compiler's waits for them never hold back the copies
   wait_vmem();
-  for (int jb = 0; jb < 4; ++jb) issue(jb, step_row(jb));
+  for (int jb = 0; jb < 4; ++jb) issue(jb, step_row(jb, step_page(jb)));
 
   f32x4 acc_o[8];
 #pragma unroll
@@ -240,7 +261,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   for (int it = 0; it < n_iter; ++it) {
     // cache rows of the steps copied at the end of this iteration, looked up
     // now so the block-table reads are long done by then
-    const size_t row4 = step_row(2 * it + 4), row5 = step_row(2 * it + 5);
+    const int page4 = step_page(2 * it + 4), page5 = step_page(2 * it + 5);
     wait_vmem_n<2 * kDecCopies>();  // this wave's copies of steps 2it, 2it+1 (the next pair may fly)
     __syncthreads();  // everyone's copies (and the offset table)
     const int j = 2 * it + par;
@@ -333,8 +354,8 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
       }
     }
     __syncthreads();  // steps 2it, 2it+1 consumed: their buffers take steps 2it+4, 2it+5
-    issue(2 * it + 4, row4);
-    issue(2 * it + 5, row5);
+    issue(2 * it + 4, step_row(2 * it + 4, page4));
+    issue(2 * it + 5, step_row(2 * it + 5, page5));
   }
   wait_vmem();  // copies requested past the last step
   __syncthreads();  // every buffer is free again
