@@ -145,6 +145,39 @@ int jl_rope_attention_chunk(const void* q, const void* k_cache, const void* v_ca
                             int max_len, int head_dim, double rope_theta, void* stream);
 
 /*
+ * Packed (variable-length) bifocal prefill: B independent sequences of
+ * different lengths in one call, each computed exactly as jl_bifocal_prefill
+ * would compute it alone -- its own L, G = max(1, ceil(L / w_pretrained))
+ * (Eq. (2)), positions 0 .. L - 1, Eq. (3) remote positions and the Eq. (7)
+ * bifocal result (a sequence with G = 1 gets the base model, as there).
+ *   q, o: bf16 [total_tokens, Hq, head_dim]; k, v: bf16 [total_tokens, Hkv,
+ *     head_dim] (raw, before RoPE); sequence s holds rows
+ *     cu_seqlens[s] .. cu_seqlens[s + 1] - 1.
+ *   lse: NULL or fp32 [Hq, total_tokens], natural-log row sums.
+ *   cu_seqlens: DEVICE int32 [B + 1], non-decreasing from 0 to total_tokens
+ *     (read by the kernels only; the call does not synchronise).
+ *   max_seqlen: an upper bound of the sequence lengths; sets the RoPE table
+ *     size.  Longer sequences are cut to their first max_seqlen rows.
+ * Malformed cu_seqlens cannot cause an access outside the tensors: bounds are
+ * clamped into [0, total_tokens] (a decreasing step gives an empty sequence)
+ * and a sequence whose work would not fit the lists sized for well-formed
+ * input is skipped; output rows of skipped, cut or uncovered positions are
+ * left as they were.  Scratch (the library's, per stream): (3 * Hkv *
+ * (ceil(T / 64) + B)) tile images of 16 KB plus two small work lists.  Other
+ * requirements and errors as in jl_bifocal_prefill; only the Eq. (3) map.
+ */
+int jl_bifocal_prefill_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
+                              const int32_t* cu_seqlens, int B, int total_tokens, int max_seqlen,
+                              int Hq, int Hkv, int head_dim, double rope_theta, int w_pretrained,
+                              int w_local, void* stream);
+
+/* The vanilla counterpart of jl_bifocal_prefill_varlen (base rotation only;
+ * two images per tile). */
+int jl_rope_attention_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
+                             const int32_t* cu_seqlens, int B, int total_tokens, int max_seqlen,
+                             int Hq, int Hkv, int head_dim, double rope_theta, void* stream);
+
+/*
  * Vanilla causal RoPE attention with the same tiling and RoPE of raw Q/K at
  * base positions: the base model of Sec. 3 and the denominator of the
  * overhead measurements.  Arguments and scratch as in jl_bifocal_prefill

@@ -57,6 +57,12 @@ def lib() -> ctypes.CDLL:
         L.jl_rope_attention_chunk.restype = i32
         L.jl_rope_attention_chunk.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
                                               i32, dbl, vp]
+        L.jl_bifocal_prefill_varlen.restype = i32
+        L.jl_bifocal_prefill_varlen.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
+                                                i32, dbl, i32, i32, vp]
+        L.jl_rope_attention_varlen.restype = i32
+        L.jl_rope_attention_varlen.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
+                                               i32, dbl, vp]
         L.jl_rope_attention.restype = i32
         L.jl_rope_attention.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl, vp]
         L.jl_prefill_literal_workspace_bytes.restype = sz
@@ -196,6 +202,37 @@ def prefill_chunk(q, k_cache, v_cache, *, q_start: int, w_pretrained: int = 1, w
                                               _stream(stream)))
     else:
         _check(lib().jl_rope_attention_chunk(*args, _stream(stream)))
+    return (out, lse) if want_lse else out
+
+
+def prefill_varlen(q, k, v, cu_seqlens, *, max_seqlen: int, w_pretrained: int = 1,
+                   w_local: int = 0, rope_theta: float = 1e6, bifocal: bool = True, out=None,
+                   lse=None, want_lse: bool = False, stream=None):
+    """jl_bifocal_prefill_varlen / jl_rope_attention_varlen: packed sequences, q [T, Hq, 128],
+    k, v [T, Hkv, 128], cu_seqlens int32 [B + 1] on the device; lse is [Hq, T]."""
+    import torch
+    T, Hq, D = q.shape
+    Hkv = k.shape[1]
+    if k.shape != (T, Hkv, D) or v.shape != k.shape:
+        raise ValueError("k and v must be [T, Hkv, D] matching q [T, Hq, D]")
+    if cu_seqlens.dim() != 1 or cu_seqlens.numel() < 2:
+        raise ValueError("cu_seqlens must be [B + 1] with B >= 1")
+    B = cu_seqlens.numel() - 1
+    if out is None:
+        out = torch.empty_like(q)
+    want_lse = want_lse or lse is not None
+    if lse is None and want_lse:
+        lse = torch.empty((Hq, T), dtype=torch.float32, device=q.device)
+    args = [_dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
+            _dev(v, "v", torch.bfloat16), _dev(out, "out", torch.bfloat16),
+            _dev(lse, "lse", torch.float32) if lse is not None else None,
+            _dev(cu_seqlens, "cu_seqlens", torch.int32), B, T, int(max_seqlen), Hq, Hkv, D,
+            float(rope_theta)]
+    if bifocal:
+        _check(lib().jl_bifocal_prefill_varlen(*args, int(w_pretrained), int(w_local),
+                                               _stream(stream)))
+    else:
+        _check(lib().jl_rope_attention_varlen(*args, _stream(stream)))
     return (out, lse) if want_lse else out
 
 

@@ -28,6 +28,12 @@ hipError_t launch_prefill_chunk(bool bifocal, const uint16_t* q, const uint16_t*
                                 const float2* rtable, int freq_map, int B, int Hq, int Hkv, int L,
                                 int q_start, int Lq, int kv_stride, int G, int w0, float slack,
                                 void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
+size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hkv);
+hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t* k,
+                                 const uint16_t* v, uint16_t* o, float* lse, const float2* table,
+                                 const int32_t* cu, int B, int T, int max_len, int Hq, int Hkv,
+                                 int w_pre, int w0, float slack, void* ws, hipStream_t stream,
+                                 hipEvent_t ev0, hipEvent_t ev1);
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L);
 hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                   uint16_t* o, float* lse, const float2* table,
@@ -345,6 +351,50 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   return ok();
 }
 
+// Packed batch of B sequences, cu_seqlens (device, B + 1) delimiting their
+// rows of the T-row tensors; every sequence is prefilled with its own length.
+int prefill_varlen(bool bifocal, const void* q, const void* k, const void* v, void* o, float* lse,
+                   const int32_t* cu, int B, int T, int max_seqlen, int Hq, int Hkv,
+                   int head_dim, double theta, int w_pre, int w0, void* stream) {
+  int st = check_common(B, Hq, Hkv, head_dim, theta);
+  if (st != JL_OK) return st;
+  if (T < 1) return fail(JL_ERR_INVALID_ARG, "total_tokens must be >= 1 (got %d)", T);
+  if (max_seqlen < 1)
+    return fail(JL_ERR_INVALID_ARG, "max_seqlen must be >= 1 (got %d)", max_seqlen);
+  if (bifocal && w_pre < 1)
+    return fail(JL_ERR_INVALID_ARG, "w_pretrained must be >= 1 (got %d)", w_pre);
+  if (bifocal && w0 < 0) return fail(JL_ERR_INVALID_ARG, "w_local must be >= 0 (got %d)", w0);
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+    return fail(JL_ERR_INVALID_ARG, "q, k, v, o must be non-null and 16-byte aligned");
+  if (lse != nullptr && !aligned4(lse)) return fail(JL_ERR_INVALID_ARG, "lse must be 4-byte aligned");
+  if (!aligned4(cu)) return fail(JL_ERR_INVALID_ARG, "cu_seqlens must be non-null and aligned");
+  const int g = Hq / Hkv;
+  const int rows = jl::prefill_rows_per_block();
+  if (rows % g != 0)
+    return fail(JL_ERR_UNSUPPORTED, "GQA group Hq/Hkv = %d must divide %d", g, rows);
+  const long long nq = ((long long)T + rows / g - 1) / (rows / g) + B;
+  if (nq * Hkv > 0x7fffffffLL || Hkv > 65535)
+    return fail(JL_ERR_INVALID_ARG, "problem too large");
+  const int max_len = std::min(max_seqlen, T);  // no sequence is longer than T
+  const float2* table = nullptr;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  st = get_table(theta, max_len, s, &table);
+  if (st != JL_OK) return st;
+  const float slack = (float)g_rescale_log2.load();
+  std::lock_guard<std::mutex> launch_lock(g_prefill_mu);
+  void* scratch = nullptr;
+  st = get_scratch(s, jl::prefill_varlen_workspace_bytes(bifocal, B, T, Hq, Hkv), &scratch);
+  if (st != JL_OK) return st;
+  hipEvent_t ev0, ev1;
+  timing_events(0, &ev0, &ev1);
+  hipError_t e = jl::launch_prefill_varlen(bifocal, (const uint16_t*)q, (const uint16_t*)k,
+                                           (const uint16_t*)v, (uint16_t*)o, lse, table, cu, B, T,
+                                           max_len, Hq, Hkv, w_pre, w0, slack, scratch, s, ev0,
+                                           ev1);
+  if (e != hipSuccess) return hip_fail(e, "varlen prefill launch");
+  return ok();
+}
+
 // block_table != nullptr: paged pools (kc, vc [n_pages][page_size][Hkv][128],
 // max_len = max_pages * page_size); else dense caches [B][max_len][Hkv][128]
 int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
@@ -467,6 +517,21 @@ int jl_rope_attention_chunk(const void* q, const void* k_cache, const void* v_ca
                             int max_len, int head_dim, double rope_theta, void* stream) {
   return prefill_chunk(false, q, k_cache, v_cache, o, lse, B, Hq, Hkv, q_start, n_queries,
                        max_len, head_dim, rope_theta, 1, 0, stream);
+}
+
+int jl_bifocal_prefill_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
+                              const int32_t* cu_seqlens, int B, int total_tokens, int max_seqlen,
+                              int Hq, int Hkv, int head_dim, double rope_theta, int w_pretrained,
+                              int w_local, void* stream) {
+  return prefill_varlen(true, q, k, v, o, lse, cu_seqlens, B, total_tokens, max_seqlen, Hq, Hkv,
+                        head_dim, rope_theta, w_pretrained, w_local, stream);
+}
+
+int jl_rope_attention_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
+                             const int32_t* cu_seqlens, int B, int total_tokens, int max_seqlen,
+                             int Hq, int Hkv, int head_dim, double rope_theta, void* stream) {
+  return prefill_varlen(false, q, k, v, o, lse, cu_seqlens, B, total_tokens, max_seqlen, Hq, Hkv,
+                        head_dim, rope_theta, 1, 0, stream);
 }
 
 size_t jl_prefill_literal_workspace_bytes(int B, int Hq, int Hkv, int L, int head_dim) {

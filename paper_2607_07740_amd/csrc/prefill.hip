@@ -86,21 +86,44 @@ struct PrepArgs {
   int kv_stride;           // rows per sequence in k and v (>= L)
   int freq_map;            // 0: Eq. (3) aliasing, 1: Sec. 4.5 frequency interpolation
   FastDiv gdiv;
+  // packed variable-length batches: per tile (seq0, L, tile, tile0) with
+  // seq0 the sequence's first row of k and v and tile0 its first tile; the
+  // images of kv head h sit at (h * n_tiles + tile0 + tile); G is the
+  // sequence's own group_size(L, w_pre).  nullptr for dense batches.
+  const int4* twork;
+  int w_pre;
 };
 
-// One workgroup per (tile, b * Hkv + kvh).  Keys past L are written as zeros.
+// One workgroup per (tile, b * Hkv + kvh), or per (tile work item, kvh) for a
+// packed batch.  Keys past the sequence's length are written as zeros.
 template <bool BIFOCAL>
 __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t sv[kPfBK * kHeadDim];
-  const int tile = blockIdx.x;
-  const int bh = blockIdx.y;
-  const int b = bh / a.Hkv, kvh = bh - b * a.Hkv;
+  int tile, L;
+  size_t seq_row, img;
+  FastDiv gdiv = a.gdiv;
+  const int kvh_v = blockIdx.y;
+  if (a.twork != nullptr) {
+    const int4 w = a.twork[blockIdx.x];
+    if (w.y <= 0) return;  // no tile here (uniform, before any barrier)
+    tile = w.z;
+    L = w.y;
+    seq_row = (size_t)w.x;
+    img = ((size_t)kvh_v * a.n_tiles + w.w + tile) * (kTileBytes / 2);
+    gdiv = make_fastdiv((uint32_t)group_size(L, a.w_pre));
+  } else {
+    tile = blockIdx.x;
+    L = a.L;
+    const int b = blockIdx.y / a.Hkv;
+    seq_row = (size_t)b * a.kv_stride;
+    img = ((size_t)blockIdx.y * a.n_tiles + tile) * (kTileBytes / 2);
+  }
+  const int kvh = a.twork != nullptr ? kvh_v : (int)(blockIdx.y % a.Hkv);
   const int t = threadIdx.x;
   const int k0 = tile * kPfBK;
   const size_t row = (size_t)a.Hkv * kHeadDim;
-  const uint16_t* kseq = a.k + ((size_t)b * a.kv_stride * a.Hkv + kvh) * kHeadDim;
-  const uint16_t* vseq = a.v + ((size_t)b * a.kv_stride * a.Hkv + kvh) * kHeadDim;
-  const size_t img = ((size_t)bh * a.n_tiles + tile) * (kTileBytes / 2);
+  const uint16_t* kseq = a.k + (seq_row * a.Hkv + kvh) * kHeadDim;
+  const uint16_t* vseq = a.v + (seq_row * a.Hkv + kvh) * kHeadDim;
 
   // V tile -> LDS, zeros past L
 #pragma unroll
@@ -108,7 +131,7 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
     const int idx = t + 256 * i;  // 64 keys x 16 chunks
     const int r = idx >> 4, c = idx & 15;
     u32x4 w = u32x4{0, 0, 0, 0};
-    if (k0 + r < a.L) w = load16(vseq + (size_t)(k0 + r) * row + 8 * c);
+    if (k0 + r < L) w = load16(vseq + (size_t)(k0 + r) * row + 8 * c);
     *(u32x4*)(sv + r * kHeadDim + 8 * c) = w;
   }
 
@@ -116,7 +139,7 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
   {
     const int r = t >> 2;
     const int key = k0 + r;
-    const bool valid = key < a.L;
+    const bool valid = key < L;
     unsigned char* kl = (unsigned char*)(a.kloc + img);
     unsigned char* kr = BIFOCAL ? (unsigned char*)(a.krem + img) : nullptr;
 #pragma unroll
@@ -128,7 +151,7 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
 #pragma unroll
       for (int view = 0; view < (BIFOCAL ? 2 : 1); ++view) {
         const int kp = valid ? key : 0;
-        const int pos = view == 0 || a.freq_map ? kp : remote_pos(kp, a.gdiv);
+        const int pos = view == 0 || a.freq_map ? kp : remote_pos(kp, gdiv);
         const float2* tab = view == 0 ? a.table : a.rtable;
         const float4* c4 = (const float4*)(tab + (size_t)pos * kHalf + 8 * c);
         float ylo[8], yhi[8];
@@ -185,6 +208,12 @@ struct PrefillArgs {
   float slack;    // log2 units a tile maximum may lie above (or, before anything
                   // was accumulated, below) the reference before it moves (64)
   float* o32;     // window passes: normalised fp32 O_X [B][L][Hq][128]
+  // packed variable-length batch (nullptr otherwise): one (seq0, L, q block,
+  // tile0) per Hkv consecutive workgroups; q and o are [T][Hq][128] with
+  // T = Lq, lse is [Hq][T], the sequence's tile images start at tile0 and
+  // each sequence takes its own G = group_size(L, w_pre)
+  const int4* qwork;
+  int w_pre;
 };
 
 // What one launch of the attention kernel computes.
@@ -257,20 +286,46 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // land on one XCD so a group's K/V tiles stay in that XCD's L2.
   const int n_groups = a.B * a.Hkv;
   const int bid = blockIdx.x;
-  int group, qblk;
-  if ((n_groups & 7) == 0) {
-    const int work = (bid & 7) * (gridDim.x >> 3) + (bid >> 3);
-    group = work / a.n_qblocks;
-    qblk = a.n_qblocks - 1 - (work - group * a.n_qblocks);
+  int kvh, qblk, q_start, q_end, w0;
+  size_t row_base, lse_base, img_base;  // rows of q/o, lse entries, tile image elements
+  FastDiv gdiv;
+  if (a.qwork != nullptr) {
+    // packed batch: the work item's sequence, its G, its tiles; the kv head
+    // follows the XCD (bid & 7) when Hkv divides 8
+    const int item = bid / a.Hkv;
+    kvh = bid - item * a.Hkv;
+    const int4 w = a.qwork[item];
+    if (w.y <= 0) return;  // no query block here (uniform, before any barrier)
+    const int G = FUSED ? group_size(w.y, a.w_pre) : 1;
+    gdiv = make_fastdiv((uint32_t)G);
+    w0 = G > 1 ? a.w0 : INT_MAX;  // G = 1: the unmodified model, as the dense call
+    qblk = w.z;
+    q_start = 0;
+    q_end = w.y;
+    row_base = (size_t)w.x;
+    lse_base = (size_t)w.x;
+    img_base = ((size_t)kvh * a.n_tiles + w.w) * (kTileBytes / 2);
   } else {
-    qblk = a.n_qblocks - 1 - bid / n_groups;
-    group = bid - (bid / n_groups) * n_groups;
+    int group;
+    if ((n_groups & 7) == 0) {
+      const int work = (bid & 7) * (gridDim.x >> 3) + (bid >> 3);
+      group = work / a.n_qblocks;
+      qblk = a.n_qblocks - 1 - (work - group * a.n_qblocks);
+    } else {
+      qblk = a.n_qblocks - 1 - bid / n_groups;
+      group = bid - (bid / n_groups) * n_groups;
+    }
+    const int b = group / a.Hkv;
+    kvh = group - b * a.Hkv;
+    gdiv = a.gdiv;
+    w0 = a.w0;
+    q_start = a.q_start;
+    q_end = a.q_start + a.Lq;  // one past the last query position
+    row_base = (size_t)b * a.Lq;
+    lse_base = (size_t)b * a.Hq * a.Lq;
+    img_base = (size_t)group * a.n_tiles * (kTileBytes / 2);
   }
-  const int b = group / a.Hkv;
-  const int kvh = group - b * a.Hkv;
-  const int q_end = a.q_start + a.Lq;  // one past the last query position
-  const int w0 = a.w0;
-  const int q0 = a.q_start + qblk * a.BQ;
+  const int q0 = q_start + qblk * a.BQ;
   const int q1 = min(q0 + a.BQ, q_end) - 1;
 
   // ---- this lane's query row: column (lane & 31) of the wave's 32
@@ -280,8 +335,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const bool row_valid = qpos < q_end;
   const int qp = row_valid ? qpos : q_end - 1;
   const int hd = kvh * a.g + hl;
-  const int qr = qp - a.q_start;  // row of this query in q, o and lse
-  const uint16_t* qrow = a.q + (((size_t)b * a.Lq + qr) * a.Hq + hd) * kHeadDim;
+  const int qr = qp - q_start;  // row of this query in its sequence's q, o and lse
+  const uint16_t* qrow = a.q + ((row_base + qr) * a.Hq + hd) * kHeadDim;
 
   // ---- visit list: segment 1 = tiles [0, n_r), segment 2 = tiles [kt_l, n_kt)
   const VisitRanges vr = visit_ranges(q0, q1, w0, kPfBK);
@@ -292,7 +347,6 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
 
   // ---- staging: each wave copies its quarter (4 KB) of a K image (k_rem or
   // k_loc) or a V^T image into buffer j & 1 of that kind
-  const size_t img_base = (size_t)group * a.n_tiles * (kTileBytes / 2);
   const uint32_t smem_base = lds_addr(smem);
   const uint32_t lane_off = 16 * lane;
   auto tile_of = [&](int j) __attribute__((always_inline)) { return j < n_r ? j : kt_l + (j - n_r); };
@@ -467,7 +521,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // ---- prologue: the first view's query operand, K(0), V(0), K(1)
   const bool q_remote = n_r > 0 || REMOTE2;
   load_q_operand(qrow, hl32, q_remote ? a.rtable : a.table,
-                 q_remote && !a.freq_map ? remote_pos(qp, a.gdiv) : qp, a.q_scale, qop);
+                 q_remote && !a.freq_map ? remote_pos(qp, gdiv) : qp, a.q_scale, qop);
   issue_k(0);
   issue_v(0);
   if (n_steps > 1) issue_k(1);
@@ -488,7 +542,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (row_valid) {
     const float inv = 1.f / l_tot;
-    const size_t orow_off = (((size_t)b * a.Lq + qr) * a.Hq + hd) * kHeadDim;
+    const size_t orow_off = ((row_base + qr) * a.Hq + hd) * kHeadDim;
 #pragma unroll
     for (int db = 0; db < 4; ++db) {
 #pragma unroll
@@ -504,7 +558,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       }
     }
     if (a.lse != nullptr && hl32 == 0)
-      a.lse[((size_t)b * a.Hq + hd) * a.Lq + qr] = (m_ref + log2f(l_tot)) * 0.69314718055994531f;
+      a.lse[lse_base + (size_t)hd * a.Lq + qr] = (m_ref + log2f(l_tot)) * 0.69314718055994531f;
   }
 }
 
@@ -583,7 +637,7 @@ static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v
   a.freq_map = freq_map;
   a.gdiv = make_fastdiv((uint32_t)G);
 
-  PrepArgs p;
+  PrepArgs p = {};
   p.k = k;
   p.v = v;
   p.kloc = (uint16_t*)a.kloc;
@@ -708,6 +762,184 @@ hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const ui
   if (nblk > 0x7fffffffULL) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL(literal_merge_kernel, dim3((unsigned)nblk), dim3(256), 0, stream, m);
   return hipGetLastError();
+}
+
+// ------------------------------------------------- packed (varlen) batches
+// Sequence s of a packed batch holds rows cu[s] .. cu[s + 1] - 1 of q, k, v
+// and o.  Its bounds are clamped into [0, T] (a non-increasing entry gives an
+// empty sequence) and its length to max_len.  The work lists hold one
+// (seq0, L, index, tile0) per query block (index = block, last block first)
+// and per key tile (index = tile); their sizes nq = ceil(T / BQ) + B and
+// nt = ceil(T / 64) + B bound the totals of any well-formed cu.  A sequence
+// whose entries would run past either list (possible only for malformed
+// cu) gets none: its output rows are left untouched.  Every list entry is
+// written exactly once, unused ones as empty (L = 0).
+struct PlanArgs {
+  const int32_t* cu;
+  int B, T, max_len, BQ;
+  int4* qwork;
+  int4* twork;
+  int nq, nt;
+};
+
+constexpr int kPlanThreads = 1024;
+
+__global__ __launch_bounds__(kPlanThreads) void varlen_plan_kernel(PlanArgs a) {
+  __shared__ long long inc_q[kPlanThreads], inc_t[kPlanThreads];  // inclusive scans
+  __shared__ int s_seq0[kPlanThreads], s_len[kPlanThreads];
+  const int t = threadIdx.x;
+  long long base_q = 0, base_t = 0;  // entries before this chunk of sequences
+  for (int c0 = 0; c0 < a.B; c0 += kPlanThreads) {
+    const int s = c0 + t;
+    int seq0 = 0, len = 0;
+    if (s < a.B) {
+      seq0 = min(max(a.cu[s], 0), a.T);
+      const int seq1 = min(max(a.cu[s + 1], seq0), a.T);
+      len = min(seq1 - seq0, a.max_len);
+    }
+    s_seq0[t] = seq0;
+    s_len[t] = len;
+    inc_q[t] = (len + a.BQ - 1) / a.BQ;
+    inc_t[t] = (len + kPfBK - 1) / kPfBK;
+    __syncthreads();
+    for (int d = 1; d < kPlanThreads; d <<= 1) {  // Hillis-Steele scan
+      const long long xq = t >= d ? inc_q[t - d] : 0;
+      const long long xt = t >= d ? inc_t[t - d] : 0;
+      __syncthreads();
+      inc_q[t] += xq;
+      inc_t[t] += xt;
+      __syncthreads();
+    }
+    const long long tot_q = inc_q[kPlanThreads - 1], tot_t = inc_t[kPlanThreads - 1];
+    // entry e of this chunk belongs to the first sequence whose inclusive
+    // count exceeds e (binary search; sequences without entries are skipped)
+    auto owner = [&](const long long* inc, long long e) {
+      int lo = 0, hi = kPlanThreads - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (inc[mid] > e) hi = mid; else lo = mid + 1;
+      }
+      return lo;
+    };
+    auto fits = [&](int j) {
+      return base_q + inc_q[j] <= a.nq && base_t + inc_t[j] <= a.nt;
+    };
+    for (long long e = t; e < tot_q && base_q + e < a.nq; e += kPlanThreads) {
+      const int j = owner(inc_q, e);
+      const int nb = (s_len[j] + a.BQ - 1) / a.BQ;
+      const long long i = e - (inc_q[j] - nb);
+      const long long toff = base_t + inc_t[j] - (s_len[j] + kPfBK - 1) / kPfBK;
+      a.qwork[base_q + e] = fits(j) ? int4{s_seq0[j], s_len[j], (int)(nb - 1 - i), (int)toff}
+                                    : int4{0, 0, 0, 0};
+    }
+    for (long long e = t; e < tot_t && base_t + e < a.nt; e += kPlanThreads) {
+      const int j = owner(inc_t, e);
+      const int nk = (s_len[j] + kPfBK - 1) / kPfBK;
+      const long long i = e - (inc_t[j] - nk);
+      a.twork[base_t + e] = fits(j) ? int4{s_seq0[j], s_len[j], (int)i, (int)(inc_t[j] - nk + base_t)}
+                                    : int4{0, 0, 0, 0};
+    }
+    base_q += tot_q;
+    base_t += tot_t;
+    __syncthreads();  // the next chunk reuses the scans
+  }
+  for (long long e = min(base_q, (long long)a.nq) + t; e < a.nq; e += kPlanThreads)
+    a.qwork[e] = int4{0, 0, 0, 0};
+  for (long long e = min(base_t, (long long)a.nt) + t; e < a.nt; e += kPlanThreads)
+    a.twork[e] = int4{0, 0, 0, 0};
+}
+
+static void varlen_sizes(int B, int T, int g, long long* nq, long long* nt) {
+  const int BQ = kPfRows / g;
+  *nq = ((long long)T + BQ - 1) / BQ + B;
+  *nt = ((long long)T + kPfBK - 1) / kPfBK + B;
+}
+
+// Scratch of a packed batch: the tile images of nt tiles per kv head (kv head
+// h's at h * nt), then the query-block and tile work lists.
+size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hkv) {
+  long long nq, nt;
+  varlen_sizes(B, T, Hq / Hkv, &nq, &nt);
+  return (size_t)(bifocal ? 3 : 2) * Hkv * nt * kTileBytes + (size_t)(nq + nt) * sizeof(int4);
+}
+
+// Packed batch: q, o [T][Hq][128], k, v [T][Hkv][128], lse [Hq][T] (optional),
+// cu: B + 1 device int32.  Each sequence is prefilled as a call with its own
+// L, G and positions 0 .. L - 1 (table must cover max_len positions).
+hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t* k,
+                                 const uint16_t* v, uint16_t* o, float* lse, const float2* table,
+                                 const int32_t* cu, int B, int T, int max_len, int Hq, int Hkv,
+                                 int w_pre, int w0, float slack, void* ws, hipStream_t stream,
+                                 hipEvent_t ev0, hipEvent_t ev1) {
+  long long nq, nt;
+  varlen_sizes(B, T, Hq / Hkv, &nq, &nt);
+  if (nq * Hkv > 0x7fffffffLL || nt > 0x7fffffffLL || Hkv > 65535)
+    return hipErrorInvalidConfiguration;
+  const size_t img = (size_t)Hkv * nt * (kTileBytes / 2);  // bf16 elements per image set
+  PrefillArgs a = {};
+  fill_geometry(a, 1, Hq, Hkv, max_len, 0, T, slack);
+  a.kloc = (const uint16_t*)ws;
+  a.vt = a.kloc + img;
+  a.krem = bifocal ? a.vt + img : nullptr;
+  int4* qwork = (int4*)((uint16_t*)ws + (bifocal ? 3 : 2) * img);
+  int4* twork = qwork + nq;
+  a.n_tiles = (int)nt;
+  a.table = table;
+  a.rtable = table;
+  a.freq_map = 0;
+  a.gdiv = make_fastdiv(1);
+  a.q = q;
+  a.o = o;
+  a.lse = lse;
+  a.w0 = bifocal ? w0 : INT_MAX;
+  a.qwork = qwork;
+  a.w_pre = w_pre;
+
+  PlanArgs pl;
+  pl.cu = cu;
+  pl.B = B;
+  pl.T = T;
+  pl.max_len = max_len;
+  pl.BQ = a.BQ;
+  pl.qwork = qwork;
+  pl.twork = twork;
+  pl.nq = (int)nq;
+  pl.nt = (int)nt;
+  hipLaunchKernelGGL(varlen_plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, pl);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  PrepArgs p = {};
+  p.k = k;
+  p.v = v;
+  p.kloc = (uint16_t*)a.kloc;
+  p.krem = (uint16_t*)a.krem;
+  p.vt = (uint16_t*)a.vt;
+  p.table = table;
+  p.rtable = table;
+  p.B = 1;
+  p.Hkv = Hkv;
+  p.L = max_len;
+  p.kv_stride = T;
+  p.n_tiles = (int)nt;
+  p.gdiv = a.gdiv;
+  p.twork = twork;
+  p.w_pre = w_pre;
+  if (bifocal)
+    hipLaunchKernelGGL(prep_kernel<true>, dim3((unsigned)nt, Hkv), dim3(256), 0, stream, p);
+  else
+    hipLaunchKernelGGL(prep_kernel<false>, dim3((unsigned)nt, Hkv), dim3(256), 0, stream, p);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+
+  if (ev0 != nullptr && (e = hipEventRecord(ev0, stream)) != hipSuccess) return e;
+  const dim3 grid((unsigned)(nq * Hkv)), block(kPfThreads);
+  if (bifocal)
+    hipLaunchKernelGGL(prefill_kernel<kModeFused>, grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL(prefill_kernel<kModeVanilla>, grid, block, 0, stream, a);
+  e = hipGetLastError();
+  if (e == hipSuccess && ev1 != nullptr) e = hipEventRecord(ev1, stream);
+  return e;
 }
 
 int prefill_rows_per_block() { return kPfRows; }

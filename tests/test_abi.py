@@ -93,6 +93,34 @@ def test_prefill_chunk_rejects_bad_ranges(q_start, n, max_len):
         assert L.jl_last_error().decode() != ""
 
 
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=0), api.JL_ERR_INVALID_ARG),
+    (dict(max_seqlen=0), api.JL_ERR_INVALID_ARG),
+    (dict(cu=None), api.JL_ERR_INVALID_ARG),
+    (dict(cu=P(0x1002)), api.JL_ERR_INVALID_ARG),
+    (dict(B=0), api.JL_ERR_INVALID_ARG),
+    (dict(Hq=12, Hkv=1), api.JL_ERR_UNSUPPORTED),
+    (dict(q=MIS), api.JL_ERR_INVALID_ARG),
+    (dict(lse=P(0x1001)), api.JL_ERR_INVALID_ARG),
+    (dict(w=0), api.JL_ERR_INVALID_ARG),
+    (dict(w0=-1), api.JL_ERR_INVALID_ARG),
+    (dict(T=2 ** 31 - 1, Hkv=1024, Hq=1024), api.JL_ERR_INVALID_ARG),
+])
+def test_prefill_varlen_rejects_before_launch(kw, code):
+    a = dict(q=A, lse=None, cu=A2, B=3, T=300, max_seqlen=200, Hq=8, Hkv=2, w=64, w0=8)
+    a.update(kw)
+    L = api.lib()
+    rc = L.jl_bifocal_prefill_varlen(a["q"], A, A, A, a["lse"], a["cu"], a["B"], a["T"],
+                                     a["max_seqlen"], a["Hq"], a["Hkv"], 128, 1e6, a["w"],
+                                     a["w0"], None)
+    assert rc == code, L.jl_last_error()
+    assert L.jl_last_error().decode() != ""
+    if "w" not in kw and "w0" not in kw:
+        rc = L.jl_rope_attention_varlen(a["q"], A, A, A, a["lse"], a["cu"], a["B"], a["T"],
+                                        a["max_seqlen"], a["Hq"], a["Hkv"], 128, 1e6, None)
+        assert rc == code
+
+
 @pytest.mark.parametrize("kw", [dict(page_size=8), dict(page_size=48), dict(page_size=0),
                                 dict(max_pages=0), dict(n_pages=0), dict(table=None),
                                 dict(table=P(0x1002))])
