@@ -63,10 +63,22 @@ def _dev(bits, torch, np):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
 
 
-def cpu_baseline(q, k, v, w, target_s: float):
-    """Time the oracle (as it stands) on a seeded sample of prefill rows."""
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(q, k, v, w, target_s: float, dec=None):
+    """Time the oracle (as it stands) on a seeded sample of prefill rows; also
+    its full wall time on the tiny prefill and on the decode workload."""
     import numpy as np
     from oracle import oracle as O
+    from paper_2607_07740_amd import synth
     rng = np.random.default_rng(1234)
     g = w.Hq // w.Hkv
 
@@ -91,10 +103,98 @@ def cpu_baseline(q, k, v, w, target_s: float):
     rows = rows_of(n)
     dt, threads = run(rows)
     flops = float(np.sum(4.0 * w.d * (rows[:, 2] + 1)))
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": "%d rows (b=0, heads of kv head 0, uniform positions) of %s, %.1f s wall, "
-                      "includes rotating that kv head's keys" % (n, w.name, dt)}
+    full_s = float(np.sum(4.0 * w.d * w.B * w.Hq * (np.arange(w.L) + 1.0))) / (flops / dt)
+    res = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+           "kind": "oracle",
+           "sample": "%d rows (b=0, heads of kv head 0, uniform positions) of %s, %.1f s wall, "
+                     "includes rotating that kv head's keys" % (n, w.name, dt),
+           "cpu_model": _cpu_model(),
+           "full_prefill_s_extrapolated": round(full_s, 1)}
+    tw = synth.WORKLOADS["tiny_prefill"]
+    tq, tk, tv = synth.make_inputs(tw)
+    t0 = time.perf_counter()
+    O.prefill(tq, tk, tv, theta=tw.theta, w_pretrained=tw.w_pretrained, w_local=tw.w_local)
+    res["tiny_prefill_s"] = round(time.perf_counter() - t0, 3)
+    if dec is not None:
+        dq, dk, dv, lens, wd = dec
+        t0 = time.perf_counter()
+        O.decode(dq, dk, dv, lens, theta=wd.theta, w_pretrained=wd.w_pretrained,
+                 w_local=wd.w_local)
+        res["decode_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
+    return res
+
+
+EXTRA_PREFILL = ["qwen3_8b_prefill_64k", "qwen3_1p7b_prefill_128k", "qwen3_1p7b_within_32k"]
+
+
+def measure_configs(api, synth, torch, np, stream, reps, decode_batch):
+    """The workload list's other configurations, each timed bifocal against the
+    same-build vanilla kernel (interleaved, medians): the 8B-like layer at 64K
+    (G = 2), the 1.7B-like layer at 128K (G = 4), the within-window case
+    (G = 1), and B = 8 decode at the ragged boundary lengths and at seeded
+    uniform lengths in [32768, 131072].  Inputs are drawn on the device."""
+    med = lambda x: sorted(x)[len(x) // 2]
+
+    def timed(fn, n=1):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    res = {}
+    for name in EXTRA_PREFILL:
+        w = synth.WORKLOADS[name]
+        q, k, v = synth.device_inputs(w, torch)
+        out = torch.empty_like(q)
+        bif = lambda: api.bifocal_prefill(q, k, v, w_pretrained=w.w_pretrained, w_local=w.w_local,
+                                          rope_theta=w.theta, out=out, stream=stream)
+        van = lambda: api.rope_attention(q, k, v, rope_theta=w.theta, out=out, stream=stream)
+        bif()
+        van()
+        tb, tv = [], []
+        for _ in range(reps):
+            tv.append(timed(van))
+            tb.append(timed(bif))
+        flops = 4.0 * w.d * w.B * w.Hq * w.L * (w.L + 1) / 2.0
+        res[name] = {"B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "L": w.L,
+                     "G": api.group_size(w.L, w.w_pretrained),
+                     "bifocal_ms": round(med(tb), 3), "vanilla_ms": round(med(tv), 3),
+                     "TFLOPs": round(flops / (med(tb) * 1e-3) / 1e12, 1),
+                     "mfma_frac": round(flops / (med(tb) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                     "overhead_vs_vanilla": round(med(tb) / med(tv) - 1.0, 4)}
+        del q, k, v, out
+    wd = synth.WORKLOADS["qwen3_4b_decode_b8_ragged"]
+    variants = {"qwen3_4b_decode_b8_ragged": list(wd.kv_lens),
+                "qwen3_4b_decode_b8_uniform": [int(x) for x in
+                                               synth.ragged_lengths(8, 32768, 131072, seed=0)]}
+    for name, lens in variants.items():
+        q, kc, vc, ln = synth.device_inputs(wd, torch, kv_lens=lens)
+        lens_d = torch.from_numpy(ln).cuda()
+        out = torch.empty_like(q)
+        ws = torch.empty(api.decode_workspace_bytes(wd.B, wd.Hq, wd.Hkv, wd.L), dtype=torch.uint8,
+                         device="cuda")
+        bif = lambda: api.bifocal_decode(q, kc, vc, lens_d, w_pretrained=wd.w_pretrained,
+                                         w_local=wd.w_local, rope_theta=wd.theta, out=out,
+                                         workspace=ws, stream=stream)
+        van = lambda: api.rope_attention_decode(q, kc, vc, lens_d, rope_theta=wd.theta, out=out,
+                                                workspace=ws, stream=stream)
+        bif()
+        van()
+        tb, tv = [], []
+        for _ in range(max(reps, 5)):
+            tv.append(timed(van, decode_batch))
+            tb.append(timed(bif, decode_batch))
+        nbytes = 2.0 * float(np.sum(ln)) * wd.Hkv * wd.d * 2.0 + 2.0 * wd.B * wd.Hq * wd.d * 2.0
+        gbps = nbytes / (med(tb) * 1e-3) / 1e9
+        res[name] = {"B": wd.B, "kv_lens": lens, "bifocal_us": round(med(tb) * 1e3, 1),
+                     "vanilla_us": round(med(tv) * 1e3, 1), "GBps": round(gbps, 1),
+                     "hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
+                     "overhead_vs_vanilla": round(med(tb) / med(tv) - 1.0, 4)}
+        del q, kc, vc, out, ws
+    return res
 
 
 def main() -> int:
@@ -118,6 +218,9 @@ def main() -> int:
     ap.add_argument("--freq-reps", type=int, default=1,
                     help="timed calls of the prefill with the frequency-interpolation remote map "
                          "(0 skips it)")
+    ap.add_argument("--config-reps", type=int, default=3,
+                    help="timed vanilla/bifocal pairs for each of the other workload "
+                         "configurations (64K, 1.7B-like 128K, within-window, B=8 decode; 0 skips)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -164,7 +267,6 @@ def main() -> int:
     dout = torch.empty_like(dqd)
     ws = torch.empty(api.decode_workspace_bytes(wd.B, wd.Hq, wd.Hkv, wd.L), dtype=torch.uint8,
                      device="cuda")
-    del dk, dv
 
     stream = torch.cuda.current_stream()
 
@@ -310,6 +412,15 @@ def main() -> int:
         ft = [timed(freq_map) for _ in range(args.freq_reps)]
         fm = {"freq_map_prefill_ms": round(med(ft), 3)}
 
+    # ---- decode served warm: the same cache call after call (the Infinity
+    # Cache then holds part of K/V); the primary decode figure above is cold
+    warm = [timed(lambda: [decode(0) for _ in range(args.decode_batch)]) / args.decode_batch
+            for _ in range(max(1, args.decode_reps // 4))]
+
+    cfg = {}
+    if args.config_reps > 0:
+        cfg = measure_configs(api, synth, torch, np, stream, args.config_reps, args.decode_batch)
+
     traffic = _traffic_from_profile()
     line = {
         "metric": METRIC,
@@ -344,6 +455,7 @@ def main() -> int:
         "overhead_decode_vs_vanilla": round(med(db_) / med(dv_) - 1.0, 4),
         "vanilla_prefill_ms": round(med(pv), 3),
         "vanilla_decode_us": round(med(dv_) * 1e3, 2),
+        "decode_warm_us": round(med(warm) * 1e3, 2),
         **lit,
         **fm,
         **pg,
@@ -363,8 +475,11 @@ def main() -> int:
             "frac": round(split_gbps / PEAK_HBM_GBPS, 4), "kernel_us": round(split_avg * 1e3, 2),
         },
     }
+    if cfg:
+        line["configs"] = cfg
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(qh, kh, vh, wp, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(qh, kh, vh, wp, args.cpu_seconds,
+                                            (dq, dk, dv, lens, wd))
     print(json.dumps(line), flush=True)
     return 0
 

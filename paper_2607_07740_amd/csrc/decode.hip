@@ -51,12 +51,107 @@ struct DecodeArgs {
   // caches [B][max_len][Hkv][128]
   const int32_t* block_table;
   int max_pages, n_pages, page_shift;
-  int chunk, n_split, n_hgroups;
+  int chunk, n_split, n_hgroups;  // n_split: split slots per (b, kv-head group)
+  int balanced;  // split counts from the actual lengths (B <= 64), else from max_len
+  int n_target;  // balanced: workgroups of the grid (one wave of them fills the GPU)
   int w_pre, w0;
   float q_scale;
 };
 
 __device__ inline int clamp_len(int n, int max_len) { return n < 1 ? 1 : (n > max_len ? max_len : n); }
+
+__device__ inline int wave_sum(int x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+__device__ inline int wave_max(int x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = max(x, __shfl_xor(x, o));
+  return x;
+}
+
+// 16-key steps of sequence `lane` (0 for lanes past B)
+__device__ inline int lane_steps(const DecodeArgs& a, int lane) {
+  return lane < a.B ? (clamp_len(a.kv_lens[lane], a.max_len) + kDecTile - 1) / kDecTile : 0;
+}
+
+// Balanced splits of a ragged batch (one lane per sequence, s = its steps):
+// every split takes at most u steps, u the smallest count for which the
+// busy workgroups, n_hgroups * sum_b min(n_split, ceil(s_b / u)), fit the
+// grid's n_target slots; the bisection starts from the bounds
+//   ceil(total / S) <= u <= ceil(total / (S - B))   (S = n_target / n_hgroups)
+// since sum_b ceil(s_b / u) lies between total / u and total / u + B.
+__device__ inline int balanced_unit(const DecodeArgs& a, int s) {
+  const int S = a.n_target / a.n_hgroups;  // >= B
+  const int smax = wave_max(s);
+  if (a.B == 1) return max(1, (smax + S - 1) / S);
+  const int total = wave_sum(s);
+  int lo = max(1, (total + S - 1) / S);
+  int hi = S > a.B ? min(smax, (total + S - a.B - 1) / (S - a.B)) : smax;
+  lo = min(lo, hi);
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    const int c = wave_sum(s > 0 ? min(a.n_split, (s + mid - 1) / mid) : 0);
+    if (c <= S) hi = mid; else lo = mid + 1;
+  }
+  return lo;
+}
+
+// What workgroup bid does: sequence b, kv-head group, split `split` of ns
+// (ns == 0: nothing, the workgroup exits).  Balanced grids list, per
+// sequence, its ns_b * n_hgroups workgroups one after another.
+struct SplitWork {
+  int b, hgroup, split, ns;
+};
+
+__device__ inline SplitWork split_work(const DecodeArgs& a, int bid) {
+  SplitWork w;
+  if (!a.balanced) {
+    w.split = bid % a.n_split;
+    const int t0 = bid / a.n_split;
+    w.hgroup = t0 % a.n_hgroups;
+    w.b = t0 / a.n_hgroups;
+    const int s_all = (clamp_len(a.kv_lens[w.b], a.max_len) + kDecTile - 1) / kDecTile;
+    w.ns = min(a.n_split, s_all);
+    if (w.split >= w.ns) w.ns = 0;
+    return w;
+  }
+  const int lane = threadIdx.x & 63;
+  const int s = lane_steps(a, lane);
+  const int u = balanced_unit(a, s);
+  const int ns = s > 0 ? min(a.n_split, (s + u - 1) / u) : 0;
+  int incl = ns * a.n_hgroups;  // inclusive scan over the sequences
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int x = __shfl_up(incl, o);
+    if (lane >= o) incl += x;
+  }
+  const int b = __popcll(__ballot(lane < a.B && incl <= bid));
+  w.b = min(b, a.B - 1);
+  const int incl_b = __shfl(incl, w.b);
+  const int ns_b = __shfl(ns, w.b);
+  const int r = bid - (incl_b - ns_b * a.n_hgroups);
+  w.ns = b < a.B ? ns_b : 0;
+  w.hgroup = w.ns > 0 ? r / ns_b : 0;
+  w.split = w.ns > 0 ? r - w.hgroup * ns_b : 0;
+  w.b = __builtin_amdgcn_readfirstlane(w.b);
+  w.ns = __builtin_amdgcn_readfirstlane(w.ns);
+  w.hgroup = __builtin_amdgcn_readfirstlane(w.hgroup);
+  w.split = __builtin_amdgcn_readfirstlane(w.split);
+  return w;
+}
+
+// Splits holding the states of sequence b (the same count split_work gave it).
+__device__ inline int split_count(const DecodeArgs& a, int b) {
+  if (!a.balanced)
+    return min(a.n_split, (clamp_len(a.kv_lens[b], a.max_len) + kDecTile - 1) / kDecTile);
+  const int s = lane_steps(a, threadIdx.x & 63);
+  const int u = balanced_unit(a, s);
+  const int sb = __shfl(s, b);
+  return __builtin_amdgcn_readfirstlane(min(a.n_split, (sb + u - 1) / u));
+}
 
 // Rotate an 8-element pair of slices (d, d + 64) by the (cos, sin) pairs c4[0..3]
 // (frequencies d..d+7), optional scale.
@@ -116,28 +211,25 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   const int i16 = lane & 15;
   const int g4 = lane >> 4;
 
-  const int bid = blockIdx.x;
-  const int split = bid % a.n_split;
-  const int t0 = bid / a.n_split;
-  const int hgroup = t0 % a.n_hgroups;
-  const int b = t0 / a.n_hgroups;
+  const SplitWork sw = split_work(a, blockIdx.x);
+  if (sw.ns == 0) return;  // whole workgroup, before any barrier
+  const int split = sw.split, hgroup = sw.hgroup, b = sw.b, ns = sw.ns;
   const int h0 = hgroup * kDecHeads;
   const int Hg = min(kDecHeads, a.Hkv - h0);  // heads in this group
   const int kvh = h0 + hw;
   const bool head_on = hw < Hg;
   const int kv_len = clamp_len(a.kv_lens[b], a.max_len);
-  // this split's steps: global 16-key steps split, split + n_split, ... below
+  // this split's steps: global 16-key steps split, split + ns, ... below
   // kv_len, so at any moment all splits read neighbouring parts of the cache
   const int s_all = (kv_len + kDecTile - 1) / kDecTile;
-  if (split >= s_all) return;  // whole workgroup, before any barrier
   const int c1 = kv_len;
-  const int kstride = a.n_split * kDecTile;
+  const int kstride = ns * kDecTile;
   const int c0 = split * kDecTile;
   const int G = BIFOCAL ? group_size(kv_len, a.w_pre) : 1;
   const FastDiv gdiv = make_fastdiv((uint32_t)G);
   const int qpos = kv_len - 1;
   const int fq = BIFOCAL ? remote_pos(qpos, gdiv) : qpos;
-  const int n_steps = (s_all - split + a.n_split - 1) / a.n_split;
+  const int n_steps = (s_all - split + ns - 1) / ns;
   const int n_iter = (n_steps + 1) / 2;
 
   // ---- copies: a step's K image is 16 keys x Hg heads x 256 B = 4 Hg chunks
@@ -430,8 +522,7 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
   const int quarter = blockIdx.y;
   const int b = bh / a.Hq;
   const int tid = threadIdx.x;
-  const int kv_len = clamp_len(a.kv_lens[b], a.max_len);
-  const int ns = min(a.n_split, (kv_len + kDecTile - 1) / kDecTile);  // splits with keys
+  const int ns = split_count(a, b);  // splits with keys
   const float* base = a.ws + (size_t)bh * a.n_split * kStateFloats;
   const int c = tid & 7;
   const int grp = tid >> 3;
@@ -484,19 +575,37 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
 }
 
 // ---------------------------------------------------------------- launcher
+// Batches of up to this many sequences get split counts balanced over their
+// actual lengths (each workgroup computes the plan from kv_lens, one lane
+// per sequence); larger batches split every sequence by max_len.
+constexpr int kDecBalancedMaxB = 64;
+
+// About one workgroup per CU (each holds 157 KB of LDS): enough copies in
+// flight to stream at full bandwidth while keeping few split states for the
+// reduce (at most kRedGroups * kRedPerGroup per head).  Split s takes the
+// 16-key steps s, s + ns, ...; *chunk is the most keys one split covers.
 void decode_geometry(int B, int Hkv, int max_len, int* chunk, int* n_split) {
-  // about one workgroup per CU (256 CUs; each holds 144 KB of LDS): enough
-  // copies in flight to stream at full bandwidth while keeping few split
-  // states for the reduce (at most kRedGroups * kRedPerGroup per head).
-  // Split s takes the 16-key steps s, s + n_split, ...; *chunk is the most
-  // keys one split covers.
   const long long groups = (long long)B * ((Hkv + kDecHeads - 1) / kDecHeads);
-  long long want = (256 + groups - 1) / groups;
-  if (want > kRedGroups * kRedPerGroup) want = kRedGroups * kRedPerGroup;
   const long long steps = ((long long)max_len + kDecTile - 1) / kDecTile;
+  long long want = B <= kDecBalancedMaxB ? kRedGroups * kRedPerGroup : (256 + groups - 1) / groups;
+  if (want > kRedGroups * kRedPerGroup) want = kRedGroups * kRedPerGroup;
   if (want > steps) want = steps;
   *n_split = (int)want;
   *chunk = (int)((steps + want - 1) / want * kDecTile);
+}
+
+static int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n < 1)
+      n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
 }
 
 size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len) {
@@ -530,10 +639,13 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
   a.page_shift = page_shift;
   decode_geometry(B, Hkv, max_len, &a.chunk, &a.n_split);
   a.n_hgroups = (Hkv + kDecHeads - 1) / kDecHeads;
+  a.balanced = B <= kDecBalancedMaxB;
+  const int n_cu = cu_count();
+  a.n_target = n_cu > B * a.n_hgroups ? n_cu : B * a.n_hgroups;
   a.w_pre = w_pre;
   a.w0 = w0;
   a.q_scale = 1.4426950408889634f / sqrtf((float)kHeadDim);
-  const long long nwg = (long long)a.n_split * a.n_hgroups * B;
+  const long long nwg = a.balanced ? (long long)a.n_target : (long long)a.n_split * a.n_hgroups * B;
   if (nwg > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   // ev0 / ev1 (optional) are recorded on the stream around the split kernel
   hipError_t e = hipSuccess;

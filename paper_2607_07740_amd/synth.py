@@ -83,6 +83,31 @@ def ragged_lengths(B: int, lo: int, hi: int, *, seed: int = 0) -> np.ndarray:
     return rng.integers(lo, hi + 1, size=B).astype(np.int32)
 
 
+def device_inputs(w: "Workload", torch, kv_lens: Optional[Sequence[int]] = None):
+    """Timing inputs drawn on the device: torch's seeded CUDA generator
+    (``manual_seed(w.seed)``), ``randn`` float32 in the order Q, K, V, the same
+    outlier-channel scaling of K, then bf16 (torch's round-to-nearest-even).
+    A different random stream from ``make_inputs`` (same distribution and
+    shapes); used where a workload is too large to draw on the host quickly.
+    Prefill: Q [B, L, Hq, d], K, V [B, L, Hkv, d].  Decode: Q [B, Hq, d], caches
+    [B, L, Hkv, d] and the int32 lengths (``kv_lens`` overrides the workload's)."""
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(w.seed)
+    qshape = (w.B, w.L, w.Hq, w.d) if w.kind == "prefill" else (w.B, w.Hq, w.d)
+    kshape = (w.B, w.L, w.Hkv, w.d)
+    q = torch.randn(qshape, generator=gen, device="cuda").to(torch.bfloat16)
+    k = torch.randn(kshape, generator=gen, device="cuda")
+    if w.outlier_channels:
+        ch = np.random.default_rng(w.seed).choice(w.d, w.outlier_channels, replace=False)
+        k[..., torch.from_numpy(ch).cuda()] *= 1.5
+    k = k.to(torch.bfloat16)
+    v = torch.randn(kshape, generator=gen, device="cuda").to(torch.bfloat16)
+    if w.kind == "prefill":
+        return q, k, v
+    lens = np.asarray(kv_lens if kv_lens is not None else w.kv_lens, dtype=np.int32)
+    return q, k, v, lens
+
+
 @dataclass(frozen=True)
 class Workload:
     """One synthetic attention-layer workload (shapes of a Qwen3-like layer)."""

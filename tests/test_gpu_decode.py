@@ -90,3 +90,22 @@ def test_decode_deterministic_and_workspace_contents_irrelevant():
     a = _run(True, q, kc, vc, lens, 1024, 100, ws_fill=float("nan"))
     b = _run(True, q, kc, vc, lens, 1024, 100, ws_fill=0.0)
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+@pytest.mark.parametrize("B", [2, 64, 65])
+def test_decode_batch_split_plans(B):
+    """Split counts balanced over the actual lengths (B <= 64: one short and
+    long sequences side by side, so most workgroups go to the long ones) and
+    the max_len-based split of larger batches (B = 65); NaN tails catch any
+    read past a length."""
+    Hq, Hkv, w_pre, w0, max_len = 8, 8, 512, 100, 4096
+    rng = np.random.default_rng(B)
+    lens = [int(x) for x in rng.integers(1, max_len + 1, size=B)]
+    lens[0], lens[-1] = max_len, 1
+    q, kc, vc, lens = synth.decode_inputs(B, Hq, Hkv, max_len, lens, seed=B, nan_tail=True)
+    say("decode split plans B=%d" % B)
+    for bif in (True, False):
+        out = _run(bif, q, kc, vc, lens, w_pre, w0)
+        want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=w0,
+                              bifocal=bif)
+        assert_close(to_f64(out), want, what="decode B=%d bifocal=%s" % (B, bif))
