@@ -31,7 +31,8 @@ constexpr int kDecBufs = 4;   // LDS buffers: the two steps in use and the next 
 constexpr int kDecImgBytes = kDecTile * kDecHeads * kHeadDim * 2;  // K or V of one step: 16 KB
 constexpr int kDecBufBytes = 2 * kDecImgBytes + 1024;  // K, V and the step's two query cos/sin rows
 constexpr int kDecOffTab = kDecBufs * kDecBufBytes;
-constexpr int kDecOffDummy = kDecOffTab + kDecTile * kHalf * 8;     // + 16 offset rows (8 KB)
+constexpr int kDecTabRow = kHalf * 8 + 16;  // one offset row: 64 (cos, sin) pairs + 16 B pad
+constexpr int kDecOffDummy = kDecOffTab + kDecTile * kDecTabRow;  // + 16 offset rows
 constexpr int kDecOffPages = kDecOffDummy + 1024;                  // + landing slot for padding copies
 constexpr int kDecPageCap = 4096;  // paged caches: page indices of up to this many steps in LDS
 constexpr int kDecSmem = kDecOffPages + kDecPageCap * 4;
@@ -153,6 +154,24 @@ __device__ inline int split_count(const DecodeArgs& a, int b) {
   return __builtin_amdgcn_readfirstlane(min(a.n_split, (sb + u - 1) / u));
 }
 
+// Rotate 8 (d, d + 64) pairs given in fp32 by the (cos, sin) pairs c4[0..3]
+// (frequencies d..d+7).
+__device__ inline void rotate8f(const float* lo, const float* hi, const float4* c4, bf16x8& olo,
+                                bf16x8& ohi) {
+  float ylo[8], yhi[8];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    float4 w = c4[t];
+    int j = 2 * t;
+    ylo[j] = lo[j] * w.x - hi[j] * w.y;
+    yhi[j] = hi[j] * w.x + lo[j] * w.y;
+    ylo[j + 1] = lo[j + 1] * w.z - hi[j + 1] * w.w;
+    yhi[j + 1] = hi[j + 1] * w.z + lo[j + 1] * w.w;
+  }
+  olo = pack8(ylo);
+  ohi = pack8(yhi);
+}
+
 // Rotate an 8-element pair of slices (d, d + 64) by the (cos, sin) pairs c4[0..3]
 // (frequencies d..d+7), optional scale.
 __device__ inline void rotate8(const u32x4 rlo, const u32x4 rhi, const float4* c4, float scale,
@@ -199,7 +218,8 @@ __device__ inline f32x4 mfma16k16(bf16x4 a, bf16x4 b, f32x4 c) {
 // LDS layouts (16-byte slots inside one head's 256-byte row of a key t):
 //   K: slot s holds chunk s ^ t          (16 keys read at one d: 16 bank groups)
 //   V: slot s holds chunk s ^ 2 (t & 7)  (8 keys x 32 B of a transposing read)
-//   offset table row r (512 B): slot s holds frequencies 2 (s ^ r), +1
+//   offset table row r (512 B + 16 B pad, so the 16 rows start 4 banks
+//   apart): slot s holds frequencies 2 s, 2 s + 1
 template <bool BIFOCAL>
 __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kDecSmem];
@@ -313,7 +333,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     unsigned char* tab = smem + kDecOffTab;
     for (int i = threadIdx.x; i < kDecTile * 32; i += kDecThreads) {
       const int r = i >> 5, s = i & 31;
-      *(float4*)(tab + r * 512 + 16 * (s ^ r)) = *(const float4*)(a.table + r * kHalf + 2 * s);
+      *(float4*)(tab + r * kDecTabRow + 16 * s) = *(const float4*)(a.table + r * kHalf + 2 * s);
     }
   }
   const unsigned char* tab = smem + kDecOffTab;
@@ -323,12 +343,26 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   const int view = col >> 3;
   const int hj = col & 7;
   const bool col_on = head_on && hj < a.g && (BIFOCAL || view == 0);
-  u32x4 qraw[4];
+  // distances q - k this column keeps: [keep_lo, keep_lo + keep_n) as one
+  // unsigned compare; base view 0 .. w0 (every causal key for the vanilla
+  // kernel), remote view w0 + 1 .. INT_MAX (Eq. (1)), none for unused columns
+  const int keep_lo = BIFOCAL && view == 1 ? (int)min((uint32_t)a.w0 + 1u, (uint32_t)INT_MAX) : 0;
+  const uint32_t keep_n = !col_on ? 0u
+                          : !BIFOCAL ? 0x80000000u
+                          : view == 0 ? (uint32_t)a.w0 + 1u
+                                      : (uint32_t)INT_MAX - (uint32_t)a.w0;
+  // the raw query slices in fp32, scaled once (log2(e) / sqrt(d)): every
+  // step rotates them by its own offset without unpacking or scaling again
+  float qf[4][8];
   {
     const uint16_t* qrow =
         a.q + ((size_t)b * a.Hq + min(kvh, a.Hkv - 1) * a.g + min(hj, a.g - 1)) * kHeadDim;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) qraw[s] = load16(qrow + 32 * s + 8 * g4);
+    for (int s = 0; s < 4; ++s) {
+      unpack8(load16(qrow + 32 * s + 8 * g4), qf[s]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) qf[s][i] *= a.q_scale;
+    }
   }
 
   // paged caches: the page index of every step of this split, into LDS
@@ -370,7 +404,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
         const float4* c4 = (const float4*)(sb + 2 * kDecImgBytes + 512 * view);
 #pragma unroll
         for (int s = 0; s < 2; ++s)
-          rotate8(qraw[s], qraw[s + 2], c4 + 16 * s + 4 * g4, a.q_scale, qop[s], qop[s + 2]);
+          rotate8f(qf[s], qf[s + 2], c4 + 16 * s + 4 * g4, qop[s], qop[s + 2]);
         if (!col_on) {
 #pragma unroll
           for (int s = 0; s < 4; ++s) qop[s] = bf16x8{};
@@ -392,7 +426,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
           float4 cs[4];
 #pragma unroll
           for (int u = 0; u < 4; ++u)
-            cs[u] = *(const float4*)(tab + r * 512 + 16 * ((16 * s + 4 * g4 + u) ^ r));
+            cs[u] = *(const float4*)(tab + r * kDecTabRow + 16 * (16 * s + 4 * g4 + u));
           bf16x8 lo, hi;
           rotate8(kr[s], kr[s + 2], cs, 1.f, lo, hi);
           sc = mfma16(lo, qop[s], sc);
@@ -400,18 +434,12 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
         }
       }
 
-      // each column keeps only the keys of its own view; lane holds keys 4 g4 + i
+      // each column keeps only the keys of its own view (q - k in [lo, lo +
+      // keep)); lane holds keys 4 g4 + i
       float sv[4];
+      const uint32_t dbase = (uint32_t)(qpos - k0 - 4 * g4) - (uint32_t)keep_lo;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int kk = k0 + 4 * g4 + i;
-        bool ok = col_on && kk < c1;
-        if (BIFOCAL) {
-          const bool local = qpos - kk <= a.w0;
-          ok = ok && (view == 0 ? local : !local);
-        }
-        sv[i] = ok ? sc[i] : -INFINITY;
-      }
+      for (int i = 0; i < 4; ++i) sv[i] = dbase - (uint32_t)i < keep_n ? sc[i] : -INFINITY;
 
       // online softmax per column (the 4 lanes i16, i16+16, i16+32, i16+48)
       float mt = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
