@@ -213,7 +213,7 @@ def main() -> int:
                     help="decode calls per timed batch")
     ap.add_argument("--literal-reps", type=int, default=2,
                     help="timed calls of the literal three-pass prefill (0 skips it)")
-    ap.add_argument("--paged-reps", type=int, default=3,
+    ap.add_argument("--paged-reps", type=int, default=8,
                     help="timed batches of decode calls on a paged copy of the cache (0 skips)")
     ap.add_argument("--freq-reps", type=int, default=1,
                     help="timed calls of the prefill with the frequency-interpolation remote map "
@@ -391,16 +391,25 @@ def main() -> int:
         kpool[perm] = kc0[:, :n_pg * page].reshape(wd.B * n_pg, page, wd.Hkv, wd.d)
         vpool[perm] = vc0[:, :n_pg * page].reshape(wd.B * n_pg, page, wd.Hkv, wd.d)
         table = perm.to(torch.int32).reshape(wd.B, n_pg).cuda()
+        # two pools alternate, as the two dense caches do, so no call is served
+        # from the Infinity Cache
+        pools = [(kpool, vpool), (kpool.clone(), vpool.clone())]
 
         def paged_batch():
-            for _ in range(args.decode_batch):
-                api.decode_paged(dqd, kpool, vpool, table, lens_d, w_pretrained=wd.w_pretrained,
+            for i in range(args.decode_batch):
+                kp, vp = pools[i % 2]
+                api.decode_paged(dqd, kp, vp, table, lens_d, w_pretrained=wd.w_pretrained,
                                  w_local=wd.w_local, rope_theta=wd.theta, out=dout, workspace=ws,
                                  stream=stream)
         paged_batch()
-        pt = [timed(paged_batch) / args.decode_batch for _ in range(args.paged_reps)]
-        pg = {"decode_paged_us": round(med(pt) * 1e3, 2)}
-        del kpool, vpool
+        # interleaved with dense batches, so the ratio compares like with like
+        pt, pd = [], []
+        for _ in range(args.paged_reps):
+            pt.append(timed(paged_batch) / args.decode_batch)
+            pd.append(timed(lambda: decode_batch(True)) / args.decode_batch)
+        pg = {"decode_paged_us": round(med(pt) * 1e3, 2),
+              "decode_paged_vs_dense": round(med(pt) / med(pd), 4)}
+        del kpool, vpool, pools
 
     # ---- the Sec. 4.5 ablation's remote view: frequency interpolation
     fm = {}

@@ -302,6 +302,9 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     cp_t[i] = t;
     cp_off[i] = h * 256 + 16 * (slot ^ (is_v ? 2 * (t & 7) : t));
   }
+  uint32_t cp_full[kDecCopies - 1];  // byte offsets inside a step with 16 valid keys
+#pragma unroll
+  for (int i = 0; i < kDecCopies - 1; ++i) cp_full[i] = cp_t[i] * kv_row_bytes + cp_off[i];
   auto issue = [&](int jb, size_t row0) {
     const int k0 = c0 + min(jb, n_steps - 1) * kstride;
     const uint32_t buf = smem_base + (jb % kDecBufs) * kDecBufBytes;
@@ -315,16 +318,24 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
       const uint32_t off = (uint32_t)row * 512 + 16 * (lane & 31);
       dma16_s(a.table, off, wave == 0 ? buf + 2 * kDecImgBytes : smem_base + kDecOffDummy);
     }
-#pragma unroll
-    for (int i = 0; i < kDecCopies - 1; ++i) {
+    // K and V are read exactly once per call: nontemporal.  A step whose 16
+    // keys all lie below kv_len (every step but a sequence's last) takes the
+    // precomputed offsets; the last one repeats its last key past kv_len.
+    auto copy = [&](int i, uint32_t voff) __attribute__((always_inline)) {
       const int n = wave + kDecWaves * i;  // wave-uniform
       const bool is_v = n >= 4 * Hg;
       const bool real = n < 8 * Hg;
-      const uint32_t t = (uint32_t)(min(k0 + (int)cp_t[i], c1 - 1) - k0);  // < 16
       const uint32_t dst = real ? buf + (is_v ? kDecImgBytes + (n - 4 * Hg) * 1024 : n * 1024)
                                 : smem_base + kDecOffDummy;
-      // K and V are read exactly once per call: nontemporal
-      dma16_s_nt(is_v && real ? vstep : kstep, t * kv_row_bytes + cp_off[i], dst);
+      dma16_s_nt(is_v && real ? vstep : kstep, voff, dst);
+    };
+    if (k0 + kDecTile <= c1) {  // wave-uniform
+#pragma unroll
+      for (int i = 0; i < kDecCopies - 1; ++i) copy(i, cp_full[i]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < kDecCopies - 1; ++i)
+        copy(i, (uint32_t)(min(k0 + (int)cp_t[i], c1 - 1) - k0) * kv_row_bytes + cp_off[i]);
     }
   };
 
