@@ -391,28 +391,38 @@ int jlo_prefill_rows(const uint16_t* q, const uint16_t* k, const uint16_t* v, in
  * Decode: one new query per sequence.  q: bf16 [B, Hq, d] raw, at position
  * kv_lens[b] - 1; k_cache, v_cache: bf16 [B, max_len, Hkv, d] raw (pre-RoPE),
  * only the first kv_lens[b] positions are read.  G per sequence from
- * L = kv_lens[b].  out: fp64 [B, Hq, d]; lse nullable fp64 [B, Hq].
+ * L = kv_lens[b]; so is the frequency map's factor s = max(1, L / w) when
+ * remote_map = 1.  out: fp64 [B, Hq, d]; lse nullable fp64 [B, Hq].
  * Returns threads used (>= 1) or a negative status.
  */
-int jlo_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
-               const int32_t* kv_lens, int max_len, int B, int Hq, int Hkv, int d, double theta,
-               int64_t w_pretrained, int64_t w0, int bifocal, double* out, double* lse) {
+int jlo_decode_map(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                   const int32_t* kv_lens, int max_len, int B, int Hq, int Hkv, int d,
+                   double theta, int64_t w_pretrained, int64_t w0, int bifocal, int remote_map,
+                   double* out, double* lse) {
   if (!check_shape(B, Hq, Hkv, max_len, d, theta)) return -JLO_EINVAL;
   if (bifocal && (w_pretrained < 1 || w0 < 0)) return -JLO_EINVAL;
+  if (remote_map != 0 && remote_map != 1) return -JLO_EINVAL;
   for (int b = 0; b < B; ++b)
     if (kv_lens[b] < 1 || kv_lens[b] > max_len) return -JLO_EINVAL;
   int g = Hq / Hkv;
   int threads = 1;
   int status = JLO_OK;
+  double* romega = NULL;
+  if (bifocal && remote_map == 1) {
+    romega = (double*)malloc(sizeof(double) * (size_t)(d / 2));
+    if (!romega) return -JLO_ENOMEM;
+  }
   for (int b = 0; b < B && status == JLO_OK; ++b) {
     int64_t n = kv_lens[b];
     int64_t G = bifocal ? jlo_group_size(n, w_pretrained) : 1;
+    /* the frequency map's factor follows this sequence's length, as G does */
+    if (romega) jlo_yarn_frequencies(d, theta, (double)n, (double)w_pretrained, 1.0, 32.0, romega);
     for (int kvh = 0; kvh < Hkv && status == JLO_OK; ++kvh) {
       keyset_t ks;
       int64_t kstride = (int64_t)Hkv * d;
       const uint16_t* kbase = k_cache + ((int64_t)b * max_len * Hkv + kvh) * d;
       const uint16_t* vbase = v_cache + ((int64_t)b * max_len * Hkv + kvh) * d;
-      if (keyset_build(&ks, kbase, vbase, n, d, kstride, G, theta, bifocal, NULL) != JLO_OK) {
+      if (keyset_build(&ks, kbase, vbase, n, d, kstride, G, theta, bifocal, romega) != JLO_OK) {
         keyset_free(&ks);
         status = JLO_ENOMEM;
         break;
@@ -430,7 +440,7 @@ int jlo_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
           const uint16_t* qsrc = q + ((int64_t)b * Hq + h) * d;
           for (int c = 0; c < d; ++c) xq[c] = bf16_to_double(qsrc[c]);
           double* o = out + ((int64_t)b * Hq + h) * d;
-          double l = bifocal ? bifocal_row(xq, n - 1, G, w0, theta, &ks, NULL, o)
+          double l = bifocal ? bifocal_row(xq, n - 1, G, w0, theta, &ks, romega, o)
                              : rope_row(xq, n - 1, theta, &ks, o);
           if (lse) lse[(int64_t)b * Hq + h] = l;
         }
@@ -439,7 +449,16 @@ int jlo_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
       keyset_free(&ks);
     }
   }
+  free(romega);
   return status == JLO_OK ? threads : -status;
+}
+
+/* Decode with the aliasing remote map of Eq. (3). */
+int jlo_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+               const int32_t* kv_lens, int max_len, int B, int Hq, int Hkv, int d, double theta,
+               int64_t w_pretrained, int64_t w0, int bifocal, double* out, double* lse) {
+  return jlo_decode_map(q, k_cache, v_cache, kv_lens, max_len, B, Hq, Hkv, d, theta,
+                        w_pretrained, w0, bifocal, 0, out, lse);
 }
 
 /*

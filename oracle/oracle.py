@@ -35,8 +35,7 @@ def build(force: bool = False) -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
-            build()
+        build()  # compiles when the library is missing or older than the source
         lib = ctypes.CDLL(_LIB)
         i64, i32, dbl, vp = ctypes.c_int64, ctypes.c_int, ctypes.c_double, ctypes.c_void_p
         lib.jlo_group_size.restype = i64
@@ -57,6 +56,9 @@ def _load():
         lib.jlo_prefill_rows.restype = i32
         lib.jlo_prefill_rows.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, dbl, i64, i64, i32,
                                          vp, i64, vp, vp]
+        lib.jlo_decode_map.restype = i32
+        lib.jlo_decode_map.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl, i64, i64,
+                                       i32, i32, vp, vp]
         lib.jlo_decode.restype = i32
         lib.jlo_decode.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl, i64, i64, i32,
                                    vp, vp]
@@ -174,18 +176,21 @@ def prefill(q, k, v, *, theta: float, w_pretrained: int = 1, w_local: int = 0,
 
 
 def decode(q, k_cache, v_cache, kv_lens, *, theta: float, w_pretrained: int = 1,
-           w_local: int = 0, bifocal: bool = True):
+           w_local: int = 0, bifocal: bool = True, remote_map: str = "alias"):
     """Oracle decode: q uint16 [B, Hq, d]; caches uint16 [B, max_len, Hkv, d];
-    kv_lens int32 [B].  Returns fp64 [B, Hq, d], LSE fp64 [B, Hq], threads used."""
+    kv_lens int32 [B].  remote_map "alias" (Eq. (3)) or "freq" (Sec. 4.5, with
+    the factor from each sequence's own length).  Returns fp64 [B, Hq, d], LSE
+    fp64 [B, Hq], threads used."""
     q, k_cache, v_cache = _bf16(q), _bf16(k_cache), _bf16(v_cache)
     B, Hq, d = q.shape
     _, max_len, Hkv, _ = k_cache.shape
     kv_lens = np.ascontiguousarray(kv_lens, dtype=np.int32)
     out = np.empty((B, Hq, d), dtype=np.float64)
     lse = np.empty((B, Hq), dtype=np.float64)
-    rc = _load().jlo_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kv_lens), max_len, B,
-                            Hq, Hkv, d, float(theta), int(w_pretrained), int(w_local),
-                            1 if bifocal else 0, _ptr(out), _ptr(lse))
+    rc = _load().jlo_decode_map(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kv_lens), max_len,
+                                B, Hq, Hkv, d, float(theta), int(w_pretrained), int(w_local),
+                                1 if bifocal else 0, REMOTE_MAPS[remote_map], _ptr(out),
+                                _ptr(lse))
     if rc < 0:
         raise ValueError("oracle decode failed with status %d" % -rc)
     return out, lse, rc

@@ -497,3 +497,50 @@ def test_freq_map_literal_merge_equals_mask_form():
         P = np.exp(S - S.max(axis=1, keepdims=True))
         want = (P / P.sum(axis=1, keepdims=True)) @ vf[0, :, 0]
         assert np.max(np.abs(got[0, :, h] - want)) < 1e-11
+
+
+def test_decode_freq_map_equals_prefill_last_row():
+    """Decode with the frequency map at kv_len = L is the last row of the
+    frequency-map prefill of length L (same factor s = L / w), across lengths
+    inside and past the window."""
+    Hq, Hkv, d, theta, w_pre, w0 = 4, 2, 32, 1e4, 24, 6
+    max_len = 3 * w_pre + 2
+    q_all, k_all, v_all = synth.prefill_inputs(1, Hq, Hkv, max_len, d, seed=31)
+    for L in (w_pre - 1, w_pre, w_pre + 1, 2 * w_pre + 5, max_len):
+        lens = np.array([L], np.int32)
+        got, _, _ = O.decode(q_all[:, L - 1].copy(), k_all, v_all, lens, theta=theta,
+                             w_pretrained=w_pre, w_local=w0, remote_map="freq")
+        rows = np.array([[0, h, L - 1] for h in range(Hq)])
+        want, _ = O.prefill_rows(q_all[:, :L].copy(), k_all[:, :L].copy(), v_all[:, :L].copy(),
+                                 rows, theta=theta, w_pretrained=w_pre, w_local=w0,
+                                 remote_map="freq")
+        assert np.array_equal(got[0], want), L
+
+
+def test_decode_freq_map_mask_form_per_sequence_factor():
+    """A ragged batch: each sequence's remote scores use the frequencies of its
+    own length (s_b = kv_len_b / w), written out here as Eq. (1) with the
+    remote pairs rotated by those frequencies."""
+    Hq, Hkv, d, theta, w, w0 = 2, 1, 16, 1e4, 40, 9
+    lens = [30, 41, 97, 160]
+    q, k, v, lens = synth.decode_inputs(4, Hq, Hkv, 160, lens, d, seed=37)
+    got, _, _ = O.decode(q, k, v, lens, theta=theta, w_pretrained=w, w_local=w0,
+                         remote_map="freq")
+    h2 = d // 2
+    for b, n in enumerate(lens):
+        om = O.yarn_frequencies(d, theta, int(n), w)
+        kf, vf = _f64(k)[b, :n, 0], _f64(v)[b, :n, 0]
+        pos = np.arange(n)
+        rotf = lambda x, p: np.concatenate(
+            [((x[..., :h2] + 1j * x[..., h2:]) * np.exp(1j * np.asarray(p)[..., None] * om)).real,
+             ((x[..., :h2] + 1j * x[..., h2:]) * np.exp(1j * np.asarray(p)[..., None] * om)).imag],
+            axis=-1)
+        qpos = n - 1
+        for h in range(Hq):
+            qf = _f64(q)[b, h]
+            base = _complex_rope(kf, pos, theta) @ _complex_rope(qf[None], np.array([qpos]), theta)[0]
+            rem = rotf(kf, pos) @ rotf(qf, qpos)
+            s = np.where(qpos - pos <= w0, base, rem) / math.sqrt(d)
+            p = np.exp(s - s.max())
+            want = (p / p.sum()) @ vf
+            assert np.max(np.abs(got[b, h] - want)) < 1e-11, (b, h)
