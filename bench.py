@@ -420,6 +420,25 @@ def main() -> int:
         freq_map()
         ft = [timed(freq_map) for _ in range(args.freq_reps)]
         fm = {"freq_map_prefill_ms": round(med(ft), 3)}
+        # decode with the frequency map: its rows are built per call from the
+        # device lengths (included), interleaved with the Eq. (3) decode
+        fws = torch.empty(api.decode_map_workspace_bytes(wd.B, wd.Hq, wd.Hkv, wd.L, wd.d, "freq"),
+                          dtype=torch.uint8, device="cuda")
+
+        def freq_decode_batch():
+            for i in range(args.decode_batch):
+                kc, vc = caches[i % 2]
+                api.bifocal_decode(dqd, kc, vc, lens_d, w_pretrained=wd.w_pretrained,
+                                   w_local=wd.w_local, rope_theta=wd.theta, out=dout,
+                                   workspace=fws, stream=stream, remote_map="freq")
+        freq_decode_batch()
+        fdt, adt = [], []
+        for _ in range(max(3, args.decode_reps // 4)):
+            fdt.append(timed(freq_decode_batch) / args.decode_batch)
+            adt.append(timed(lambda: decode_batch(True)) / args.decode_batch)
+        fm["freq_map_decode_us"] = round(med(fdt) * 1e3, 2)
+        fm["freq_map_decode_vs_alias"] = round(med(fdt) / med(adt), 4)
+        del fws
 
     # ---- decode served warm: the same cache call after call (the Infinity
     # Cache then holds part of K/V); the primary decode figure above is cold

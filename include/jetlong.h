@@ -259,6 +259,35 @@ int jl_rope_attention_decode(const void* q, const void* k_cache, const void* v_c
                              size_t workspace_bytes, void* stream);
 
 /*
+ * Bytes of workspace jl_bifocal_decode_map needs: jl_decode_workspace_bytes
+ * for JL_REMOTE_ALIAS; for JL_REMOTE_FREQ that, rounded up to 256, plus
+ * B * (16 + 2 * ceil(max_len / 16)) * 512 bytes of per-sequence cos/sin rows.
+ * Returns 0 for invalid arguments.
+ */
+size_t jl_decode_map_workspace_bytes(int B, int Hq, int Hkv, int max_len, int head_dim,
+                                     int remote_map);
+
+/*
+ * jl_bifocal_decode with a choice of remote map (the Sec. 4.5 / Tab. 6
+ * ablation, as jl_bifocal_prefill_map does for prefill).
+ *   remote_map  JL_REMOTE_ALIAS: identical to jl_bifocal_decode.
+ *               JL_REMOTE_FREQ: remote pairs (q - k > w_local) keep their
+ *               positions and rotate by omega'_i = (1 - gamma_i) omega_i / s +
+ *               gamma_i omega_i (YaRN's ramp, alpha = 1, beta = 32, no
+ *               temperature), with s = max(1, kv_lens[b] / w_pretrained) per
+ *               sequence, so a ragged batch mixes factors the way it mixes G.
+ *               Each call first builds the rows it needs on the device (the
+ *               lengths live there) into the workspace.
+ *   workspace   at least jl_decode_map_workspace_bytes(..., remote_map) bytes,
+ *               16-byte aligned, contents on entry irrelevant.
+ * Other arguments, requirements and errors as in jl_bifocal_decode.
+ */
+int jl_bifocal_decode_map(const void* q, const void* k_cache, const void* v_cache,
+                          const int32_t* kv_lens, int max_len, void* o, int B, int Hq, int Hkv,
+                          int head_dim, double rope_theta, int w_pretrained, int w_local,
+                          int remote_map, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * jl_bifocal_decode on a paged cache: keys and values live in pools of
  * fixed-size pages and each sequence lists its pages in a block table.
  *   k_pages, v_pages bf16 [n_pages, page_size, Hkv, head_dim] raw pools

@@ -63,6 +63,11 @@ def lib() -> ctypes.CDLL:
         L.jl_rope_attention_varlen.restype = i32
         L.jl_rope_attention_varlen.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
                                                i32, dbl, vp]
+        L.jl_decode_map_workspace_bytes.restype = sz
+        L.jl_decode_map_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
+        L.jl_bifocal_decode_map.restype = i32
+        L.jl_bifocal_decode_map.argtypes = [vp, vp, vp, vp, i32, vp, i32, i32, i32, i32, dbl,
+                                            i32, i32, i32, vp, sz, vp]
         L.jl_rope_attention.restype = i32
         L.jl_rope_attention.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, dbl, vp]
         L.jl_prefill_literal_workspace_bytes.restype = sz
@@ -311,10 +316,40 @@ def _decode(bifocal, q, k_cache, v_cache, kv_lens, w_pretrained, w_local, rope_t
 
 
 def bifocal_decode(q, k_cache, v_cache, kv_lens, *, w_pretrained: int, w_local: int,
-                   rope_theta: float = 1e6, out=None, workspace=None, stream=None):
-    """jl_bifocal_decode: q [B, Hq, 128] raw, caches [B, max_len, Hkv, 128] raw, kv_lens int32."""
-    return _decode(True, q, k_cache, v_cache, kv_lens, w_pretrained, w_local, rope_theta, out,
-                   workspace, stream)
+                   rope_theta: float = 1e6, out=None, workspace=None, stream=None,
+                   remote_map: str = "alias"):
+    """jl_bifocal_decode: q [B, Hq, 128] raw, caches [B, max_len, Hkv, 128] raw, kv_lens int32.
+    remote_map "freq" calls jl_bifocal_decode_map with JL_REMOTE_FREQ (Sec. 4.5)."""
+    if remote_map == "alias":
+        return _decode(True, q, k_cache, v_cache, kv_lens, w_pretrained, w_local, rope_theta,
+                       out, workspace, stream)
+    import torch
+    if remote_map not in REMOTE_MAPS:
+        raise ValueError("remote_map must be one of %s" % sorted(REMOTE_MAPS))
+    B, Hq, D = q.shape
+    _, max_len, Hkv, _ = k_cache.shape
+    if k_cache.shape != (B, max_len, Hkv, D) or v_cache.shape != k_cache.shape:
+        raise ValueError("caches must be [B, max_len, Hkv, D]")
+    if kv_lens.shape != (B,):
+        raise ValueError("kv_lens must be [B]")
+    if out is None:
+        out = torch.empty_like(q)
+    need = decode_map_workspace_bytes(B, Hq, Hkv, max_len, D, remote_map)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    _check(lib().jl_bifocal_decode_map(
+        _dev(q, "q", torch.bfloat16), _dev(k_cache, "k_cache", torch.bfloat16),
+        _dev(v_cache, "v_cache", torch.bfloat16), _dev(kv_lens, "kv_lens", torch.int32), max_len,
+        _dev(out, "out", torch.bfloat16), B, Hq, Hkv, D, float(rope_theta), int(w_pretrained),
+        int(w_local), REMOTE_MAPS[remote_map], _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+    return out
+
+
+def decode_map_workspace_bytes(B: int, Hq: int, Hkv: int, max_len: int, head_dim: int = 128,
+                               remote_map: str = "alias") -> int:
+    return int(lib().jl_decode_map_workspace_bytes(B, Hq, Hkv, max_len, head_dim,
+                                                   REMOTE_MAPS[remote_map]))
 
 
 def rope_attention_decode(q, k_cache, v_cache, kv_lens, *, rope_theta: float = 1e6, out=None,

@@ -32,9 +32,10 @@ constexpr int kDecImgBytes = kDecTile * kDecHeads * kHeadDim * 2;  // K or V of 
 constexpr int kDecBufBytes = 2 * kDecImgBytes + 1024;  // K, V and the step's two query cos/sin rows
 constexpr int kDecOffTab = kDecBufs * kDecBufBytes;
 constexpr int kDecTabRow = kHalf * 8 + 16;  // one offset row: 64 (cos, sin) pairs + 16 B pad
-constexpr int kDecOffDummy = kDecOffTab + kDecTile * kDecTabRow;  // + 16 offset rows
+constexpr int kDecOffTab2 = kDecOffTab + kDecTile * kDecTabRow;    // + 16 offset rows (base)
+constexpr int kDecOffDummy = kDecOffTab2 + kDecTile * kDecTabRow;  // + 16 offset rows (freq map)
 constexpr int kDecOffPages = kDecOffDummy + 1024;                  // + landing slot for padding copies
-constexpr int kDecPageCap = 4096;  // paged caches: page indices of up to this many steps in LDS
+constexpr int kDecPageCap = 2048;  // paged caches: page indices of up to this many steps in LDS
 constexpr int kDecSmem = kDecOffPages + kDecPageCap * 4;
 constexpr int kDecCopies = 5;  // copies per wave and step (padded to a fixed count)
 constexpr int kStateFloats = 132;  // m, l, 2 pad, O[128]
@@ -54,6 +55,11 @@ struct DecodeArgs {
   int max_pages, n_pages, page_shift;
   int chunk, n_split, n_hgroups;  // n_split: split slots per (b, kv-head group)
   int balanced;  // split counts from the actual lengths (B <= 64), else from max_len
+  // frequency-interpolation remote map (Sec. 4.5): per sequence, frow_stride
+  // rows of 64 (cos, sin) pairs -- rows 0..15 rotate by t omega'_i, then per
+  // 16-key step m the pair R(q - 16 m) (base) and R'(q - 16 m) (omega')
+  const float2* frows;
+  int frow_stride;
   int n_target;  // balanced: workgroups of the grid (one wave of them fills the GPU)
   int w_pre, w0;
   float q_scale;
@@ -220,8 +226,12 @@ __device__ inline f32x4 mfma16k16(bf16x4 a, bf16x4 b, f32x4 c) {
 //   V: slot s holds chunk s ^ 2 (t & 7)  (8 keys x 32 B of a transposing read)
 //   offset table row r (512 B + 16 B pad, so the 16 rows start 4 banks
 //   apart): slot s holds frequencies 2 s, 2 s + 1
-template <bool BIFOCAL>
+// RMODE: 0 the vanilla kernel, 1 bifocal with the Eq. (3) map, 2 bifocal with
+// the frequency map (remote rotations at unchanged positions by omega').
+template <int RMODE>
 __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs a) {
+  constexpr bool BIFOCAL = RMODE != 0;
+  constexpr bool FREQ = RMODE == 2;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kDecSmem];
 
   const int lane = threadIdx.x & 63;
@@ -249,6 +259,7 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   const FastDiv gdiv = make_fastdiv((uint32_t)G);
   const int qpos = kv_len - 1;
   const int fq = BIFOCAL ? remote_pos(qpos, gdiv) : qpos;
+  const float2* frows_b = FREQ ? a.frows + (size_t)b * a.frow_stride * kHalf : nullptr;
   const int n_steps = (s_all - split + ns - 1) / ns;
   const int n_iter = (n_steps + 1) / 2;
 
@@ -312,11 +323,16 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     const unsigned char* vstep = vbase + row0 * kv_row_bytes;
     {
       // the cos/sin rows that rotate the query columns for this step: q - k0
-      // (lanes 0..31) and f(q) - f(k0) (lanes 32..63); one copy, by wave 0
-      const int fk0 = BIFOCAL ? remote_pos(k0, gdiv) : k0;
-      const int row = lane < 32 ? qpos - k0 : fq - fk0;
-      const uint32_t off = (uint32_t)row * 512 + 16 * (lane & 31);
-      dma16_s(a.table, off, wave == 0 ? buf + 2 * kDecImgBytes : smem_base + kDecOffDummy);
+      // (lanes 0..31) and f(q) - f(k0) (lanes 32..63) of the table, or the
+      // step's row pair of the frequency map; one copy, by wave 0
+      const uint32_t dst = wave == 0 ? buf + 2 * kDecImgBytes : smem_base + kDecOffDummy;
+      if (FREQ) {
+        dma16_s(frows_b, (uint32_t)(kDecTile + 2 * (k0 / kDecTile)) * 512 + 16 * lane, dst);
+      } else {
+        const int fk0 = BIFOCAL ? remote_pos(k0, gdiv) : k0;
+        const int row = lane < 32 ? qpos - k0 : fq - fk0;
+        dma16_s(a.table, (uint32_t)row * 512 + 16 * (lane & 31), dst);
+      }
     }
     // K and V are read exactly once per call: nontemporal.  A step whose 16
     // keys all lie below kv_len (every step but a sequence's last) takes the
@@ -345,6 +361,9 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     for (int i = threadIdx.x; i < kDecTile * 32; i += kDecThreads) {
       const int r = i >> 5, s = i & 31;
       *(float4*)(tab + r * kDecTabRow + 16 * s) = *(const float4*)(a.table + r * kHalf + 2 * s);
+      if (FREQ)
+        *(float4*)(tab + (kDecOffTab2 - kDecOffTab) + r * kDecTabRow + 16 * s) =
+            *(const float4*)(frows_b + r * kHalf + 2 * s);
     }
   }
   const unsigned char* tab = smem + kDecOffTab;
@@ -424,8 +443,11 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
 
       // key t = i16 of this lane, rotated once, by its view's offset
       const int key = k0 + i16;
+      // remote keys: offset f(k) - f(k0) in the base rows (Eq. (3)), or t in
+      // the frequency map's rows
       int r = i16;
-      if (BIFOCAL && qpos - key > a.w0) r = remote_pos(key, gdiv) - fk0;
+      if (BIFOCAL && qpos - key > a.w0)
+        r = FREQ ? i16 + (kDecOffTab2 - kDecOffTab) / kDecTabRow : remote_pos(key, gdiv) - fk0;
       f32x4 sc = f32x4{};
       {
         u32x4 kr[4];
@@ -653,14 +675,63 @@ size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len) {
   return (size_t)B * Hq * n_split * kStateFloats * sizeof(float);
 }
 
+// Rows of the frequency map per sequence: 16 offset rows, then a (base, freq)
+// pair per 16-key step.
+static int freq_row_stride(int max_len) { return kDecTile + 2 * ((max_len + kDecTile - 1) / kDecTile); }
+static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t decode_map_workspace_bytes(int B, int Hq, int Hkv, int max_len, bool freq) {
+  const size_t states = decode_workspace_bytes(B, Hq, Hkv, max_len);
+  if (!freq) return states;
+  return round256(states) + (size_t)B * freq_row_stride(max_len) * kHalf * sizeof(float2);
+}
+
+struct FreqRowsArgs {
+  float2* frows;
+  const int32_t* kv_lens;
+  int max_len, w_pre, stride;
+  double omega[kHalf];  // omega_i = theta^(-2i/d)
+  double gamma[kHalf];  // the ramp of pair i: 0 below alpha turns in the window, 1 above beta
+};
+
+// The frequency map of each sequence from its own length (Sec. 4.5):
+// s = max(1, L / w_pretrained), omega'_i = (1 - gamma_i) omega_i / s +
+// gamma_i omega_i.  Angles and sines in fp64, rounded once to fp32; the base
+// rows equal the RoPE table's rows bit for bit.
+__global__ __launch_bounds__(256) void decode_freq_rows_kernel(FreqRowsArgs a) {
+#pragma clang fp contract(off)
+  const int b = blockIdx.y;
+  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+  const int row = (int)(idx >> 6), i = (int)(idx & 63);
+  if (row >= a.stride) return;
+  const int n = clamp_len(a.kv_lens[b], a.max_len);
+  const double om = a.omega[i];
+  const double sc = fmax(1.0, (double)n / (double)a.w_pre);
+  const double omf = (1.0 - a.gamma[i]) * om / sc + a.gamma[i] * om;
+  double ang;
+  if (row < kDecTile) {
+    ang = (double)row * omf;
+  } else {
+    const int m = (row - kDecTile) >> 1;
+    if (m * kDecTile >= n) return;  // no such step
+    ang = (double)(n - 1 - m * kDecTile) * ((row & 1) ? omf : om);
+  }
+  double sn, cs;
+  sincos(ang, &sn, &cs);
+  a.frows[((size_t)b * a.stride + row) * kHalf + i] = make_float2((float)cs, (float)sn);
+}
+
 // block_table == nullptr: dense caches [B][max_len][Hkv][128]; otherwise
 // pools [n_pages][1 << page_shift][Hkv][128] and max_len = max_pages << page_shift.
 hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                          const int32_t* kv_lens, int max_len, uint16_t* o, const float2* table,
                          int B, int Hq, int Hkv, int w_pre, int w0, float* ws,
                          hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1,
-                         const int32_t* block_table, int max_pages, int n_pages, int page_shift) {
-  DecodeArgs a;
+                         const int32_t* block_table, int max_pages, int n_pages, int page_shift,
+                         const double* freq_og) {
+  // freq_og: nullptr for the Eq. (3) map, else the frequency map's omega_i
+  // (64) and ramp gamma_i (64); its rows follow the states in ws
+  DecodeArgs a = {};
   a.q = q;
   a.kc = kc;
   a.vc = vc;
@@ -686,15 +757,38 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
   a.q_scale = 1.4426950408889634f / sqrtf((float)kHeadDim);
   const long long nwg = a.balanced ? (long long)a.n_target : (long long)a.n_split * a.n_hgroups * B;
   if (nwg > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  // ev0 / ev1 (optional) are recorded on the stream around the split kernel
   hipError_t e = hipSuccess;
+  const bool freq = bifocal && freq_og != nullptr;
+  if (freq) {
+    FreqRowsArgs f;
+    f.frows = (float2*)((unsigned char*)ws +
+                        round256(decode_workspace_bytes(B, Hq, Hkv, max_len)));
+    f.kv_lens = kv_lens;
+    f.max_len = max_len;
+    f.w_pre = w_pre;
+    f.stride = freq_row_stride(max_len);
+    for (int i = 0; i < kHalf; ++i) {
+      f.omega[i] = freq_og[i];
+      f.gamma[i] = freq_og[kHalf + i];
+    }
+    a.frows = f.frows;
+    a.frow_stride = f.stride;
+    const long long blocks = ((long long)f.stride * kHalf + 255) / 256;
+    if (blocks > 0x7fffffffLL || B > 65535) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(decode_freq_rows_kernel, dim3((unsigned)blocks, B), dim3(256), 0, stream, f);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  // ev0 / ev1 (optional) are recorded on the stream around the split kernel
   if (ev0 != nullptr && (e = hipEventRecord(ev0, stream)) != hipSuccess) return e;
-  if (bifocal)
-    hipLaunchKernelGGL(decode_split_kernel<true>, dim3((unsigned)nwg), dim3(kDecThreads), 0,
-                       stream, a);
+  if (freq)
+    hipLaunchKernelGGL(decode_split_kernel<2>, dim3((unsigned)nwg), dim3(kDecThreads), 0, stream,
+                       a);
+  else if (bifocal)
+    hipLaunchKernelGGL(decode_split_kernel<1>, dim3((unsigned)nwg), dim3(kDecThreads), 0, stream,
+                       a);
   else
-    hipLaunchKernelGGL(decode_split_kernel<false>, dim3((unsigned)nwg), dim3(kDecThreads), 0,
-                       stream, a);
+    hipLaunchKernelGGL(decode_split_kernel<0>, dim3((unsigned)nwg), dim3(kDecThreads), 0, stream,
+                       a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (ev1 != nullptr && (e = hipEventRecord(ev1, stream)) != hipSuccess) return e;
   hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq, 4), dim3(256), 0, stream, a, o);

@@ -44,11 +44,13 @@ int prefill_rows_per_block();
 int prefill_block_q(int g);
 int prefill_block_k();
 size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len);
+size_t decode_map_workspace_bytes(int B, int Hq, int Hkv, int max_len, bool freq);
 hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                          const int32_t* kv_lens, int max_len, uint16_t* o, const float2* table,
                          int B, int Hq, int Hkv, int w_pre, int w0, float* ws,
                          hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1,
-                         const int32_t* block_table, int max_pages, int n_pages, int page_shift);
+                         const int32_t* block_table, int max_pages, int n_pages, int page_shift,
+                         const double* freq_og);
 hipError_t launch_build_table(float2* table, int n_pos, const double* omega, hipStream_t stream);
 hipError_t launch_debug_schedule(const int32_t* lengths, int nl, const int32_t* positions, int np,
                                  int w, int32_t* gout, int32_t* fout, int32_t* dout,
@@ -155,16 +157,24 @@ int get_table(double theta, int n_pos, hipStream_t stream, const float2** out) {
 // gamma_i = clamp((r_i - 1) / (32 - 1), 0, 1) and
 // omega'_i = (1 - gamma_i) omega_i / s + gamma_i omega_i.  Fast pairs keep
 // their frequency, slow pairs are divided by s.
-void freq_map_omegas(double theta, int L, int w_pre, double* out) {
+// omega_i and the ramp gamma_i of pair i (og[0..63], og[64..127]); only the
+// factor s depends on the length.
+void freq_map_ramp(double theta, int w_pre, double* og) {
   const double kAlpha = 1.0, kBeta = 32.0;
-  const double s = std::max(1.0, (double)L / (double)w_pre);
   const double two_pi = 2.0 * std::acos(-1.0);
   for (int i = 0; i < 64; ++i) {
     const double omega = std::pow(theta, -2.0 * i / (double)kHeadDim);
     const double r = (double)w_pre / (two_pi / omega);
-    const double gamma = std::min(1.0, std::max(0.0, (r - kAlpha) / (kBeta - kAlpha)));
-    out[i] = (1.0 - gamma) * omega / s + gamma * omega;
+    og[i] = omega;
+    og[64 + i] = std::min(1.0, std::max(0.0, (r - kAlpha) / (kBeta - kAlpha)));
   }
+}
+
+void freq_map_omegas(double theta, int L, int w_pre, double* out) {
+  double og[128];
+  freq_map_ramp(theta, w_pre, og);
+  const double s = std::max(1.0, (double)L / (double)w_pre);
+  for (int i = 0; i < 64; ++i) out[i] = (1.0 - og[64 + i]) * og[i] / s + og[64 + i] * og[i];
 }
 
 // One frequency-map table per device, for the last (theta, L, w_pretrained)
@@ -401,8 +411,12 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
                   const int32_t* kv_lens, int max_len, void* o, int B, int Hq, int Hkv,
                   int head_dim, double theta, int w_pre, int w0, void* ws, size_t ws_bytes,
                   void* stream, const int32_t* block_table = nullptr, int max_pages = 0,
-                  int page_size = 0, int n_pages = 0) {
+                  int page_size = 0, int n_pages = 0, int remote_map = JL_REMOTE_ALIAS) {
   int page_shift = 0;
+  if (remote_map != JL_REMOTE_ALIAS && remote_map != JL_REMOTE_FREQ)
+    return fail(JL_ERR_INVALID_ARG, "remote_map must be JL_REMOTE_ALIAS or JL_REMOTE_FREQ (got %d)",
+                remote_map);
+  const bool freq = bifocal && remote_map == JL_REMOTE_FREQ;
   if (block_table != nullptr) {
     if (!aligned4(block_table))
       return fail(JL_ERR_INVALID_ARG, "block_table must be 4-byte aligned");
@@ -427,7 +441,7 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
     return fail(JL_ERR_INVALID_ARG, "q, k_cache, v_cache, o must be non-null and 16-byte aligned");
   if (!aligned4(kv_lens)) return fail(JL_ERR_INVALID_ARG, "kv_lens must be non-null and aligned");
   if (Hq / Hkv > 8) return fail(JL_ERR_UNSUPPORTED, "decode GQA group %d > 8", Hq / Hkv);
-  const size_t need = jl::decode_workspace_bytes(B, Hq, Hkv, max_len);
+  const size_t need = jl::decode_map_workspace_bytes(B, Hq, Hkv, max_len, freq);
   if (ws == nullptr || ws_bytes < need)
     return fail(JL_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   if (!aligned16(ws)) return fail(JL_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
@@ -435,12 +449,14 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   st = get_table(theta, max_len, s, &table);
   if (st != JL_OK) return st;
+  double og[128];
+  if (freq) freq_map_ramp(theta, w_pre, og);
   hipEvent_t ev0, ev1;
   timing_events(1, &ev0, &ev1);
   hipError_t e = jl::launch_decode(bifocal, (const uint16_t*)q, (const uint16_t*)kc,
                                    (const uint16_t*)vc, kv_lens, max_len, (uint16_t*)o, table, B,
                                    Hq, Hkv, w_pre, w0, (float*)ws, s, ev0, ev1, block_table,
-                                   max_pages, n_pages, page_shift);
+                                   max_pages, n_pages, page_shift, freq ? og : nullptr);
   if (e != hipSuccess) return hip_fail(e, "decode launch");
   return ok();
 }
@@ -545,6 +561,22 @@ int jl_bifocal_prefill_literal(const void* q, const void* k, const void* v, void
                                size_t workspace_bytes, void* stream) {
   return prefill_common(true, q, k, v, o, lse, B, Hq, Hkv, L, head_dim, rope_theta, w_pretrained,
                         w_local, stream, true, workspace, workspace_bytes);
+}
+
+size_t jl_decode_map_workspace_bytes(int B, int Hq, int Hkv, int max_len, int head_dim,
+                                     int remote_map) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || max_len < 1 || head_dim != kHeadDim) return 0;
+  if (remote_map != JL_REMOTE_ALIAS && remote_map != JL_REMOTE_FREQ) return 0;
+  return jl::decode_map_workspace_bytes(B, Hq, Hkv, max_len, remote_map == JL_REMOTE_FREQ);
+}
+
+int jl_bifocal_decode_map(const void* q, const void* k_cache, const void* v_cache,
+                          const int32_t* kv_lens, int max_len, void* o, int B, int Hq, int Hkv,
+                          int head_dim, double rope_theta, int w_pretrained, int w_local,
+                          int remote_map, void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_common(true, q, k_cache, v_cache, kv_lens, max_len, o, B, Hq, Hkv, head_dim,
+                       rope_theta, w_pretrained, w_local, workspace, workspace_bytes, stream,
+                       nullptr, 0, 0, 0, remote_map);
 }
 
 size_t jl_decode_workspace_bytes(int B, int Hq, int Hkv, int max_len, int head_dim) {

@@ -137,6 +137,21 @@ def test_decode_paged_rejects_bad_pages(kw):
     assert rc == api.JL_ERR_INVALID_ARG
 
 
+def test_decode_map_rejects_bad_map_and_small_workspace():
+    L = api.lib()
+    for rm in (-1, 2):
+        assert L.jl_bifocal_decode_map(A, A, A, A2, 1024, A, 1, 8, 2, 128, 1e6, 64, 8, rm, A,
+                                       1 << 30, None) == api.JL_ERR_INVALID_ARG
+        assert L.jl_decode_map_workspace_bytes(1, 8, 2, 1024, 128, rm) == 0
+    alias = L.jl_decode_map_workspace_bytes(1, 8, 2, 1024, 128, 0)
+    freq = L.jl_decode_map_workspace_bytes(1, 8, 2, 1024, 128, 1)
+    assert alias == api.decode_workspace_bytes(1, 8, 2, 1024)
+    assert freq >= alias + (16 + 2 * 64) * 512
+    rc = L.jl_bifocal_decode_map(A, A, A, A2, 1024, A, 1, 8, 2, 128, 1e6, 64, 8, 1, A, freq - 1,
+                                 None)
+    assert rc == api.JL_ERR_WORKSPACE
+
+
 def test_rope_attention_rejects_before_launch():
     L = api.lib()
     assert L.jl_rope_attention(A, A, A, A, None, 1, 4, 2, 0, 128, 1e6, None) == api.JL_ERR_INVALID_ARG

@@ -87,3 +87,72 @@ def test_freq_map_1p7b_128k_sampled_rows():
     got = o[rows[:, 0], rows[:, 2], rows[:, 1]].astype(np.float64)
     assert_close(got, want, what="freq map 128K rows")
     assert np.isfinite(o).all()
+
+
+# ---------------------------------------------------------------- decode
+def _decode_freq(q, kc, vc, lens, w, w0, remote_map="freq", theta=1e6):
+    B, Hq, _ = q.shape
+    Hkv, max_len = kc.shape[2], kc.shape[1]
+    nbytes = api.decode_map_workspace_bytes(B, Hq, Hkv, max_len, 128, remote_map)
+    ws = torch.full((nbytes // 4,), float("nan"), dtype=torch.float32, device="cuda")
+    out = api.bifocal_decode(to_dev(q), to_dev(kc), to_dev(vc),
+                             torch.from_numpy(np.asarray(lens, dtype=np.int32)).cuda(),
+                             w_pretrained=w, w_local=w0, rope_theta=theta, workspace=ws,
+                             remote_map=remote_map)
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("g", [1, 4, 8])
+def test_freq_map_decode_ragged_across_factors(g):
+    """One cache, lengths inside and past the window: every sequence takes the
+    frequencies of its own length (s = kv_len / w), NaN past each length."""
+    Hkv, w_pre, w0 = 2, 96, 20
+    max_len = 4 * w_pre + 40
+    lens = [1, w0 + 1, w_pre, w_pre + 1, 2 * w_pre + 1, 3 * w_pre + 7, max_len]
+    q, kc, vc, lens = synth.decode_inputs(len(lens), g * Hkv, Hkv, max_len, lens, seed=g,
+                                          nan_tail=True, outlier_channels=8)
+    say("freq-map decode g=%d" % g)
+    out = _decode_freq(q, kc, vc, lens, w_pre, w0)
+    want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=w0,
+                          remote_map="freq")
+    assert_close(to_f64(out), want, what="freq decode g=%d" % g)
+    alias, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    assert np.abs(want - alias).max() > 1e-2  # the two maps really differ here
+
+
+def test_freq_map_decode_4b_128k():
+    w = synth.WORKLOADS["qwen3_4b_decode_128k"]
+    say("generating decode 4b 128k")
+    q, kc, vc, lens = synth.make_inputs(w)
+    say("freq-map decode 128k")
+    out = _decode_freq(q, kc, vc, lens, w.w_pretrained, w.w_local)
+    want, _, _ = O.decode(q, kc, vc, lens, theta=w.theta, w_pretrained=w.w_pretrained,
+                          w_local=w.w_local, remote_map="freq")
+    assert_close(to_f64(out), want, what="freq decode 128k")
+
+
+def test_freq_map_decode_matches_prefill_last_row():
+    """Decode at kv_len = L and the frequency-map prefill of length L agree on
+    the last row (both take s = L / w)."""
+    Hq, Hkv, L, w_pre, w0 = 8, 2, 700, 200, 64
+    q, k, v = synth.prefill_inputs(1, Hq, Hkv, L, 128, seed=41, outlier_channels=8)
+    say("freq-map prefill vs decode, L=%d" % L)
+    pre = _run(q, k, v, w_pre, w0, "freq")
+    dec = _decode_freq(q[:, L - 1].copy(), k, v, [L], w_pre, w0)
+    assert_close(to_f64(dec)[0], to_f64(pre)[0, L - 1], max_abs=1e-2, mean_abs=1e-3,
+                 what="decode vs prefill row")
+
+
+def test_freq_map_decode_alias_entry_equals_plain_decode():
+    """jl_bifocal_decode_map with JL_REMOTE_ALIAS is jl_bifocal_decode, bit for bit."""
+    Hq, Hkv, w_pre, w0, max_len = 8, 2, 64, 16, 300
+    lens = [300, 65, 129]
+    q, kc, vc, lens = synth.decode_inputs(3, Hq, Hkv, max_len, lens, seed=43)
+    say("decode map alias entry")
+    a = _decode_freq(q, kc, vc, lens, w_pre, w0, remote_map="alias")
+    b = api.bifocal_decode(to_dev(q), to_dev(kc), to_dev(vc),
+                           torch.from_numpy(np.asarray(lens, dtype=np.int32)).cuda(),
+                           w_pretrained=w_pre, w_local=w0)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
