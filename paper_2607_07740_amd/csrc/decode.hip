@@ -9,7 +9,10 @@
 // ragged batch whose sequences have different G.
 //
 // Split-K: workgroup (b, group of up to 4 kv heads, split) streams every
-// n_split-th 16-key step of the sequence, two waves per kv head.  The g query
+// ns_b-th 16-key step of sequence b, two waves per kv head; ns_b follows the
+// sequence's length (split_work), so a ragged batch keeps every CU busy for
+// about the same time.  The Sec. 4.5 frequency map replaces the remote
+// rotation by one at unchanged positions with rescaled frequencies.  The g query
 // heads of a kv head are rotated twice (base and remote) and placed in the 16
 // columns of a v_mfma_f32_16x16x32_bf16 B operand: columns 0..7 hold
 // the base-rotated heads, 8..15 the remote-rotated ones.  Each key is rotated
