@@ -215,6 +215,8 @@ def main() -> int:
                     help="timed calls of the literal three-pass prefill (0 skips it)")
     ap.add_argument("--paged-reps", type=int, default=8,
                     help="timed batches of decode calls on a paged copy of the cache (0 skips)")
+    ap.add_argument("--varlen-reps", type=int, default=3,
+                    help="timed packed prefills of 131072 tokens in seven sequences (0 skips)")
     ap.add_argument("--freq-reps", type=int, default=1,
                     help="timed calls of the prefill with the frequency-interpolation remote map "
                          "(0 skips it)")
@@ -440,6 +442,40 @@ def main() -> int:
         fm["freq_map_decode_vs_alias"] = round(med(fdt) / med(adt), 4)
         del fws
 
+    # ---- packed variable-length prefill: the prefill layer's 131072 tokens as
+    # seven sequences of 64K .. 1K in one call, against one call per sequence
+    vl = {}
+    if args.varlen_reps > 0:
+        lens = [65536, 32768, 16384, 8192, 4096, 3072, 1024]
+        cu = torch.tensor([0] + list(np.cumsum(lens)), dtype=torch.int32, device="cuda")
+        qv, kv_, vv = q[0], k[0], v[0]  # [T, H, 128] views of the resident inputs
+        ov = out[0]
+
+        def varlen():
+            api.prefill_varlen(qv, kv_, vv, cu, max_seqlen=max(lens), w_pretrained=wp.w_pretrained,
+                               w_local=wp.w_local, rope_theta=wp.theta, out=ov, stream=stream)
+        parts = []
+        for a, b in zip(cu[:-1].tolist(), cu[1:].tolist()):
+            parts.append((q[:, a:b].contiguous(), k[:, a:b].contiguous(), v[:, a:b].contiguous()))
+
+        def separate():
+            for qs, ks, vs in parts:
+                api.bifocal_prefill(qs, ks, vs, w_pretrained=wp.w_pretrained, w_local=wp.w_local,
+                                    rope_theta=wp.theta, stream=stream)
+        varlen()
+        separate()
+        tv_, ts_ = [], []
+        for _ in range(args.varlen_reps):
+            tv_.append(timed(varlen))
+            ts_.append(timed(separate))
+        vfl = sum(4.0 * wp.d * wp.Hq * n * (n + 1) / 2.0 for n in lens)
+        vl = {"varlen_prefill": {"lens": lens, "ms": round(med(tv_), 3),
+                                 "TFLOPs": round(vfl / (med(tv_) * 1e-3) / 1e12, 1),
+                                 "mfma_frac": round(vfl / (med(tv_) * 1e-3) / 1e12 /
+                                                    PEAK_BF16_TFLOPS, 4),
+                                 "separate_calls_ms": round(med(ts_), 3)}}
+        del parts
+
     # ---- decode served warm: the same cache call after call (the Infinity
     # Cache then holds part of K/V); the primary decode figure above is cold
     warm = [timed(lambda: [decode(0) for _ in range(args.decode_batch)]) / args.decode_batch
@@ -487,6 +523,7 @@ def main() -> int:
         **lit,
         **fm,
         **pg,
+        **vl,
         "roofline": {
             "bound": "mfma",
             "kernel": "prefill_kernel<fused>",

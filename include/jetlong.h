@@ -261,7 +261,7 @@ int jl_rope_attention_decode(const void* q, const void* k_cache, const void* v_c
 /*
  * Bytes of workspace jl_bifocal_decode_map needs: jl_decode_workspace_bytes
  * for JL_REMOTE_ALIAS; for JL_REMOTE_FREQ that, rounded up to 256, plus
- * B * (16 + 2 * ceil(max_len / 16)) * 512 bytes of per-sequence cos/sin rows.
+ * B * (16 + ceil(max_len / 16)) * 512 bytes of per-sequence cos/sin rows.
  * Returns 0 for invalid arguments.
  */
 size_t jl_decode_map_workspace_bytes(int B, int Hq, int Hkv, int max_len, int head_dim,

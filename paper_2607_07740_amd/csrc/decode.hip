@@ -60,7 +60,7 @@ struct DecodeArgs {
   int balanced;  // split counts from the actual lengths (B <= 64), else from max_len
   // frequency-interpolation remote map (Sec. 4.5): per sequence, frow_stride
   // rows of 64 (cos, sin) pairs -- rows 0..15 rotate by t omega'_i, then per
-  // 16-key step m the pair R(q - 16 m) (base) and R'(q - 16 m) (omega')
+  // 16-key step m the row R'(q - 16 m) (omega')
   const float2* frows;
   int frow_stride;
   int n_target;  // balanced: workgroups of the grid (one wave of them fills the GPU)
@@ -330,7 +330,12 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
       // step's row pair of the frequency map; one copy, by wave 0
       const uint32_t dst = wave == 0 ? buf + 2 * kDecImgBytes : smem_base + kDecOffDummy;
       if (FREQ) {
-        dma16_s(frows_b, (uint32_t)(kDecTile + 2 * (k0 / kDecTile)) * 512 + 16 * lane, dst);
+        // two half-wave copies (each lane's LDS slot is fixed by its lane id):
+        // the base row from the table, the step's row of the frequency map
+        if (lane < 32)
+          dma16_s(a.table, (uint32_t)(qpos - k0) * 512 + 16 * lane, dst);
+        else
+          dma16_s(frows_b, (uint32_t)(kDecTile + k0 / kDecTile) * 512 + 16 * (lane - 32), dst);
       } else {
         const int fk0 = BIFOCAL ? remote_pos(k0, gdiv) : k0;
         const int row = lane < 32 ? qpos - k0 : fq - fk0;
@@ -421,7 +426,9 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     // cache rows of the steps copied at the end of this iteration, looked up
     // now so the block-table reads are long done by then
     const int page4 = step_page(2 * it + 4), page5 = step_page(2 * it + 5);
-    wait_vmem_n<2 * kDecCopies>();  // this wave's copies of steps 2it, 2it+1 (the next pair may fly)
+    // this wave's copies of steps 2it, 2it+1 (the next pair may fly); the
+    // frequency map copies its query rows in two instructions
+    wait_vmem_n<2 * (kDecCopies + (FREQ ? 1 : 0))>();
     __syncthreads();  // everyone's copies (and the offset table)
     const int j = 2 * it + par;
     if (head_on && j < n_steps) {
@@ -678,9 +685,9 @@ size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len) {
   return (size_t)B * Hq * n_split * kStateFloats * sizeof(float);
 }
 
-// Rows of the frequency map per sequence: 16 offset rows, then a (base, freq)
-// pair per 16-key step.
-static int freq_row_stride(int max_len) { return kDecTile + 2 * ((max_len + kDecTile - 1) / kDecTile); }
+// Rows of the frequency map per sequence: 16 offset rows, then one row per
+// 16-key step.
+static int freq_row_stride(int max_len) { return kDecTile + (max_len + kDecTile - 1) / kDecTile; }
 static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t decode_map_workspace_bytes(int B, int Hq, int Hkv, int max_len, bool freq) {
@@ -699,8 +706,9 @@ struct FreqRowsArgs {
 
 // The frequency map of each sequence from its own length (Sec. 4.5):
 // s = max(1, L / w_pretrained), omega'_i = (1 - gamma_i) omega_i / s +
-// gamma_i omega_i.  Angles and sines in fp64, rounded once to fp32; the base
-// rows equal the RoPE table's rows bit for bit.
+// gamma_i omega_i.  The angle is formed and reduced modulo 2 pi in fp64
+// (exact to ~1e-11 rad at 1.3e5 rad), then its sine and cosine are taken in
+// fp32, within an ulp or two of the fp64 result rounded to fp32.
 __global__ __launch_bounds__(256) void decode_freq_rows_kernel(FreqRowsArgs a) {
 #pragma clang fp contract(off)
   const int b = blockIdx.y;
@@ -711,17 +719,18 @@ __global__ __launch_bounds__(256) void decode_freq_rows_kernel(FreqRowsArgs a) {
   const double om = a.omega[i];
   const double sc = fmax(1.0, (double)n / (double)a.w_pre);
   const double omf = (1.0 - a.gamma[i]) * om / sc + a.gamma[i] * om;
-  double ang;
-  if (row < kDecTile) {
-    ang = (double)row * omf;
-  } else {
-    const int m = (row - kDecTile) >> 1;
+  int pos = row;
+  if (row >= kDecTile) {
+    const int m = row - kDecTile;
     if (m * kDecTile >= n) return;  // no such step
-    ang = (double)(n - 1 - m * kDecTile) * ((row & 1) ? omf : om);
+    pos = n - 1 - m * kDecTile;
   }
-  double sn, cs;
-  sincos(ang, &sn, &cs);
-  a.frows[((size_t)b * a.stride + row) * kHalf + i] = make_float2((float)cs, (float)sn);
+  const double two_pi = 6.283185307179586476925286766559;
+  double ang = (double)pos * omf;
+  ang -= two_pi * rint(ang * (1.0 / two_pi));
+  float sn, cs;
+  sincosf((float)ang, &sn, &cs);
+  a.frows[((size_t)b * a.stride + row) * kHalf + i] = make_float2(cs, sn);
 }
 
 // block_table == nullptr: dense caches [B][max_len][Hkv][128]; otherwise
