@@ -459,27 +459,33 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
     return psum;
   };
-  // Reference check, before the tile's softmax: the reference moves when
-  // the tile's largest (relative) score in a column exceeds it by more than
-  // the slack (exp2 could overflow), or, before anything was accumulated,
-  // lies more than the slack below it (everything could underflow).  The
-  // common path is a per-lane maximum and one ballot; the rare path settles
-  // each column (both lane halves), re-bases the tile's scores and rescales
-  // the running state.
-  auto ref_check = [&](f32x16* sc) __attribute__((always_inline)) {
+  // Reference check, after the tile's softmax: the reference moves when a
+  // tile probability in a column could exceed 2^slack (their sum does: exp2
+  // could overflow), or, before anything was accumulated, when the tile's
+  // probabilities sum below 2^-slack (everything could underflow).  The
+  // common path is one compare of the sum the softmax already formed and one
+  // ballot; the rare path settles each column's maximum (both lane halves),
+  // re-bases the tile's scores and the next tile's (computed against the old
+  // reference), rescales the running state and redoes the tile's softmax.
+  const float p_hi = exp2f(a.slack), p_lo = exp2f(-a.slack);
+  auto ref_fix = [&](f32x16* sc, f32x16* nx, bf16x8* pb, float& ps) __attribute__((always_inline)) {
+    const bool bad = ps > p_hi || (l_run == 0.f && ps < p_lo);
+    if (__ballot(bad) == 0) return;
     float mt = -INFINITY;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mt = fmaxf(mt, sc[blk][i]);
-    const bool bad = mt > a.slack || (l_run == 0.f && mt < -a.slack && mt != -INFINITY);
-    if (__ballot(bad) == 0) return;
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     const float lc = l_run + __shfl_xor(l_run, 32);
     const bool upd = mt != -INFINITY && (mt > a.slack || (lc == 0.f && mt < -a.slack));
+    if (__ballot(upd) == 0) return;
     const float shift = upd ? mt : 0.f;
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) sc[blk] -= shift;
+    for (int blk = 0; blk < 2; ++blk) {
+      sc[blk] -= shift;
+      nx[blk] -= shift;
+    }
     // a downward move only happens before anything was accumulated (lc == 0)
     const float alpha = lc == 0.f ? 1.f : fast_exp2(-shift);
     if (__ballot(upd && lc != 0.f) != 0) {
@@ -490,6 +496,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     m_ref += shift;
 #pragma unroll
     for (int i = 0; i < 16; ++i) neg_m[i] = -m_ref;
+    ps = softmax(sc, pb);
   };
 
   // One pipelined visit: on entry `cur` holds the scores of tile j, this
@@ -499,14 +506,15 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // QK product reads whatever the next K buffer holds and is discarded.
   auto visit = [&](int j, f32x16* cur, f32x16* nxt) __attribute__((always_inline)) {
     if (need_mask(j)) mask(j, cur);
-    ref_check(cur);
     wait_vmem();      // this wave's copies of K(j+1), V(j)
     __syncthreads();  // everyone's; QK(j) and PV(j-1) are done everywhere
     if (j + 2 < n_steps) issue_k(j + 2);
     if (j + 1 < n_steps) issue_v(j + 1);
     bf16x8 pb[4];
     qk(kbuf(j + 1), nxt);
-    l_run += softmax(cur, pb);
+    float ps = softmax(cur, pb);
+    ref_fix(cur, nxt, pb, ps);
+    l_run += ps;
     pv(vbuf(j), pb);
   };
   // segment [j, jend): the first tile's scores are in sc_a on entry
