@@ -121,6 +121,21 @@ def cpu_baseline(q, k, v, w, target_s: float, dec=None):
         O.decode(dq, dk, dv, lens, theta=wd.theta, w_pretrained=wd.w_pretrained,
                  w_local=wd.w_local)
         res["decode_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
+    # the B = 8 ragged decode: inputs drawn on the device and copied to the host
+    try:
+        import torch
+        w8 = synth.WORKLOADS["qwen3_4b_decode_b8_ragged"]
+        host = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)
+        q8, k8, v8, l8 = synth.device_inputs(w8, torch)
+        q8, k8, v8 = host(q8), host(k8), host(v8)
+        torch.cuda.empty_cache()
+        t0 = time.perf_counter()
+        O.decode(q8, k8, v8, l8, theta=w8.theta, w_pretrained=w8.w_pretrained,
+                 w_local=w8.w_local)
+        res["decode_b8_ragged_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
+        del q8, k8, v8
+    except (ImportError, RuntimeError) as e:  # no device for the inputs
+        res["decode_b8_ragged_ms"] = "skipped: %s" % e
     return res
 
 
