@@ -230,6 +230,9 @@ def main() -> int:
                     help="timed calls of the literal three-pass prefill (0 skips it)")
     ap.add_argument("--paged-reps", type=int, default=8,
                     help="timed batches of decode calls on a paged copy of the cache (0 skips)")
+    ap.add_argument("--sweep-reps", type=int, default=2,
+                    help="timed vanilla/bifocal pairs per length of the 8B-like prefill sweep "
+                         "4K .. 128K (0 skips)")
     ap.add_argument("--varlen-reps", type=int, default=3,
                     help="timed packed prefills of 131072 tokens in seven sequences (0 skips)")
     ap.add_argument("--freq-reps", type=int, default=1,
@@ -496,6 +499,32 @@ def main() -> int:
     warm = [timed(lambda: [decode(0) for _ in range(args.decode_batch)]) / args.decode_batch
             for _ in range(max(1, args.decode_reps // 4))]
 
+    # ---- the paper's length sweep (Tab. 7 lengths) on the 8B-like layer: the
+    # G = 1 plateau below the window, then G = 2, 3, 4
+    sweep = []
+    if args.sweep_reps > 0:
+        for Lx in (4096, 8192, 16384, 32768, 65536, 98304, 131072):
+            qx, kx, vx = q[:, :Lx], k[:, :Lx].contiguous(), v[:, :Lx].contiguous()
+            qx = qx.contiguous()
+            ox = torch.empty_like(qx)
+            fb = lambda: api.bifocal_prefill(qx, kx, vx, w_pretrained=wp.w_pretrained,
+                                             w_local=wp.w_local, rope_theta=wp.theta, out=ox,
+                                             stream=stream)
+            fv = lambda: api.rope_attention(qx, kx, vx, rope_theta=wp.theta, out=ox,
+                                            stream=stream)
+            fb()
+            fv()
+            tb, tv = [], []
+            for _ in range(args.sweep_reps):
+                tv.append(timed(fv))
+                tb.append(timed(fb))
+            fl = 4.0 * wp.d * wp.B * wp.Hq * Lx * (Lx + 1) / 2.0
+            sweep.append({"L": Lx, "G": api.group_size(Lx, wp.w_pretrained),
+                          "bifocal_ms": round(med(tb), 3), "vanilla_ms": round(med(tv), 3),
+                          "TFLOPs": round(fl / (med(tb) * 1e-3) / 1e12, 1),
+                          "bifocal_vs_vanilla_throughput": round(med(tv) / med(tb), 4)})
+            del qx, kx, vx, ox
+
     cfg = {}
     if args.config_reps > 0:
         cfg = measure_configs(api, synth, torch, np, stream, args.config_reps, args.decode_batch)
@@ -557,6 +586,8 @@ def main() -> int:
     }
     if cfg:
         line["configs"] = cfg
+    if sweep:
+        line["length_sweep"] = sweep
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(qh, kh, vh, wp, args.cpu_seconds,
                                             (dq, dk, dv, lens, wd))
