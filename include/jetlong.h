@@ -345,10 +345,14 @@ int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_
  * reference (and rescale the running output) when a key tile's largest score
  * in that row exceeds the reference by more than log2_bound (scores in log2
  * units), or lies more than log2_bound below it before anything was
- * accumulated; the default is 64, far from anything ordinary data reaches.  A small bound (e.g. 3) makes the rescale path run on almost every
- * tile of ordinary inputs, which tests use to check it.  Values outside
- * [1, 100] leave the setting unchanged.  Returns the previous value.  Not for
- * use while prefill calls are in flight.
+ * accumulated; the default is 64, far from anything ordinary data reaches.
+ * The fused and vanilla calls first run a pass without that check, which only
+ * notes whether a tile's probability sum exceeded 2^log2_bound or a row's
+ * total fell below 2^-log2_bound; such blocks are then rerun with the check.
+ * A small bound (e.g. 3) sends almost every block through the rerun and the
+ * rescale path, which tests use to check both.  Values outside [1, 100] leave
+ * the setting unchanged.  Returns the previous value.  Not for use while
+ * prefill calls are in flight.
  */
 double jl_debug_prefill_rescale_log2(double log2_bound);
 

@@ -92,6 +92,7 @@ struct PrepArgs {
   // sequence's own group_size(L, w_pre).  nullptr for dense batches.
   const int4* twork;
   int w_pre;
+  int* retry_count;  // zeroed here for the attention kernel that follows
 };
 
 // One workgroup per (tile, b * Hkv + kvh), or per (tile work item, kvh) for a
@@ -99,6 +100,8 @@ struct PrepArgs {
 template <bool BIFOCAL>
 __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t sv[kPfBK * kHeadDim];
+  if (a.retry_count != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
+    *a.retry_count = 0;
   int tile, L;
   size_t seq_row, img;
   FastDiv gdiv = a.gdiv;
@@ -214,6 +217,10 @@ struct PrefillArgs {
   // each sequence takes its own G = group_size(L, w_pre)
   const int4* qwork;
   int w_pre;
+  // blocks whose fast pass needs the reference check (see prefill_kernel):
+  // a counter and the workgroup indices; nullptr where unused
+  int* retry_count;
+  int* retry_list;
 };
 
 // What one launch of the attention kernel computes.
@@ -264,8 +271,16 @@ __device__ inline float sum8(bf16x8 p, float acc) {
 }
 
 
-template <int MODE>
+// SAFE = false (fused and vanilla modes): the fast pass.  It never waits on
+// the softmax reference check; instead it records, without a branch, whether
+// any tile's probability sum exceeded 2^slack, and at the end whether a row's
+// total fell below 2^-slack.  A block with either writes nothing and lists
+// itself; the SAFE launch that follows reruns only the listed blocks with the
+// per-tile check, which moves the reference as needed.  Window modes always
+// run SAFE.
+template <int MODE, bool SAFE>
 __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
+  constexpr bool CHECK_LATE = !SAFE;
   // The visit list has at most two segments: the fused kernel's remote tiles
   // (segment 1), then tiles [kt_l, n_kt) in one view, keeping 0 <= q - k <= w0
   // (segment 2; w0 = INT_MAX makes it the causal set).
@@ -275,6 +290,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   constexpr bool FROM_ZERO = MODE == kModeVanilla || MODE == kModeWinB;  // kt_l = 0
   // LDS: K images in [0, 32K) (two buffers), V^T images in [32K, 64K) (two buffers)
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmemBytes];
+  __shared__ int s_bad;
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -285,7 +301,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // (b, kv head) groups are a multiple of the 8 XCDs, consecutive work items
   // land on one XCD so a group's K/V tiles stay in that XCD's L2.
   const int n_groups = a.B * a.Hkv;
-  const int bid = blockIdx.x;
+  int bid = blockIdx.x;
+  if (SAFE && a.retry_list != nullptr) {  // rerun of the listed blocks only
+    if (bid >= *a.retry_count) return;    // uniform, before any barrier
+    bid = a.retry_list[bid];
+  }
   int kvh, qblk, q_start, q_end, w0;
   size_t row_base, lse_base, img_base;  // rows of q/o, lse entries, tile image elements
   FastDiv gdiv;
@@ -468,6 +488,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // re-bases the tile's scores and the next tile's (computed against the old
   // reference), rescales the running state and redoes the tile's softmax.
   const float p_hi = exp2f(a.slack), p_lo = exp2f(-a.slack);
+  unsigned long long late_bad = 0;
   auto ref_fix = [&](f32x16* sc, f32x16* nx, bf16x8* pb, float& ps) __attribute__((always_inline)) {
     const bool bad = ps > p_hi || (l_run == 0.f && ps < p_lo);
     if (__ballot(bad) == 0) return;
@@ -513,7 +534,10 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     bf16x8 pb[4];
     qk(kbuf(j + 1), nxt);
     float ps = softmax(cur, pb);
-    ref_fix(cur, nxt, pb, ps);
+    if (CHECK_LATE)
+      late_bad |= __ballot(ps > p_hi);
+    else
+      ref_fix(cur, nxt, pb, ps);
     l_run += ps;
     pv(vbuf(j), pb);
   };
@@ -530,6 +554,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const bool q_remote = n_r > 0 || REMOTE2;
   load_q_operand(qrow, hl32, q_remote ? a.rtable : a.table,
                  q_remote && !a.freq_map ? remote_pos(qp, gdiv) : qp, a.q_scale, qop);
+  if (CHECK_LATE && tid == 0) s_bad = 0;  // read after the end-of-block barrier
   issue_k(0);
   issue_v(0);
   if (n_steps > 1) issue_k(1);
@@ -548,6 +573,15 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
 
   // ---- normalise and write
   const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (CHECK_LATE) {
+    late_bad |= __ballot(row_valid && !(l_tot >= p_lo));
+    if (late_bad != 0 && lane == 0) s_bad = 1;
+    __syncthreads();
+    if (s_bad != 0) {
+      if (tid == 0) a.retry_list[atomicAdd(a.retry_count, 1)] = bid;
+      return;
+    }
+  }
   if (row_valid) {
     const float inv = 1.f / l_tot;
     const size_t orow_off = ((row_base + qr) * a.Hq + hd) * kHeadDim;
@@ -613,9 +647,14 @@ __global__ __launch_bounds__(256) void literal_merge_kernel(MergeArgs a) {
 }
 
 // ---------------------------------------------------------------- launchers
+// Tile images, then the retry counter (256 B) and list (one int per
+// workgroup: at most ceil(L / 16) query blocks per (b, kv head), BQ >= 16).
+static size_t retry_bytes(long long nwg) { return 256 + (size_t)nwg * sizeof(int); }
+
 size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L) {
   const size_t tiles = (size_t)(L + kPfBK - 1) / kPfBK;
-  return (size_t)(bifocal ? 3 : 2) * B * Hkv * tiles * kTileBytes;
+  return (size_t)(bifocal ? 3 : 2) * B * Hkv * tiles * kTileBytes +
+         retry_bytes((long long)B * Hkv * ((L + 15) / 16));
 }
 
 // Literal mode workspace: O_A, O_B, O_C (fp32 [B][L][Hq][128] each), then
@@ -639,6 +678,8 @@ static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v
   a.kloc = (const uint16_t*)images;
   a.vt = a.kloc + img;
   a.krem = bifocal ? a.vt + img : nullptr;
+  a.retry_count = (int*)(a.kloc + (bifocal ? 3 : 2) * img);
+  a.retry_list = a.retry_count + 64;
   a.n_tiles = n_tiles;
   a.table = table;
   a.rtable = freq_map ? rtable : table;
@@ -660,6 +701,7 @@ static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v
   p.kv_stride = kv_stride;
   p.n_tiles = n_tiles;
   p.gdiv = a.gdiv;
+  p.retry_count = a.retry_count;
   if ((long long)B * Hkv > 65535) return hipErrorInvalidConfiguration;
   if (bifocal)
     hipLaunchKernelGGL(prep_kernel<true>, dim3(n_tiles, B * Hkv), dim3(256), 0, stream, p);
@@ -684,16 +726,29 @@ static void fill_geometry(PrefillArgs& a, int B, int Hq, int Hkv, int L, int q_s
   a.slack = slack;
 }
 
+// The fused and vanilla modes: the fast pass over the grid, then the checked
+// pass over the blocks it listed (same grid size; the rest exit at once).
+template <int MODE>
+static hipError_t launch_fast_then_checked(const PrefillArgs& a, dim3 grid, hipStream_t stream) {
+  hipLaunchKernelGGL((prefill_kernel<MODE, false>), grid, dim3(kPfThreads), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((prefill_kernel<MODE, true>), grid, dim3(kPfThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
 static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream) {
   const long long nwg = (long long)a.n_qblocks * a.B * a.Hkv;
   if (nwg > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   const dim3 grid((unsigned)nwg), block(kPfThreads);
+  PrefillArgs w = a;
+  w.retry_list = nullptr;  // the window passes check every tile
   switch (mode) {
-    case kModeFused: hipLaunchKernelGGL(prefill_kernel<kModeFused>, grid, block, 0, stream, a); break;
-    case kModeVanilla: hipLaunchKernelGGL(prefill_kernel<kModeVanilla>, grid, block, 0, stream, a); break;
-    case kModeWinA: hipLaunchKernelGGL(prefill_kernel<kModeWinA>, grid, block, 0, stream, a); break;
-    case kModeWinB: hipLaunchKernelGGL(prefill_kernel<kModeWinB>, grid, block, 0, stream, a); break;
-    case kModeWinC: hipLaunchKernelGGL(prefill_kernel<kModeWinC>, grid, block, 0, stream, a); break;
+    case kModeFused: return launch_fast_then_checked<kModeFused>(a, grid, stream);
+    case kModeVanilla: return launch_fast_then_checked<kModeVanilla>(a, grid, stream);
+    case kModeWinA: hipLaunchKernelGGL((prefill_kernel<kModeWinA, true>), grid, block, 0, stream, w); break;
+    case kModeWinB: hipLaunchKernelGGL((prefill_kernel<kModeWinB, true>), grid, block, 0, stream, w); break;
+    case kModeWinC: hipLaunchKernelGGL((prefill_kernel<kModeWinC, true>), grid, block, 0, stream, w); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -868,7 +923,8 @@ static void varlen_sizes(int B, int T, int g, long long* nq, long long* nt) {
 size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hkv) {
   long long nq, nt;
   varlen_sizes(B, T, Hq / Hkv, &nq, &nt);
-  return (size_t)(bifocal ? 3 : 2) * Hkv * nt * kTileBytes + (size_t)(nq + nt) * sizeof(int4);
+  return (size_t)(bifocal ? 3 : 2) * Hkv * nt * kTileBytes + (size_t)(nq + nt) * sizeof(int4) +
+         retry_bytes(nq * Hkv);
 }
 
 // Packed batch: q, o [T][Hq][128], k, v [T][Hkv][128], lse [Hq][T] (optional),
@@ -891,6 +947,8 @@ hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t
   a.krem = bifocal ? a.vt + img : nullptr;
   int4* qwork = (int4*)((uint16_t*)ws + (bifocal ? 3 : 2) * img);
   int4* twork = qwork + nq;
+  a.retry_count = (int*)(twork + nt);
+  a.retry_list = a.retry_count + 64;
   a.n_tiles = (int)nt;
   a.table = table;
   a.rtable = table;
@@ -932,6 +990,7 @@ hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t
   p.n_tiles = (int)nt;
   p.gdiv = a.gdiv;
   p.twork = twork;
+  p.retry_count = a.retry_count;
   p.w_pre = w_pre;
   if (bifocal)
     hipLaunchKernelGGL(prep_kernel<true>, dim3((unsigned)nt, Hkv), dim3(256), 0, stream, p);
@@ -940,12 +999,9 @@ hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
   if (ev0 != nullptr && (e = hipEventRecord(ev0, stream)) != hipSuccess) return e;
-  const dim3 grid((unsigned)(nq * Hkv)), block(kPfThreads);
-  if (bifocal)
-    hipLaunchKernelGGL(prefill_kernel<kModeFused>, grid, block, 0, stream, a);
-  else
-    hipLaunchKernelGGL(prefill_kernel<kModeVanilla>, grid, block, 0, stream, a);
-  e = hipGetLastError();
+  const dim3 grid((unsigned)(nq * Hkv));
+  e = bifocal ? launch_fast_then_checked<kModeFused>(a, grid, stream)
+              : launch_fast_then_checked<kModeVanilla>(a, grid, stream);
   if (e == hipSuccess && ev1 != nullptr) e = hipEventRecord(ev1, stream);
   return e;
 }
