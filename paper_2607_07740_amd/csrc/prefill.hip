@@ -442,10 +442,26 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
   };
 
-  // element masks where tile j is not wholly inside its visit's key set
+  // Element masks where tile j is not wholly inside its visit's key set.  The
+  // fast pass sets each segment's unmasked run [lo, hi] when the segment
+  // starts: segment 1 tiles before m1 hold remote pairs only, segment 2
+  // tiles t with 64 t >= q1 - w0 and 64 t + 63 <= q0 hold band pairs only.
+  // The checked pass tests each tile (fewer live registers).
   auto need_mask = [&](int j) __attribute__((always_inline)) {
     const int k0 = tile_of(j) * kPfBK;
     return j < n_r ? !(q0 - (k0 + kPfBK - 1) > w0) : !(q1 - k0 <= w0 && k0 + kPfBK - 1 <= q0);
+  };
+  auto seg1_bounds = [&](int& lo, int& hi) __attribute__((always_inline)) {
+    const long long x = (long long)q0 - (kPfBK - 1) - w0;  // tile j fully remote: 64 j < x
+    lo = 0;
+    hi = (x > 0 ? (int)((x + kPfBK - 1) / kPfBK) : 0) - 1;
+  };
+  auto seg2_bounds = [&](int& lo, int& hi) __attribute__((always_inline)) {
+    const long long y = (long long)q1 - w0;
+    const int t_lo = y > 0 ? (int)((y + kPfBK - 1) / kPfBK) : 0;
+    const int t_hi = q0 >= kPfBK - 1 ? (q0 - (kPfBK - 1)) / kPfBK : -1;
+    lo = n_r + t_lo - kt_l;
+    hi = n_r + t_hi - kt_l;
   };
   auto mask = [&](int j, f32x16* sc) __attribute__((always_inline)) {
     // keep iff lo <= q - k <= hi: segment 1 keeps q - k > w0, segment 2
@@ -525,8 +541,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // j+1 is issued next to the softmax of tile j, then PV of tile j; K(j+2)
   // and V(j+1) are copied meanwhile.  For the last tile of a segment the
   // QK product reads whatever the next K buffer holds and is discarded.
-  auto visit = [&](int j, f32x16* cur, f32x16* nxt) __attribute__((always_inline)) {
-    if (need_mask(j)) mask(j, cur);
+  auto visit = [&](int j, f32x16* cur, f32x16* nxt, int lo, int hi) __attribute__((always_inline)) {
+    if (SAFE ? need_mask(j) : (j < lo || j > hi)) mask(j, cur);
     wait_vmem();      // this wave's copies of K(j+1), V(j)
     __syncthreads();  // everyone's; QK(j) and PV(j-1) are done everywhere
     if (j + 2 < n_steps) issue_k(j + 2);
@@ -542,12 +558,12 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     pv(vbuf(j), pb);
   };
   // segment [j, jend): the first tile's scores are in sc_a on entry
-  auto segment = [&](int j, int jend) __attribute__((always_inline)) {
+  auto segment = [&](int j, int jend, int lo, int hi) __attribute__((always_inline)) {
     for (; j + 2 <= jend; j += 2) {
-      visit(j, sc_a, sc_b);
-      visit(j + 1, sc_b, sc_a);
+      visit(j, sc_a, sc_b, lo, hi);
+      visit(j + 1, sc_b, sc_a, lo, hi);
     }
-    if (j < jend) visit(j, sc_a, sc_b);
+    if (j < jend) visit(j, sc_a, sc_b, lo, hi);
   };
 
   // ---- prologue: the first view's query operand, K(0), V(0), K(1)
@@ -563,13 +579,19 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   qk(kbuf(0), sc_a);
 
   if (FUSED && n_r > 0) {
-    segment(0, n_r);
+    int lo = 0, hi = 0;
+    if (!SAFE) seg1_bounds(lo, hi);
+    segment(0, n_r, lo, hi);
     // segment 2 in the base view: its first tile's K image (in buffer n_r & 1,
     // not overwritten since) is scored again with the base-rotated operand
     load_q_operand(qrow, hl32, a.table, qp, a.q_scale, qop);
     qk(kbuf(n_r), sc_a);
   }
-  segment(n_r, n_steps);
+  {
+    int lo = 0, hi = 0;
+    if (!SAFE) seg2_bounds(lo, hi);
+    segment(n_r, n_steps, lo, hi);
+  }
 
   // ---- normalise and write
   const float l_tot = l_run + __shfl_xor(l_run, 32);
