@@ -76,9 +76,11 @@ int64_t jl_group_size(int64_t L, int64_t w_pretrained);
  * w_pretrained >= 1, w_local >= 0; keys with q - k <= w_local use the base
  * rotation, older keys the remote one.  When G == 1 the output equals
  * jl_rope_attention bit for bit (the method reduces to the base model).
- * Requires Hq % Hkv == 0, 128 % (Hq / Hkv) == 0 and B * Hkv <= 65535.
+ * Requires Hq % Hkv == 0, 256 % (Hq / Hkv) == 0 and B * Hkv <= 65535.
  * Memory: the call rotates K once per view and transposes V into a
- * library-owned scratch buffer of (3 * B * Hkv * ceil(L / 64) * 16 KB) bytes,
+ * library-owned scratch buffer of 3 * B * Hkv * ceil(L / 64) * 16 KB bytes
+ * of tile images plus 4 * B * Hkv * L + 256 bytes for the list of blocks the
+ * checked pass reruns,
  * one per (device, stream), grown on demand (growing waits for the stream)
  * and freed by jl_release_caches; q, k, v are only read.
  */

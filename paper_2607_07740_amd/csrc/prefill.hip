@@ -28,17 +28,19 @@
 // the base view.  The same kernel also runs Eq. (7) literally: three launches
 // for the windows A, B and C, each over one view, then a merge kernel.
 //
-// Work decomposition: a workgroup is 4 wave64s and owns 128 query rows =
+// Work decomposition: a workgroup is 8 wave64s and owns 256 query rows =
 // (head hl = r / BQ, position q0 + r % BQ) for the g = Hq/Hkv query heads
-// sharing one kv head (GQA packing), BQ = 128 / g.  Two workgroups share a CU
-// (64 KB of LDS each), so every SIMD runs two waves.  A wave owns 32 rows; a
+// sharing one kv head (GQA packing), BQ = 256 / g.  One workgroup fills a CU
+// (64 KB of LDS), so every SIMD runs two waves; each K/V tile copied into LDS
+// serves 256 rows (a 4-wave, 128-row build is 3% slower: twice the tile
+// traffic from L2 and into LDS per flop).  A wave owns 32 rows; a
 // lane owns one query column of S^T = K Q^T (v_mfma_f32_32x32x16_bf16, lanes l
 // and l + 32 split the column's 16 accumulator rows), and O^T += V^T P^T takes
 // P^T straight from the S^T accumulator registers.  K images and V^T images
 // of 64-key tiles are double-buffered separately.  The loop is software
 // pipelined: while the softmax of tile j runs on the VALU, the QK product of
-// tile j+1 is already on the matrix cores, followed by PV of tile j; all four
-// waves copy their quarter of K(j+2) and V(j+1) into LDS meanwhile.  The O^T
+// tile j+1 is already on the matrix cores, followed by PV of tile j; all
+// waves copy their share of K(j+2) and V(j+1) into LDS meanwhile.  The O^T
 // accumulator (4 x 16 fp32 per lane) stays in VGPRs, and each segment's loop
 // is unrolled twice so the two score buffers alternate without copies.
 //
@@ -56,11 +58,17 @@
 
 namespace jl {
 
-constexpr int kPfThreads = 256;  // 4 waves; two workgroups per CU, so two waves per SIMD
-constexpr int kPfRows = 128;     // query rows per workgroup: 32 per wave
-constexpr int kPfBK = 64;        // keys per tile
+#ifndef JL_PF_WAVES
+#define JL_PF_WAVES 8
+#endif
+constexpr int kPfWaves = JL_PF_WAVES;   // waves per workgroup; two waves per SIMD either way
+constexpr int kPfThreads = 64 * kPfWaves;
+constexpr int kPfRows = 32 * kPfWaves;  // query rows per workgroup: 32 per wave
+constexpr int kPfBK = 64;               // keys per tile
 constexpr int kTileBytes = kPfBK * kHeadDim * 2;  // one K image or one V^T image: 16 KB
 constexpr int kSmemBytes = 2 * 2 * kTileBytes;    // double-buffered K + V^T: 64 KB
+constexpr int kPfCopyBytes = kTileBytes / kPfWaves;  // each wave's share of an image copy
+static_assert(kPfWaves == 4 || kPfWaves == 8, "4 or 8 waves per workgroup");
 
 // Tile images (byte layout, also the LDS layout):
 //   K image:   key r (0..63) at r * 256; its 16-byte chunk c (d = 8c .. 8c+7)
@@ -365,29 +373,29 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const int kt_l = FROM_ZERO ? 0 : vr.kt_l;
   const int n_steps = n_r + (n_kt - kt_l);
 
-  // ---- staging: each wave copies its quarter (4 KB) of a K image (k_rem or
-  // k_loc) or a V^T image into buffer j & 1 of that kind
+  // ---- staging: each wave copies its share (16 KB / waves) of a K image
+  // (k_rem or k_loc) or a V^T image into buffer j & 1 of that kind
   const uint32_t smem_base = lds_addr(smem);
   const uint32_t lane_off = 16 * lane;
   auto tile_of = [&](int j) __attribute__((always_inline)) { return j < n_r ? j : kt_l + (j - n_r); };
+  auto copy_share = [&](const unsigned char* g, uint32_t l) __attribute__((always_inline)) {
+    dma16_s<0>(g, lane_off, l);
+    dma16_s<1024>(g, lane_off, l);
+    if constexpr (kPfCopyBytes > 2048) {
+      dma16_s<2048>(g, lane_off, l);
+      dma16_s<3072>(g, lane_off, l);
+    }
+  };
   auto issue_k = [&](int j) __attribute__((always_inline)) {
-    const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * 2048;
+    const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * (kPfCopyBytes / 2);
     const bool use_rem = REMOTE2 || (FUSED && j < n_r);
     const unsigned char* gk = (const unsigned char*)((use_rem ? a.krem : a.kloc) + off);
-    const uint32_t lk = smem_base + (j & 1) * kTileBytes + wave * 4096;
-    dma16_s<0>(gk, lane_off, lk);
-    dma16_s<1024>(gk, lane_off, lk);
-    dma16_s<2048>(gk, lane_off, lk);
-    dma16_s<3072>(gk, lane_off, lk);
+    copy_share(gk, smem_base + (j & 1) * kTileBytes + wave * kPfCopyBytes);
   };
   auto issue_v = [&](int j) __attribute__((always_inline)) {
-    const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * 2048;
+    const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * (kPfCopyBytes / 2);
     const unsigned char* gv = (const unsigned char*)(a.vt + off);
-    const uint32_t lv = smem_base + 2 * kTileBytes + (j & 1) * kTileBytes + wave * 4096;
-    dma16_s<0>(gv, lane_off, lv);
-    dma16_s<1024>(gv, lane_off, lv);
-    dma16_s<2048>(gv, lane_off, lv);
-    dma16_s<3072>(gv, lane_off, lv);
+    copy_share(gv, smem_base + 2 * kTileBytes + (j & 1) * kTileBytes + wave * kPfCopyBytes);
   };
   auto kbuf = [&](int j) __attribute__((always_inline)) { return (const unsigned char*)smem + (j & 1) * kTileBytes; };
   auto vbuf = [&](int j) __attribute__((always_inline)) { return (const unsigned char*)smem + (2 + (j & 1)) * kTileBytes; };
@@ -670,38 +678,44 @@ __global__ __launch_bounds__(256) void literal_merge_kernel(MergeArgs a) {
 
 // ---------------------------------------------------------------- launchers
 // Tile images, then the retry counter (256 B) and list (one int per
-// workgroup: at most ceil(L / 16) query blocks per (b, kv head), BQ >= 16).
+// workgroup: at most L query blocks per (b, kv head), since BQ = rows / g can
+// be as small as 1).
 static size_t retry_bytes(long long nwg) { return 256 + (size_t)nwg * sizeof(int); }
 
-size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L) {
+static size_t image_bytes(bool bifocal, int B, int Hkv, int L) {
   const size_t tiles = (size_t)(L + kPfBK - 1) / kPfBK;
-  return (size_t)(bifocal ? 3 : 2) * B * Hkv * tiles * kTileBytes +
-         retry_bytes((long long)B * Hkv * ((L + 15) / 16));
+  return (size_t)(bifocal ? 3 : 2) * B * Hkv * tiles * kTileBytes;
+}
+
+size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L) {
+  return image_bytes(bifocal, B, Hkv, L) + retry_bytes((long long)B * Hkv * L);
 }
 
 // Literal mode workspace: O_A, O_B, O_C (fp32 [B][L][Hq][128] each), then
 // LSE_A, LSE_B, LSE_C (fp32 [B][Hq][L] each), then the tile images at the next
-// 256-byte boundary.
+// 256-byte boundary (the window passes run checked, with no rerun list).
 static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L) {
   const size_t rows = (size_t)B * L * Hq;
   return 3 * rows * kHeadDim * sizeof(float) + round256(3 * rows * sizeof(float)) +
-         prefill_workspace_bytes(true, B, Hkv, L);
+         image_bytes(true, B, Hkv, L);
 }
 
 // rtable: the remote view's table, nullptr for the aliasing map (then the
-// base table is read at f(p)); with freq_map it is read at p.
+// base table is read at f(p)); with freq_map it is read at p.  With
+// `retry`, the rerun counter and list follow the images (the prep kernel
+// zeroes the counter); without, nothing past the images is touched.
 static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v,
                               const float2* table, const float2* rtable, int freq_map, int B,
-                              int Hkv, int L, int kv_stride, int G, void* images, PrefillArgs& a,
-                              hipStream_t stream) {
+                              int Hkv, int L, int kv_stride, int G, void* images, bool retry,
+                              PrefillArgs& a, hipStream_t stream) {
   const int n_tiles = (L + kPfBK - 1) / kPfBK;
   const size_t img = (size_t)B * Hkv * n_tiles * (kTileBytes / 2);  // bf16 elements per image set
   a.kloc = (const uint16_t*)images;
   a.vt = a.kloc + img;
   a.krem = bifocal ? a.vt + img : nullptr;
-  a.retry_count = (int*)(a.kloc + (bifocal ? 3 : 2) * img);
-  a.retry_list = a.retry_count + 64;
+  a.retry_count = retry ? (int*)(a.kloc + (bifocal ? 3 : 2) * img) : nullptr;
+  a.retry_list = retry ? a.retry_count + 64 : nullptr;
   a.n_tiles = n_tiles;
   a.table = table;
   a.rtable = freq_map ? rtable : table;
@@ -788,7 +802,7 @@ hipError_t launch_prefill_chunk(bool bifocal, const uint16_t* q, const uint16_t*
   PrefillArgs a = {};
   fill_geometry(a, B, Hq, Hkv, L, q_start, Lq, slack);
   hipError_t e = launch_prep(bifocal, k, v, table, rtable, freq_map, B, Hkv, L, kv_stride, G, ws,
-                             a, stream);
+                             true, a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
   a.o = o;
@@ -821,8 +835,8 @@ hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const ui
                  round256(3 * rows * sizeof(float));
   PrefillArgs a = {};
   fill_geometry(a, B, Hq, Hkv, L, 0, L, slack);
-  hipError_t e = launch_prep(true, k, v, table, rtable, freq_map, B, Hkv, L, L, G, images, a,
-                             stream);
+  hipError_t e = launch_prep(true, k, v, table, rtable, freq_map, B, Hkv, L, L, G, images, false,
+                             a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
   const int modes[3] = {kModeWinA, kModeWinB, kModeWinC};

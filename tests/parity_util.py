@@ -37,6 +37,18 @@ def assert_close(got, want, max_abs=MAX_ABS, mean_abs=MEAN_ABS, what=""):
     return mx, mn
 
 
+def prefill_block_q(Hq, Hkv):
+    """Query positions per prefill workgroup, as the library reports it
+    (jl_debug_prefill_tiles fills the geometry even without a buffer)."""
+    import ctypes
+    from paper_2607_07740_amd import api
+    bq, bk, nq, nk = (ctypes.c_int() for _ in range(4))
+    api.lib().jl_debug_prefill_tiles(64, Hq, Hkv, 0, None, 0, ctypes.byref(bq), ctypes.byref(bk),
+                                     ctypes.byref(nq), ctypes.byref(nk), None)
+    assert bq.value > 0
+    return bq.value
+
+
 def sample_positions(L, w0, w_pre, G, block_q, n_random, seed=0):
     """Stratified query positions: window edges, block edges, G-group edges,
     multiples of the pretraining window, the middle and the end, plus seeded

@@ -63,7 +63,7 @@ def _prefill(q=A, k=A, v=A, o=A, lse=None, B=1, Hq=4, Hkv=2, L=64, d=128, theta=
     (dict(k=MIS), api.JL_ERR_INVALID_ARG),
     (dict(o=None), api.JL_ERR_INVALID_ARG),
     (dict(lse=P(0x1001)), api.JL_ERR_INVALID_ARG),
-    (dict(Hq=6, Hkv=2), api.JL_ERR_UNSUPPORTED),  # GQA group 3 does not divide 128
+    (dict(Hq=6, Hkv=2), api.JL_ERR_UNSUPPORTED),  # GQA group 3 does not divide 256
 ])
 def test_prefill_rejects_before_launch(kw, code):
     assert _prefill(**kw) == code
@@ -198,8 +198,8 @@ def test_debug_entry_points_reject_bad_arguments():
     rc = L.jl_debug_prefill_tiles(2048, 2, 1, 128, None, 0, ctypes.byref(bq), ctypes.byref(bk),
                                   ctypes.byref(nq), ctypes.byref(nk), None)
     assert rc == api.JL_ERR_INVALID_ARG  # no buffer, but the geometry is reported
-    assert (bq.value, bk.value) == (64, 64)  # 128 rows = 64 positions x 2 heads
-    assert (nq.value, nk.value) == (32, 32)
+    assert (bq.value, bk.value) == (128, 64)  # 256 rows = 128 positions x 2 heads
+    assert (nq.value, nk.value) == (16, 32)
 
 
 def _literal(ws=A, ws_bytes=None, B=1, Hq=4, Hkv=2, L=64, w=16, w0=4, o=A):

@@ -5,7 +5,8 @@ import pytest
 
 from oracle import oracle as O
 from paper_2607_07740_amd import api, synth
-from parity_util import assert_close, rows_for, sample_positions, say, to_dev, to_f64
+from parity_util import (assert_close, prefill_block_q, rows_for, sample_positions, say, to_dev,
+                         to_f64)
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -78,7 +79,7 @@ def test_freq_map_1p7b_128k_sampled_rows():
     G = api.group_size(w.L, w.w_pretrained)
     say("freq-map prefill %s" % w.name)
     out = _run(q, k, v, w.w_pretrained, w.w_local, "freq")
-    pos = sample_positions(w.L, w.w_local, w.w_pretrained, G, 128 // (w.Hq // w.Hkv), 16)
+    pos = sample_positions(w.L, w.w_local, w.w_pretrained, G, prefill_block_q(w.Hq, w.Hkv), 16)
     rows = rows_for(w.B, w.Hq, pos)
     say("oracle rows", len(rows))
     want, _ = O.prefill_rows(q, k, v, rows, theta=w.theta, w_pretrained=w.w_pretrained,

@@ -4,7 +4,8 @@ import pytest
 
 from oracle import oracle as O
 from paper_2607_07740_amd import api, synth
-from parity_util import assert_close, rows_for, sample_positions, say, to_dev, to_f64
+from parity_util import (assert_close, prefill_block_q, rows_for, sample_positions, say, to_dev,
+                         to_f64)
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -87,6 +88,25 @@ def test_rescale_path_on_every_tile(bifocal, L, g, w_pre, w0):
     assert_close(lse.cpu().numpy(), want_lse, max_abs=5e-2, mean_abs=5e-3, what="rescale lse")
 
 
+@pytest.mark.parametrize("g", [64, 128])
+def test_rescale_rerun_list_holds_every_block(g):
+    """Wide GQA groups give query blocks of 2 or 1 positions, so a 300-token
+    call has up to 300 blocks per kv head.  With the bound lowered to 2^3
+    nearly every block is flagged and listed for the checked rerun; the list
+    must hold them all and the result must still match the oracle."""
+    B, Hkv, L, w_pre, w0 = 1, 2, 300, 70, 20
+    q, k, v = synth.prefill_inputs(B, g * Hkv, Hkv, L, 128, seed=g, outlier_channels=8)
+    old = api.debug_prefill_rescale_log2(3.0)
+    try:
+        say("rescale rerun list, wide group g=%d L=%d" % (g, L))
+        out, lse = _run(True, q, k, v, w_pre, w0, want_lse=True)
+    finally:
+        api.debug_prefill_rescale_log2(old)
+    want, want_lse = O.prefill(q, k, v, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    assert_close(to_f64(out), want, what="wide group g=%d" % g)
+    assert_close(lse.cpu().numpy(), want_lse, max_abs=5e-2, mean_abs=5e-3, what="wide lse")
+
+
 def test_all_scores_far_below_zero():
     """Every score of a row is about -300 nats: exp2 against the initial
     reference underflows, so the reference must move down to the row maximum
@@ -123,7 +143,7 @@ def _sampled_parity(name, n_random):
     G = api.group_size(w.L, w.w_pretrained)
     say("%s bifocal prefill B=%d Hq=%d Hkv=%d L=%d G=%d" % (name, w.B, w.Hq, w.Hkv, w.L, G))
     out = _run(True, q, k, v, w.w_pretrained, w.w_local)
-    block_q = 128 // (w.Hq // w.Hkv)
+    block_q = prefill_block_q(w.Hq, w.Hkv)
     pos = sample_positions(w.L, w.w_local, w.w_pretrained, G, block_q, n_random)
     rows = rows_for(w.B, w.Hq, pos)
     say("oracle rows", len(rows))
