@@ -386,16 +386,17 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       dma16_s<3072>(g, lane_off, l);
     }
   };
-  auto issue_k = [&](int j) __attribute__((always_inline)) {
+  // copy list entry j into buffer jb & 1 (jb = j except for the clamped copies)
+  auto issue_k = [&](int j, int jb) __attribute__((always_inline)) {
     const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * (kPfCopyBytes / 2);
     const bool use_rem = REMOTE2 || (FUSED && j < n_r);
     const unsigned char* gk = (const unsigned char*)((use_rem ? a.krem : a.kloc) + off);
-    copy_share(gk, smem_base + (j & 1) * kTileBytes + wave * kPfCopyBytes);
+    copy_share(gk, smem_base + (jb & 1) * kTileBytes + wave * kPfCopyBytes);
   };
-  auto issue_v = [&](int j) __attribute__((always_inline)) {
+  auto issue_v = [&](int j, int jb) __attribute__((always_inline)) {
     const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * (kPfCopyBytes / 2);
     const unsigned char* gv = (const unsigned char*)(a.vt + off);
-    copy_share(gv, smem_base + 2 * kTileBytes + (j & 1) * kTileBytes + wave * kPfCopyBytes);
+    copy_share(gv, smem_base + 2 * kTileBytes + (jb & 1) * kTileBytes + wave * kPfCopyBytes);
   };
   auto kbuf = [&](int j) __attribute__((always_inline)) { return (const unsigned char*)smem + (j & 1) * kTileBytes; };
   auto vbuf = [&](int j) __attribute__((always_inline)) { return (const unsigned char*)smem + (2 + (j & 1)) * kTileBytes; };
@@ -553,10 +554,14 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     if (SAFE ? need_mask(j) : (j < lo || j > hi)) mask(j, cur);
     wait_vmem();      // this wave's copies of K(j+1), V(j)
     __syncthreads();  // everyone's; QK(j) and PV(j-1) are done everywhere
-    if (j + 2 < n_steps) issue_k(j + 2);
-    if (j + 1 < n_steps) issue_v(j + 1);
     bf16x8 pb[4];
     qk(kbuf(j + 1), nxt);
+    // K(j+2) and V(j+1) go into the buffers QK(j) and PV(j-1) released.
+    // Issued after the QK product, so its operand reads start right after
+    // the barrier; past the list's end the last entry is copied again (into
+    // the free buffer), so no branch splits the loop body.
+    issue_k(min(j + 2, n_steps - 1), j + 2);
+    issue_v(min(j + 1, n_steps - 1), j + 1);
     float ps = softmax(cur, pb);
     if (CHECK_LATE)
       late_bad |= __ballot(ps > p_hi);
@@ -579,9 +584,9 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   load_q_operand(qrow, hl32, q_remote ? a.rtable : a.table,
                  q_remote && !a.freq_map ? remote_pos(qp, gdiv) : qp, a.q_scale, qop);
   if (CHECK_LATE && tid == 0) s_bad = 0;  // read after the end-of-block barrier
-  issue_k(0);
-  issue_v(0);
-  if (n_steps > 1) issue_k(1);
+  issue_k(0, 0);
+  issue_v(0, 0);
+  if (n_steps > 1) issue_k(1, 1);
   wait_vmem();
   __syncthreads();
   qk(kbuf(0), sc_a);
@@ -600,6 +605,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     if (!SAFE) seg2_bounds(lo, hi);
     segment(n_r, n_steps, lo, hi);
   }
+  wait_vmem();  // the copies past the list's end
 
   // ---- normalise and write
   const float l_tot = l_run + __shfl_xor(l_run, 32);
