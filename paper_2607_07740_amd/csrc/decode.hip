@@ -593,22 +593,28 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
   const int quarter = blockIdx.y;
   const int b = bh / a.Hq;
   const int tid = threadIdx.x;
-  const int ns = split_count(a, b);  // splits with keys
   const float* base = a.ws + (size_t)bh * a.n_split * kStateFloats;
   const int c = tid & 7;
   const int grp = tid >> 3;
 
+  // every slot is read without waiting for the split count (which needs
+  // kv_lens); the slots past it hold stale states and are dropped below
   float m[kRedPerGroup], l[kRedPerGroup];
   f32x4 ov[kRedPerGroup];
 #pragma unroll
   for (int i = 0; i < kRedPerGroup; ++i) {
-    const int s = grp + kRedGroups * i;
-    if (s < ns) {
-      const float* stt = base + (size_t)s * kStateFloats;
-      m[i] = stt[0];
-      l[i] = stt[1];
-      ov[i] = *(const f32x4*)(stt + 4 + 32 * quarter + 4 * c);
-    } else {
+    // no branch: all loads are issued together (slots past n_split read the
+    // last slot again and are dropped with the rest)
+    const float* stt = base + (size_t)min(grp + kRedGroups * i, a.n_split - 1) * kStateFloats;
+    const float2 ml = *(const float2*)stt;
+    m[i] = ml.x;
+    l[i] = ml.y;
+    ov[i] = *(const f32x4*)(stt + 4 + 32 * quarter + 4 * c);
+  }
+  const int ns = split_count(a, b);  // splits with keys
+#pragma unroll
+  for (int i = 0; i < kRedPerGroup; ++i) {
+    if (grp + kRedGroups * i >= ns) {
       m[i] = -INFINITY;
       l[i] = 0.f;
       ov[i] = f32x4{};
