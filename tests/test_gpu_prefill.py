@@ -88,13 +88,14 @@ def test_rescale_path_on_every_tile(bifocal, L, g, w_pre, w0):
     assert_close(lse.cpu().numpy(), want_lse, max_abs=5e-2, mean_abs=5e-3, what="rescale lse")
 
 
-@pytest.mark.parametrize("g", [64, 128])
-def test_rescale_rerun_list_holds_every_block(g):
-    """Wide GQA groups give query blocks of 2 or 1 positions, so a 300-token
-    call has up to 300 blocks per kv head.  With the bound lowered to 2^3
-    nearly every block is flagged and listed for the checked rerun; the list
-    must hold them all and the result must still match the oracle."""
-    B, Hkv, L, w_pre, w0 = 1, 2, 300, 70, 20
+@pytest.mark.parametrize("g,Hkv", [(64, 2), (128, 2), (256, 1)])
+def test_rescale_rerun_list_holds_every_block(g, Hkv):
+    """Wide GQA groups give query blocks of a few positions (one at g = 256),
+    so a 300-token call has up to 300 blocks per kv head.  With the bound
+    lowered to 2^3 nearly every block is flagged and listed for the checked
+    rerun; the list must hold them all and the result must still match the
+    oracle."""
+    B, L, w_pre, w0 = 1, 300, 70, 20
     q, k, v = synth.prefill_inputs(B, g * Hkv, Hkv, L, 128, seed=g, outlier_channels=8)
     old = api.debug_prefill_rescale_log2(3.0)
     try:
