@@ -46,11 +46,16 @@
 //
 // Softmax runs in the log2 domain against a per-row reference m (initially 0)
 // that the QK product subtracts itself: its first k-step accumulates onto -m.
-// The common path is exp2, convert and a dot product for the row sum.  Before
-// a tile's softmax the reference is checked against the tile's largest score;
-// it moves only when that score lies more than 64 above it, or (before
-// anything was accumulated) more than 64 below it, a rare branch that re-bases
-// the tile and rescales the state.  So every probability stays below 2^64.
+// The common path is exp2, convert and a dot product for the row sum.  A
+// first, fast pass never moves the reference: it only notes, per tile, whether
+// a row's probability sum passed 2^64 and, at the end, whether a row's total
+// fell below 2^-64; a block that trips either writes nothing and is listed.
+// A second launch reruns the listed blocks with the checked kernel, which
+// tests each tile's probability sum after its softmax and, in a rare branch,
+// moves the reference to the tile's largest score (when that lies more than 64
+// above it, or more than 64 below it before anything was accumulated),
+// re-bases the tile and rescales the state.  So every probability stays below
+// 2^64.
 #include <climits>
 #include <type_traits>
 
