@@ -560,6 +560,9 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     wait_vmem();      // this wave's copies of K(j+1), V(j)
     __syncthreads();  // everyone's; QK(j) and PV(j-1) are done everywhere
     bf16x8 pb[4];
+    // ask the scheduler to interleave the LDS operand reads with the MFMAs
+    // (0.8% faster fused, vanilla unchanged, measured on one box)
+    __builtin_amdgcn_iglp_opt(0);
     qk(kbuf(j + 1), nxt);
     // K(j+2) and V(j+1) go into the buffers QK(j) and PV(j-1) released.
     // Issued after the QK product, so its operand reads start right after
