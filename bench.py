@@ -121,6 +121,7 @@ def cpu_baseline(q, k, v, w, target_s: float, dec=None):
         O.decode(dq, dk, dv, lens, theta=wd.theta, w_pretrained=wd.w_pretrained,
                  w_local=wd.w_local)
         res["decode_ms"] = round((time.perf_counter() - t0) * 1e3, 1)
+        res["decode_kv_lens"] = [int(x) for x in lens]
     # the B = 8 ragged decode: inputs drawn on the device and copied to the host
     try:
         import torch
@@ -137,6 +138,20 @@ def cpu_baseline(q, k, v, w, target_s: float, dec=None):
     except (ImportError, RuntimeError) as e:  # no device for the inputs
         res["decode_b8_ragged_ms"] = "skipped: %s" % e
     return res
+
+
+def config_block(wp, wd, dlens, G):
+    """The bench line's `config`: the timed prefill and decode workloads, with
+    the decode batch's own kv lengths."""
+    return {
+        "workload": "%s + %s" % (wp.name, wd.name),
+        "prefill": {"B": wp.B, "Hq": wp.Hq, "Hkv": wp.Hkv, "L": wp.L, "head_dim": wp.d,
+                    "w_pretrained": wp.w_pretrained, "w_local": wp.w_local,
+                    "rope_theta": wp.theta, "G": int(G)},
+        "decode": {"B": wd.B, "Hq": wd.Hq, "Hkv": wd.Hkv, "kv_lens": [int(x) for x in dlens],
+                   "head_dim": wd.d, "w_pretrained": wd.w_pretrained,
+                   "w_local": wd.w_local, "rope_theta": wd.theta},
+    }
 
 
 EXTRA_PREFILL = ["qwen3_8b_prefill_64k", "qwen3_1p7b_prefill_128k", "qwen3_1p7b_within_32k"]
@@ -277,13 +292,13 @@ def main() -> int:
     qh, kh, vh = synth.make_inputs(wp)
     q, k, v = _dev(qh, torch, np), _dev(kh, torch, np), _dev(vh, torch, np)
     out = torch.empty_like(q)
-    dq, dk, dv, lens = synth.make_inputs(wd)
+    dq, dk, dv, dlens = synth.make_inputs(wd)
     dqd = _dev(dq, torch, np)
     caches = [(_dev(dk, torch, np), _dev(dv, torch, np))]
     # a second cache with the same contents, alternated so consecutive decode
     # calls cannot be served from the 256 MB Infinity Cache
     caches.append((caches[0][0].clone(), caches[0][1].clone()))
-    lens_d = torch.from_numpy(lens).cuda()
+    lens_d = torch.from_numpy(dlens).cuda()
     dout = torch.empty_like(dqd)
     ws = torch.empty(api.decode_workspace_bytes(wd.B, wd.Hq, wd.Hkv, wd.L), dtype=torch.uint8,
                      device="cuda")
@@ -348,7 +363,7 @@ def main() -> int:
     flops = 4.0 * wp.d * wp.B * wp.Hq * wp.L * (wp.L + 1) / 2.0
     tflops = flops / (pre_avg * 1e-3) / 1e12
     attn_tflops = flops / (attn_avg * 1e-3) / 1e12
-    kv_bytes = 2.0 * float(np.sum(lens)) * wd.Hkv * wd.d * 2.0
+    kv_bytes = 2.0 * float(np.sum(dlens)) * wd.Hkv * wd.d * 2.0
     io_bytes = 2.0 * wd.B * wd.Hq * wd.d * 2.0
     dec_gbps = (kv_bytes + io_bytes) / (dec_avg * 1e-3) / 1e9
 
@@ -479,13 +494,13 @@ def main() -> int:
     # seven sequences of 64K .. 1K in one call, against one call per sequence
     vl = {}
     if args.varlen_reps > 0:
-        lens = [65536, 32768, 16384, 8192, 4096, 3072, 1024]
-        cu = torch.tensor([0] + list(np.cumsum(lens)), dtype=torch.int32, device="cuda")
+        vlens = [65536, 32768, 16384, 8192, 4096, 3072, 1024]
+        cu = torch.tensor([0] + list(np.cumsum(vlens)), dtype=torch.int32, device="cuda")
         qv, kv_, vv = q[0], k[0], v[0]  # [T, H, 128] views of the resident inputs
         ov = out[0]
 
         def varlen():
-            api.prefill_varlen(qv, kv_, vv, cu, max_seqlen=max(lens), w_pretrained=wp.w_pretrained,
+            api.prefill_varlen(qv, kv_, vv, cu, max_seqlen=max(vlens), w_pretrained=wp.w_pretrained,
                                w_local=wp.w_local, rope_theta=wp.theta, out=ov, stream=stream)
         parts = []
         for a, b in zip(cu[:-1].tolist(), cu[1:].tolist()):
@@ -501,8 +516,8 @@ def main() -> int:
         for _ in range(args.varlen_reps):
             tv_.append(timed(varlen))
             ts_.append(timed(separate))
-        vfl = sum(4.0 * wp.d * wp.Hq * n * (n + 1) / 2.0 for n in lens)
-        vl = {"varlen_prefill": {"lens": lens, "ms": round(med(tv_), 3),
+        vfl = sum(4.0 * wp.d * wp.Hq * n * (n + 1) / 2.0 for n in vlens)
+        vl = {"varlen_prefill": {"lens": vlens, "ms": round(med(tv_), 3),
                                  "TFLOPs": round(vfl / (med(tv_) * 1e-3) / 1e12, 1),
                                  "mfma_frac": round(vfl / (med(tv_) * 1e-3) / 1e12 /
                                                     PEAK_BF16_TFLOPS, 4),
@@ -558,16 +573,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {
-            "workload": "%s + %s" % (wp.name, wd.name),
-            "prefill": {"B": wp.B, "Hq": wp.Hq, "Hkv": wp.Hkv, "L": wp.L, "head_dim": wp.d,
-                        "w_pretrained": wp.w_pretrained, "w_local": wp.w_local,
-                        "rope_theta": wp.theta,
-                        "G": api.group_size(wp.L, wp.w_pretrained)},
-            "decode": {"B": wd.B, "Hq": wd.Hq, "Hkv": wd.Hkv, "kv_lens": [int(x) for x in lens],
-                       "head_dim": wd.d, "w_pretrained": wd.w_pretrained,
-                       "w_local": wd.w_local, "rope_theta": wd.theta},
-        },
+        "config": config_block(wp, wd, dlens, api.group_size(wp.L, wp.w_pretrained)),
         "prefill_ms": round(pre_avg, 3),
         "prefill_mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
         "decode_us": round(dec_med * 1e3, 2),
@@ -606,7 +612,7 @@ def main() -> int:
         line["length_sweep"] = sweep
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(qh, kh, vh, wp, args.cpu_seconds,
-                                            (dq, dk, dv, lens, wd))
+                                            (dq, dk, dv, dlens, wd))
     print(json.dumps(line), flush=True)
     return 0
 
