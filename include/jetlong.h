@@ -77,10 +77,12 @@ int64_t jl_group_size(int64_t L, int64_t w_pretrained);
  * rotation, older keys the remote one.  When G == 1 the output equals
  * jl_rope_attention bit for bit (the method reduces to the base model).
  * Requires Hq % Hkv == 0, 256 % (Hq / Hkv) == 0 and B * Hkv <= 65535.
- * Memory: the call rotates K once per view and transposes V into a
- * library-owned scratch buffer of 3 * B * Hkv * ceil(L / 64) * 16 KB bytes
- * of tile images plus 4 * B * Hkv * L + 256 bytes for the list of blocks the
- * checked pass reruns,
+ * K is read raw: each staged 64-key tile is rotated in registers to the view
+ * of its visit (R(k) x_k on the band, R(f(k)) x_k beyond it, Sec. 3.2) and
+ * kept only in on-chip memory; no rotated key is written anywhere.
+ * Memory: V is transposed into a library-owned scratch buffer of
+ * B * Hkv * ceil(L / 64) * 16 KB bytes of tile images plus
+ * 4 * B * Hkv * L + 256 bytes for the list of blocks the checked pass reruns,
  * one per (device, stream), grown on demand (growing waits for the stream)
  * and freed by jl_release_caches; q, k, v are only read.
  */
@@ -129,10 +131,10 @@ int jl_bifocal_prefill_map(const void* q, const void* k, const void* v, void* o,
  * The call's sequence length is L = q_start + n_queries: G = max(1,
  * ceil(L / w_pretrained)) for every query of the chunk, as in a prefill of
  * length L, so the output equals rows q_start .. L - 1 of
- * jl_bifocal_prefill over the first L cache rows.  The caches are only read.
- * Each call rotates keys [0, L) once per view into the library scratch (as
- * jl_bifocal_prefill does for its L), so a chunk costs O(L) extra work on top
- * of its attention.  Requires 0 <= q_start, n_queries >= 1,
+ * jl_bifocal_prefill over the first L cache rows.  The caches are only read:
+ * keys are rotated on chip per visit, as in jl_bifocal_prefill, and values
+ * [0, L) are transposed into the library scratch, so a chunk costs O(L)
+ * extra work on top of its attention.  Requires 0 <= q_start, n_queries >= 1,
  * q_start + n_queries <= max_len; other requirements and errors as in
  * jl_bifocal_prefill.
  */
@@ -164,8 +166,8 @@ int jl_rope_attention_chunk(const void* q, const void* k_cache, const void* v_ca
  * clamped into [0, total_tokens] (a decreasing step gives an empty sequence)
  * and a sequence whose work would not fit the lists sized for well-formed
  * input is skipped; output rows of skipped, cut or uncovered positions are
- * left as they were.  Scratch (the library's, per stream): (3 * Hkv *
- * (ceil(T / 64) + B)) tile images of 16 KB plus two small work lists.  Other
+ * left as they were.  Scratch (the library's, per stream): (Hkv *
+ * (ceil(T / 64) + B)) V^T tile images of 16 KB plus two small work lists.  Other
  * requirements and errors as in jl_bifocal_prefill; only the Eq. (3) map.
  */
 int jl_bifocal_prefill_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
@@ -173,8 +175,7 @@ int jl_bifocal_prefill_varlen(const void* q, const void* k, const void* v, void*
                               int Hq, int Hkv, int head_dim, double rope_theta, int w_pretrained,
                               int w_local, void* stream);
 
-/* The vanilla counterpart of jl_bifocal_prefill_varlen (base rotation only;
- * two images per tile). */
+/* The vanilla counterpart of jl_bifocal_prefill_varlen (base rotation only). */
 int jl_rope_attention_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
                              const int32_t* cu_seqlens, int B, int total_tokens, int max_seqlen,
                              int Hq, int Hkv, int head_dim, double rope_theta, void* stream);
@@ -182,8 +183,7 @@ int jl_rope_attention_varlen(const void* q, const void* k, const void* v, void* 
 /*
  * Vanilla causal RoPE attention with the same tiling and RoPE of raw Q/K at
  * base positions: the base model of Sec. 3 and the denominator of the
- * overhead measurements.  Arguments and scratch as in jl_bifocal_prefill
- * (two images per tile instead of three).
+ * overhead measurements.  Arguments and scratch as in jl_bifocal_prefill.
  */
 int jl_rope_attention(const void* q, const void* k, const void* v, void* o, float* lse, int B,
                       int Hq, int Hkv, int L, int head_dim, double rope_theta, void* stream);
@@ -191,8 +191,8 @@ int jl_rope_attention(const void* q, const void* k, const void* v, void* o, floa
 /*
  * Bytes of device workspace jl_bifocal_prefill_literal needs for this shape:
  * 3 * B * L * Hq * head_dim * 4 (the window outputs) + the window LSEs
- * (3 * B * Hq * L * 4, rounded up to 256) + 3 * B * Hkv * ceil(L / 64) * 16 KB
- * (rotated key and transposed value tiles).  Returns 0 for invalid arguments.
+ * (3 * B * Hq * L * 4, rounded up to 256) + B * Hkv * ceil(L / 64) * 16 KB
+ * (transposed value tiles).  Returns 0 for invalid arguments.
  */
 size_t jl_prefill_literal_workspace_bytes(int B, int Hq, int Hkv, int L, int head_dim);
 
@@ -363,7 +363,7 @@ double jl_debug_prefill_rescale_log2(double log2_bound);
  * jl_bifocal_prefill / jl_rope_attention call records the HIP event `start`
  * on its stream right before its attention kernel and `stop` right after it,
  * so hipEventElapsedTime(start, stop) is that kernel's duration alone (the
- * key-rotation kernel in front of it stays outside).  which = 1: the same
+ * value-transpose kernel in front of it stays outside).  which = 1: the same
  * around the split kernel of every decode call (the reduce stays outside).
  * start, stop: hipEvent_t created and owned by the caller; NULL, NULL clears
  * the hook.  JL_ERR_INVALID_ARG for another `which` or when only one event is

@@ -7,10 +7,23 @@ struct Omega {
   double w[kHalf];  // omega_i = theta^(-2i/d), computed on the host in fp64
 };
 
+// Round an fp64 value to bf16 with one correct round-to-nearest-even step:
+// rounding to fp32 toward zero and setting the last bit when inexact (round
+// to odd) keeps enough information for the second rounding to be exact.
+__device__ inline uint32_t bf16_bits_rne(double x) {
+  const float t = __double2float_rz(x);
+  uint32_t b = __float_as_uint(t) | ((double)t != x ? 1u : 0u);
+  return (b + 0x7fffu + ((b >> 16) & 1u)) >> 16;
+}
+
 // table[p][i] = (cos(p * omega_i), sin(p * omega_i)): the angle and its
 // trigonometric functions are evaluated in fp64 and rounded once to fp32
 // (positions reach ~1.3e5, where an fp32 angle would be off by ~1e-2 rad).
-__global__ void build_table_kernel(float2* table, int n_pos, Omega om) {
+// table16 (optional) holds the same pairs rounded once from fp64 to bf16,
+// packed (cos in the low half, sin in the high half) into one 32-bit word:
+// the operand of the prefill's key rotation, whose products are exact in
+// fp32 and whose result is rounded to bf16 anyway.
+__global__ void build_table_kernel(float2* table, uint32_t* table16, int n_pos, Omega om) {
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long long)n_pos * kHalf) return;
   const int p = (int)(idx >> 6);
@@ -18,14 +31,17 @@ __global__ void build_table_kernel(float2* table, int n_pos, Omega om) {
   double s, c;
   sincos((double)p * om.w[i], &s, &c);
   table[idx] = make_float2((float)c, (float)s);
+  if (table16 != nullptr) table16[idx] = bf16_bits_rne(c) | (bf16_bits_rne(s) << 16);
 }
 
-hipError_t launch_build_table(float2* table, int n_pos, const double* omega, hipStream_t stream) {
+hipError_t launch_build_table(float2* table, uint32_t* table16, int n_pos, const double* omega,
+                              hipStream_t stream) {
   Omega om;
   for (int i = 0; i < kHalf; ++i) om.w[i] = omega[i];
   const long long n = (long long)n_pos * kHalf;
   const unsigned blocks = (unsigned)((n + 255) / 256);
-  hipLaunchKernelGGL(build_table_kernel, dim3(blocks), dim3(256), 0, stream, table, n_pos, om);
+  hipLaunchKernelGGL(build_table_kernel, dim3(blocks), dim3(256), 0, stream, table, table16, n_pos,
+                     om);
   return hipGetLastError();
 }
 

@@ -19,25 +19,25 @@
 namespace jl {
 // kernels (prefill.hip, decode.hip, aux.hip)
 size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L);
-hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                          uint16_t* o, float* lse, const float2* table, const float2* rtable,
-                          int freq_map, int B, int Hq, int Hkv, int L, int G, int w0, float slack,
-                          void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
 hipError_t launch_prefill_chunk(bool bifocal, const uint16_t* q, const uint16_t* k,
                                 const uint16_t* v, uint16_t* o, float* lse, const float2* table,
-                                const float2* rtable, int freq_map, int B, int Hq, int Hkv, int L,
-                                int q_start, int Lq, int kv_stride, int G, int w0, float slack,
-                                void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1);
+                                const float2* rtable, const uint32_t* table16,
+                                const uint32_t* rtable16, int freq_map, int B, int Hq, int Hkv,
+                                int L, int q_start, int Lq, int kv_stride, int G, int w0,
+                                float slack, void* ws, hipStream_t stream, hipEvent_t ev0,
+                                hipEvent_t ev1);
 size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hkv);
 hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t* k,
                                  const uint16_t* v, uint16_t* o, float* lse, const float2* table,
-                                 const int32_t* cu, int B, int T, int max_len, int Hq, int Hkv,
+                                 const uint32_t* table16, const int32_t* cu, int B, int T,
+                                 int max_len, int Hq, int Hkv,
                                  int w_pre, int w0, float slack, void* ws, hipStream_t stream,
                                  hipEvent_t ev0, hipEvent_t ev1);
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L);
 hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                   uint16_t* o, float* lse, const float2* table,
-                                  const float2* rtable, int freq_map, int B, int Hq, int Hkv,
+                                  const float2* rtable, const uint32_t* table16,
+                                  const uint32_t* rtable16, int freq_map, int B, int Hq, int Hkv,
                                   int L, int G, int w0, float slack, void* ws,
                                   hipStream_t stream);
 int prefill_rows_per_block();
@@ -51,7 +51,8 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
                          hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1,
                          const int32_t* block_table, int max_pages, int n_pages, int page_shift,
                          const double* freq_og);
-hipError_t launch_build_table(float2* table, int n_pos, const double* omega, hipStream_t stream);
+hipError_t launch_build_table(float2* table, uint32_t* table16, int n_pos, const double* omega,
+                              hipStream_t stream);
 hipError_t launch_debug_schedule(const int32_t* lengths, int nl, const int32_t* positions, int np,
                                  int w, int32_t* gout, int32_t* fout, int32_t* dout,
                                  hipStream_t stream);
@@ -101,6 +102,9 @@ bool aligned16(const void* p) { return p != nullptr && (reinterpret_cast<uintptr
 bool aligned4(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 3) == 0; }
 
 // ------------------------------------------------------------ table cache
+// A table of cap positions is one allocation: cap x 64 fp32 (cos, sin) pairs
+// (512 B per position), then the same pairs in fp16, one 32-bit word each
+// (256 B per position).
 struct TableEntry {
   int device;
   double theta;
@@ -109,10 +113,23 @@ struct TableEntry {
 };
 std::mutex g_mu;
 std::vector<TableEntry> g_tables;
-std::vector<std::pair<int, float2*>> g_retired;  // superseded tables, freed by jl_release_caches
+std::vector<std::pair<int, float2*>> g_retired;  // superseded base tables, freed by jl_release_caches
 
-// Returns a device table covering positions [0, n_pos) for the current device.
-int get_table(double theta, int n_pos, hipStream_t stream, const float2** out) {
+size_t table_bytes(long long cap) { return (size_t)cap * 64 * (sizeof(float2) + sizeof(uint32_t)); }
+const uint32_t* table16_of(const float2* p, long long cap) {
+  return reinterpret_cast<const uint32_t*>(p + (size_t)cap * 64);
+}
+
+struct Tables {
+  const float2* f32;
+  const uint32_t* f16;
+};
+
+// Returns device tables covering positions [0, n_pos) for the current device.
+// A larger request doubles the capacity (waiting for the stream once); the
+// superseded table is kept until jl_release_caches (calls in flight on other
+// streams may still read it), so the retired total stays below the live one.
+int get_table(double theta, int n_pos, hipStream_t stream, Tables* out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -121,7 +138,7 @@ int get_table(double theta, int n_pos, hipStream_t stream, const float2** out) {
   for (auto& t : g_tables)
     if (t.device == dev && t.theta == theta) found = &t;
   if (found && found->cap >= n_pos) {
-    *out = found->ptr;
+    *out = Tables{found->ptr, table16_of(found->ptr, found->cap)};
     return JL_OK;
   }
   long long cap = 4096;
@@ -129,11 +146,11 @@ int get_table(double theta, int n_pos, hipStream_t stream, const float2** out) {
   if (found && cap < 2LL * found->cap) cap = 2LL * found->cap;
   if (cap > (1LL << 30) / 64) cap = n_pos;  // keep the element count in range
   float2* p = nullptr;
-  e = hipMalloc(&p, (size_t)cap * 64 * sizeof(float2));
+  e = hipMalloc(&p, table_bytes(cap));
   if (e != hipSuccess) return hip_fail(e, "hipMalloc(rope table)");
   double omega[64];
   for (int i = 0; i < 64; ++i) omega[i] = std::pow(theta, -2.0 * i / (double)kHeadDim);
-  e = jl::launch_build_table(p, (int)cap, omega, stream);
+  e = jl::launch_build_table(p, const_cast<uint32_t*>(table16_of(p, cap)), (int)cap, omega, stream);
   if (e == hipSuccess) e = hipStreamSynchronize(stream);  // usable from any stream afterwards
   if (e != hipSuccess) {
     (void)hipFree(p);
@@ -146,7 +163,7 @@ int get_table(double theta, int n_pos, hipStream_t stream, const float2** out) {
   } else {
     g_tables.push_back(TableEntry{dev, theta, (int)cap, p});
   }
-  *out = p;
+  *out = Tables{p, table16_of(p, cap)};
   return JL_OK;
 }
 
@@ -178,17 +195,22 @@ void freq_map_omegas(double theta, int L, int w_pre, double* out) {
 }
 
 // One frequency-map table per device, for the last (theta, L, w_pretrained)
-// used: [L][64] (cos, sin) of p * omega'_i, rebuilt when the configuration
-// changes (the old one is retired, not freed, while calls may still read it).
+// used: [L][64] (cos, sin) of p * omega'_i (fp32, then fp16 as in the base
+// table), held in a buffer of cap >= L positions.  A new configuration that
+// fits is rebuilt in place; one that does not replaces the buffer with one of
+// at least twice the capacity.  Either way the device is synchronised first,
+// since calls on any stream may still read the old contents: nothing is
+// retired, so repeated calls with new lengths keep one buffer per device.
 struct FreqTable {
   int device;
   double theta;
   int L, w_pre;
+  long long cap;
   float2* ptr;
 };
 std::vector<FreqTable> g_freq_tables;
 
-int get_freq_table(double theta, int L, int w_pre, hipStream_t stream, const float2** out) {
+int get_freq_table(double theta, int L, int w_pre, hipStream_t stream, Tables* out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -197,27 +219,46 @@ int get_freq_table(double theta, int L, int w_pre, hipStream_t stream, const flo
   for (auto& t : g_freq_tables)
     if (t.device == dev) found = &t;
   if (found && found->theta == theta && found->L == L && found->w_pre == w_pre) {
-    *out = found->ptr;
+    *out = Tables{found->ptr, table16_of(found->ptr, found->cap)};
     return JL_OK;
   }
-  float2* p = nullptr;
-  e = hipMalloc(&p, (size_t)L * 64 * sizeof(float2));
-  if (e != hipSuccess) return hip_fail(e, "hipMalloc(frequency-map table)");
+  if (found) {
+    e = hipDeviceSynchronize();  // every earlier call that reads the old table is done
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  }
+  float2* p = found ? found->ptr : nullptr;
+  long long cap = found ? found->cap : 0;
+  if (cap < L) {
+    const long long want = std::max<long long>(L, 2 * cap);
+    float2* q = nullptr;
+    e = hipMalloc(&q, table_bytes(want));
+    if (e != hipSuccess) return hip_fail(e, "hipMalloc(frequency-map table)");
+    if (p != nullptr) (void)hipFree(p);
+    p = q;
+    cap = want;
+    if (found) {
+      found->ptr = p;
+      found->cap = cap;
+      found->L = -1;  // contents not valid until the build below succeeds
+    }
+  }
   double omega[64];
   freq_map_omegas(theta, L, w_pre, omega);
-  e = jl::launch_build_table(p, L, omega, stream);
+  e = jl::launch_build_table(p, const_cast<uint32_t*>(table16_of(p, cap)), L, omega, stream);
   if (e == hipSuccess) e = hipStreamSynchronize(stream);
   if (e != hipSuccess) {
-    (void)hipFree(p);
+    if (found) found->L = -1;
+    else (void)hipFree(p);
     return hip_fail(e, "building frequency-map table");
   }
   if (found) {
-    g_retired.emplace_back(found->device, found->ptr);
-    *found = FreqTable{dev, theta, L, w_pre, p};
+    found->theta = theta;
+    found->L = L;
+    found->w_pre = w_pre;
   } else {
-    g_freq_tables.push_back(FreqTable{dev, theta, L, w_pre, p});
+    g_freq_tables.push_back(FreqTable{dev, theta, L, w_pre, cap, p});
   }
-  *out = p;
+  *out = Tables{p, table16_of(p, cap)};
   return JL_OK;
 }
 
@@ -322,27 +363,27 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
       return fail(JL_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   }
   const int G = bifocal ? (int)jl_group_size(L, w_pre) : 1;
-  const float2* table = nullptr;
+  Tables tab{};
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  st = get_table(theta, L, s, &table);
+  st = get_table(theta, L, s, &tab);
   if (st != JL_OK) return st;
   // G == 1: f is the identity and the method is the base model (Sec. 3), so
   // the bifocal entry runs the vanilla kernel and matches it bit for bit.
   // The frequency map's factor s = L / w_pretrained is 1 exactly then too.
   const bool use_bifocal = bifocal && G > 1;
   const int freq_map = remote_map == JL_REMOTE_FREQ ? 1 : 0;
-  const float2* rtable = nullptr;
+  Tables rtab{};
   if (use_bifocal && freq_map) {
-    st = get_freq_table(theta, L, w_pre, s, &rtable);
+    st = get_freq_table(theta, L, w_pre, s, &rtab);
     if (st != JL_OK) return st;
   }
   const float slack = (float)g_rescale_log2.load();
   if (literal) {
     if (use_bifocal) {
       hipError_t e = jl::launch_prefill_literal((const uint16_t*)q, (const uint16_t*)k,
-                                                (const uint16_t*)v, (uint16_t*)o, lse, table,
-                                                rtable, freq_map, B, Hq, Hkv, L, G, w0, slack,
-                                                ws, s);
+                                                (const uint16_t*)v, (uint16_t*)o, lse, tab.f32,
+                                                rtab.f32, tab.f16, rtab.f16, freq_map, B, Hq,
+                                                Hkv, L, G, w0, slack, ws, s);
       if (e != hipSuccess) return hip_fail(e, "literal prefill launch");
       return ok();
     }
@@ -354,9 +395,9 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   hipEvent_t ev0, ev1;
   timing_events(0, &ev0, &ev1);
   hipError_t e = jl::launch_prefill_chunk(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,
-                                          (const uint16_t*)v, (uint16_t*)o, lse, table, rtable,
-                                          freq_map, B, Hq, Hkv, L, q_start, Lq, kv_stride, G, w0,
-                                          slack, scratch, s, ev0, ev1);
+                                          (const uint16_t*)v, (uint16_t*)o, lse, tab.f32, rtab.f32,
+                                          tab.f16, rtab.f16, freq_map, B, Hq, Hkv, L, q_start, Lq,
+                                          kv_stride, G, w0, slack, scratch, s, ev0, ev1);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   return ok();
 }
@@ -386,9 +427,9 @@ int prefill_varlen(bool bifocal, const void* q, const void* k, const void* v, vo
   if (nq * Hkv > 0x7fffffffLL || Hkv > 65535)
     return fail(JL_ERR_INVALID_ARG, "problem too large");
   const int max_len = std::min(max_seqlen, T);  // no sequence is longer than T
-  const float2* table = nullptr;
+  Tables tab{};
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  st = get_table(theta, max_len, s, &table);
+  st = get_table(theta, max_len, s, &tab);
   if (st != JL_OK) return st;
   const float slack = (float)g_rescale_log2.load();
   std::lock_guard<std::mutex> launch_lock(g_prefill_mu);
@@ -398,7 +439,8 @@ int prefill_varlen(bool bifocal, const void* q, const void* k, const void* v, vo
   hipEvent_t ev0, ev1;
   timing_events(0, &ev0, &ev1);
   hipError_t e = jl::launch_prefill_varlen(bifocal, (const uint16_t*)q, (const uint16_t*)k,
-                                           (const uint16_t*)v, (uint16_t*)o, lse, table, cu, B, T,
+                                           (const uint16_t*)v, (uint16_t*)o, lse, tab.f32, tab.f16,
+                                           cu, B, T,
                                            max_len, Hq, Hkv, w_pre, w0, slack, scratch, s, ev0,
                                            ev1);
   if (e != hipSuccess) return hip_fail(e, "varlen prefill launch");
@@ -445,16 +487,16 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
   if (ws == nullptr || ws_bytes < need)
     return fail(JL_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   if (!aligned16(ws)) return fail(JL_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
-  const float2* table = nullptr;
+  Tables tab{};
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  st = get_table(theta, max_len, s, &table);
+  st = get_table(theta, max_len, s, &tab);
   if (st != JL_OK) return st;
   double og[128];
   if (freq) freq_map_ramp(theta, w_pre, og);
   hipEvent_t ev0, ev1;
   timing_events(1, &ev0, &ev1);
   hipError_t e = jl::launch_decode(bifocal, (const uint16_t*)q, (const uint16_t*)kc,
-                                   (const uint16_t*)vc, kv_lens, max_len, (uint16_t*)o, table, B,
+                                   (const uint16_t*)vc, kv_lens, max_len, (uint16_t*)o, tab.f32, B,
                                    Hq, Hkv, w_pre, w0, (float*)ws, s, ev0, ev1, block_table,
                                    max_pages, n_pages, page_shift, freq ? og : nullptr);
   if (e != hipSuccess) return hip_fail(e, "decode launch");

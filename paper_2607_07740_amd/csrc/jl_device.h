@@ -18,6 +18,7 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- schedule
@@ -55,10 +56,12 @@ __host__ __device__ inline uint32_t fastdiv(uint32_t x, FastDiv f) {
 }
 
 // The same quotient for d >= 2 only, without the d = 1 branch (straight-line
-// code for kernels that are launched with G >= 2).
+// code for kernels that are launched with G >= 2).  For d = 1 the value is
+// meaningless but defined (the shift count is taken mod 32, as the hardware
+// shift does), so callers may form it and discard it.
 __host__ __device__ inline uint32_t fastdiv_ge2(uint32_t x, FastDiv f) {
   const uint32_t t = (uint32_t)(((uint64_t)f.m * x) >> 32);
-  return (t + ((x - t) >> 1)) >> (f.l - 1);
+  return (t + ((x - t) >> 1)) >> ((f.l - 1) & 31);
 }
 
 // Eq. (3): f(x) = floor(x / G) for x >= 0 (truncating division is the floor).
@@ -150,6 +153,29 @@ __device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
 }
 
 __device__ inline u32x4 load16(const void* p) { return *(const u32x4*)p; }
+
+// One rotate-half pair by two v_dot2_f32_bf16 (exact bf16 products, one fp32
+// rounding): from the raw words wl = (x_a, x_b) and wh = (x_{a+64}, x_{b+64})
+// and cs = (cos, sin) as bf16, with HI selecting element b,
+//   lo = x cos - x' sin,  hi = x' cos + x sin   (x = x_a or x_b, x' its partner).
+// The dot instructions sit in one assembly block with the wait states that a
+// dot result needs before another VALU instruction reads it (the compiler's
+// hazard tracking does not look inside assembly), so the results leave the
+// block ready to use.
+template <bool HI>
+__device__ inline void rot_pair_dot2(uint32_t wl, uint32_t wh, uint32_t cs, float& lo, float& hi) {
+  uint32_t p, q;
+  const uint32_t sp = HI ? 0x07060302u : 0x05040100u;  // (x, x')
+  const uint32_t sq = HI ? 0x03020706u : 0x01000504u;  // (x', x)
+  asm("v_perm_b32 %2, %5, %4, %7\n\t"
+      "v_perm_b32 %3, %5, %4, %8\n\t"
+      "s_nop 1\n\t"
+      "v_dot2_f32_bf16 %0, %2, %6, 0 neg_hi:[0,1,0]\n\t"
+      "v_dot2_f32_bf16 %1, %3, %6, 0\n\t"
+      "s_nop 3"
+      : "=&v"(lo), "=&v"(hi), "=&v"(p), "=&v"(q)
+      : "v"(wl), "v"(wh), "v"(cs), "s"(sp), "s"(sq));
+}
 
 // ------------------------------------------------- direct-to-LDS staging
 // Byte address of a __shared__ object inside the workgroup's LDS window.

@@ -7,26 +7,17 @@
 // two views (Sec. 3.3, Eq. (7)), fused into one kernel.
 //
 // Two launches per call:
-//  1. prep_kernel rotates every raw key once per view, k_loc = R(k) x_k and
-//     k_rem = R(f(k)) x_k, and transposes V, writing each 64-key tile as the
-//     exact byte image the attention kernel wants in LDS (a call-scoped
-//     buffer; the caller's K and V are only read).  Rotating a key once per
-//     call instead of once per (query block, key tile) takes the rotation and
-//     the cos/sin table out of the quadratic loop.
-//  2. prefill_kernel streams those images with direct-to-LDS copies and runs
-//     the fused two-view attention.
-//
-// Two views, one running state.  For a block of queries the key tiles that
-// hold remote pairs are visited first with the remote-rotated query operand
-// and k_rem, then the tiles that hold band pairs with the base-rotated operand
-// and k_loc; a tile straddling the band edge is visited once per view, each
-// visit keeping only its own view's elements.  Every visit produces a partial
-// softmax state over disjoint keys and is folded into the running fp32 state
-// (m, l, O) with the max-shifted, linear-space merge of Eq. (7).  Band keys
-// never enter the remote state, so the exclusion window C of Eq. (7) is empty
-// and nothing is subtracted.  The vanilla kernel is the same code with only
-// the base view.  The same kernel also runs Eq. (7) literally: three launches
-// for the windows A, B and C, each over one view, then a merge kernel.
+//  1. vt_prep_kernel transposes V into the byte image of each 64-key tile that
+//     the attention kernel reads in the PV product (a call-scoped buffer; the
+//     caller's K and V are only read).
+//  2. prefill_kernel stages raw (pre-RoPE) K tiles in LDS with direct-to-LDS
+//     copies and rotates each staged tile in registers to the view of its
+//     visit: k_loc = R(k) x_k on band tiles, k_rem = R(f(k)) x_k on remote
+//     tiles (Sec. 3.2, Eqs. (4)-(6): the cache keeps unrotated keys and the
+//     rotation is formed on the fly).  The rotated tile lives only in LDS, for
+//     the QK product of that visit; no rotated key is ever written to memory.
+//     The eight waves of a workgroup share the rotation of a tile: each
+//     rotates its own 8 keys, one rotate-half pair of 16-byte chunks per lane.
 //
 // Work decomposition: a workgroup is 8 wave64s and owns 256 query rows =
 // (head hl = r / BQ, position q0 + r % BQ) for the g = Hq/Hkv query heads
@@ -63,61 +54,71 @@
 
 namespace jl {
 
-#ifndef JL_PF_WAVES
-#define JL_PF_WAVES 8
-#endif
-constexpr int kPfWaves = JL_PF_WAVES;   // waves per workgroup; two waves per SIMD either way
+constexpr int kPfWaves = 8;             // waves per workgroup: two per SIMD
 constexpr int kPfThreads = 64 * kPfWaves;
 constexpr int kPfRows = 32 * kPfWaves;  // query rows per workgroup: 32 per wave
 constexpr int kPfBK = 64;               // keys per tile
-constexpr int kTileBytes = kPfBK * kHeadDim * 2;  // one K image or one V^T image: 16 KB
-constexpr int kSmemBytes = 2 * 2 * kTileBytes;    // double-buffered K + V^T: 64 KB
-constexpr int kPfCopyBytes = kTileBytes / kPfWaves;  // each wave's share of an image copy
-static_assert(kPfWaves == 4 || kPfWaves == 8, "4 or 8 waves per workgroup");
+constexpr int kTileBytes = kPfBK * kHeadDim * 2;  // one K tile or one V^T image: 16 KB
+constexpr int kTabBytes = kPfBK * kHalf * 4;  // a tile's cos/sin rows in fp16: 16 KB
+// LDS: raw K tiles (two buffers), rotated K tiles (two), V^T images (two) and
+// the cos/sin rows of the staged raw tiles (two)
+constexpr int kRawOff = 0, kRotOff = 2 * kTileBytes, kVtOff = 4 * kTileBytes;
+constexpr int kTabOff = 6 * kTileBytes;
+constexpr int kSmemBytes = kTabOff + 2 * kTabBytes;  // 128 KB
+constexpr int kPfCopyBytes = kTileBytes / kPfWaves;  // each wave's share of a tile copy: 8 keys
+constexpr int kKeysPerWave = kPfBK / kPfWaves;
+#ifndef JL_SCHED_QK
+#define JL_SCHED_QK 5
+#endif
+#ifndef JL_SCHED_PV
+#define JL_SCHED_PV 5
+#endif
+constexpr int kSchedValuQK = JL_SCHED_QK;  // VALU instructions issued per QK MFMA
+constexpr int kSchedValuPV = JL_SCHED_PV;  // and per PV MFMA
 
-// Tile images (byte layout, also the LDS layout):
-//   K image:   key r (0..63) at r * 256; its 16-byte chunk c (d = 8c .. 8c+7)
-//              sits in slot c ^ (r & 15).  16 lanes reading 16 keys at one d
-//              hit 16 distinct bank groups.
+// LDS layouts.
+//   K tile (raw and rotated alike): key r (0..63) at r * 256; its 16-byte
+//              chunk c (d = 8c .. 8c+7) sits in slot c ^ kswz(r), with
+//              kswz(r) = (r & 15) >> 1 | (r & 1) << 3 a permutation of 0..15.
+//              16 lanes reading 16 consecutive keys at one chunk (the QK
+//              operand reads) hit 16 distinct bank groups, and so do 16 lanes
+//              covering chunks 0..7 (or 8..15) of an even and the following
+//              odd key (the rotation's reads and writes).
+//   cos/sin rows of a tile: row i (0..63) at i * 256 holds table row
+//              row0 + i (clamped to the tile's last row) as 64 fp16 pairs;
+//              its 16-byte chunk s (pairs 4s .. 4s+3) sits in slot s ^ (i & 1),
+//              so the rotation's lanes reading two consecutive rows hit
+//              distinct bank groups (lanes on one row read the same bytes).
 //   V^T image: d (0..127) at d * 128; slot s of a row holds the 8 keys of
 //              group g = s ^ ((d >> 1) & 7), g = 2 ks + h, in the order
 //              t -> key 16 ks + 8 (t / 4) + 4 h + t % 4 (the k order of the
 //              P^T operand, i.e. of the S^T accumulator rows).  16 lanes
 //              reading 16 consecutive d at one group hit 16 distinct groups.
-__device__ inline int kimg_off(int r, int c) { return r * 256 + 16 * (c ^ (r & 15)); }
+__device__ inline int kswz(int r) { return ((r & 15) >> 1) | ((r & 1) << 3); }
+__device__ inline int kimg_off(int r, int c) { return r * 256 + 16 * (c ^ kswz(r)); }
 __device__ inline int vtimg_off(int d, int g) { return d * 128 + 16 * (g ^ ((d >> 1) & 7)); }
 
 struct PrepArgs {
-  const uint16_t* k;
   const uint16_t* v;
-  uint16_t* kloc;  // [B][Hkv][n_tiles] K images, base view
-  uint16_t* krem;  // same, remote view (bifocal only)
-  uint16_t* vt;    // [B][Hkv][n_tiles] V^T images
-  const float2* table;
-  const float2* rtable;  // remote view: table at f(p) (aliasing map) or rtable at p (frequency map)
+  uint16_t* vt;  // [B][Hkv][n_tiles] V^T images
   int B, Hkv, L, n_tiles;  // L: keys [0, L) are valid
-  int kv_stride;           // rows per sequence in k and v (>= L)
-  int freq_map;            // 0: Eq. (3) aliasing, 1: Sec. 4.5 frequency interpolation
-  FastDiv gdiv;
+  int kv_stride;           // rows per sequence in v (>= L)
   // packed variable-length batches: per tile (seq0, L, tile, tile0) with
-  // seq0 the sequence's first row of k and v and tile0 its first tile; the
-  // images of kv head h sit at (h * n_tiles + tile0 + tile); G is the
-  // sequence's own group_size(L, w_pre).  nullptr for dense batches.
+  // seq0 the sequence's first row of v and tile0 its first tile; the images
+  // of kv head h sit at (h * n_tiles + tile0 + tile).  nullptr for dense
+  // batches.
   const int4* twork;
-  int w_pre;
   int* retry_count;  // zeroed here for the attention kernel that follows
 };
 
 // One workgroup per (tile, b * Hkv + kvh), or per (tile work item, kvh) for a
 // packed batch.  Keys past the sequence's length are written as zeros.
-template <bool BIFOCAL>
-__global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
+__global__ __launch_bounds__(256) void vt_prep_kernel(PrepArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t sv[kPfBK * kHeadDim];
   if (a.retry_count != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
     *a.retry_count = 0;
   int tile, L;
   size_t seq_row, img;
-  FastDiv gdiv = a.gdiv;
   const int kvh_v = blockIdx.y;
   if (a.twork != nullptr) {
     const int4 w = a.twork[blockIdx.x];
@@ -126,7 +127,6 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
     L = w.y;
     seq_row = (size_t)w.x;
     img = ((size_t)kvh_v * a.n_tiles + w.w + tile) * (kTileBytes / 2);
-    gdiv = make_fastdiv((uint32_t)group_size(L, a.w_pre));
   } else {
     tile = blockIdx.x;
     L = a.L;
@@ -138,7 +138,6 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
   const int t = threadIdx.x;
   const int k0 = tile * kPfBK;
   const size_t row = (size_t)a.Hkv * kHeadDim;
-  const uint16_t* kseq = a.k + (seq_row * a.Hkv + kvh) * kHeadDim;
   const uint16_t* vseq = a.v + (seq_row * a.Hkv + kvh) * kHeadDim;
 
   // V tile -> LDS, zeros past L
@@ -149,42 +148,6 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs a) {
     u32x4 w = u32x4{0, 0, 0, 0};
     if (k0 + r < L) w = load16(vseq + (size_t)(k0 + r) * row + 8 * c);
     *(u32x4*)(sv + r * kHeadDim + 8 * c) = w;
-  }
-
-  // K: thread -> key r = t / 4, chunk pairs (c, c + 8), c = t % 4 and t % 4 + 4
-  {
-    const int r = t >> 2;
-    const int key = k0 + r;
-    const bool valid = key < L;
-    unsigned char* kl = (unsigned char*)(a.kloc + img);
-    unsigned char* kr = BIFOCAL ? (unsigned char*)(a.krem + img) : nullptr;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int c = (t & 3) + 4 * u;
-      float lo[8], hi[8];
-      unpack8(valid ? load16(kseq + (size_t)key * row + 8 * c) : u32x4{0, 0, 0, 0}, lo);
-      unpack8(valid ? load16(kseq + (size_t)key * row + 8 * c + kHalf) : u32x4{0, 0, 0, 0}, hi);
-#pragma unroll
-      for (int view = 0; view < (BIFOCAL ? 2 : 1); ++view) {
-        const int kp = valid ? key : 0;
-        const int pos = view == 0 || a.freq_map ? kp : remote_pos(kp, gdiv);
-        const float2* tab = view == 0 ? a.table : a.rtable;
-        const float4* c4 = (const float4*)(tab + (size_t)pos * kHalf + 8 * c);
-        float ylo[8], yhi[8];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 w = c4[q];  // (cos_i, sin_i, cos_{i+1}, sin_{i+1})
-          const int i = 2 * q;
-          ylo[i] = lo[i] * w.x - hi[i] * w.y;
-          yhi[i] = hi[i] * w.x + lo[i] * w.y;
-          ylo[i + 1] = lo[i + 1] * w.z - hi[i + 1] * w.w;
-          yhi[i + 1] = hi[i + 1] * w.z + lo[i + 1] * w.w;
-        }
-        unsigned char* dst = view == 0 ? kl : kr;
-        *(bf16x8*)(dst + kimg_off(r, c)) = pack8(ylo);
-        *(bf16x8*)(dst + kimg_off(r, c + 8)) = pack8(yhi);
-      }
-    }
   }
   __syncthreads();
 
@@ -211,10 +174,12 @@ struct PrefillArgs {
   float* lse;
   const float2* table;   // [positions][64] (cos, sin) of p * omega_i
   const float2* rtable;  // remote view: table read at f(p), or the frequency map's table at p
+  const uint32_t* table16;   // the same tables in fp16 pairs (cos low, sin high): key rotation
+  const uint32_t* rtable16;
   int freq_map;          // 0: Eq. (3) aliasing, 1: Sec. 4.5 frequency interpolation
-  const uint16_t* kloc;  // tile images from prep_kernel
-  const uint16_t* krem;
-  const uint16_t* vt;
+  const uint16_t* k;     // raw (pre-RoPE) keys, [B][kv_stride][Hkv][128] or packed [T][Hkv][128]
+  const uint16_t* vt;    // V^T tile images from vt_prep_kernel
+  int kv_stride;         // rows per sequence in k (dense batches)
   int B, Hq, Hkv, L, n_tiles;  // L: keys [0, L), the call's sequence length (G follows it)
   int q_start, Lq;              // query rows: positions q_start .. q_start + Lq - 1 (= L - Lq ..)
   int g, BQ, n_qblocks;
@@ -301,7 +266,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   constexpr bool REMOTE2 = MODE == kModeWinB || MODE == kModeWinC;  // segment 2's view
   constexpr bool OUT_F32 = MODE == kModeWinA || MODE == kModeWinB || MODE == kModeWinC;
   constexpr bool FROM_ZERO = MODE == kModeVanilla || MODE == kModeWinB;  // kt_l = 0
-  // LDS: K images in [0, 32K) (two buffers), V^T images in [32K, 64K) (two buffers)
+  // LDS: raw K tiles, rotated K tiles and V^T images, two buffers each
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmemBytes];
   __shared__ int s_bad;
 
@@ -319,8 +284,9 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     if (bid >= *a.retry_count) return;    // uniform, before any barrier
     bid = a.retry_list[bid];
   }
-  int kvh, qblk, q_start, q_end, w0;
+  int kvh, qblk, q_start, q_end, w0, Lk;  // Lk: keys [0, Lk) of the sequence are valid
   size_t row_base, lse_base, img_base;  // rows of q/o, lse entries, tile image elements
+  size_t kv_row0;                       // the sequence's first row of k
   FastDiv gdiv;
   if (a.qwork != nullptr) {
     // packed batch: the work item's sequence, its G, its tiles; the kv head
@@ -338,6 +304,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     row_base = (size_t)w.x;
     lse_base = (size_t)w.x;
     img_base = ((size_t)kvh * a.n_tiles + w.w) * (kTileBytes / 2);
+    kv_row0 = (size_t)w.x;
+    Lk = w.y;
   } else {
     int group;
     if ((n_groups & 7) == 0) {
@@ -357,6 +325,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     row_base = (size_t)b * a.Lq;
     lse_base = (size_t)b * a.Hq * a.Lq;
     img_base = (size_t)group * a.n_tiles * (kTileBytes / 2);
+    kv_row0 = (size_t)b * a.kv_stride;
+    Lk = a.L;
   }
   const int q0 = q_start + qblk * a.BQ;
   const int q1 = min(q0 + a.BQ, q_end) - 1;
@@ -378,33 +348,131 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const int kt_l = FROM_ZERO ? 0 : vr.kt_l;
   const int n_steps = n_r + (n_kt - kt_l);
 
-  // ---- staging: each wave copies its share (16 KB / waves) of a K image
-  // (k_rem or k_loc) or a V^T image into buffer j & 1 of that kind
+  // ---- staging.  For list entry j each wave copies 8 keys (2 KB) of the raw
+  // K tile, its share of the tile's cos/sin rows and its share of the V^T
+  // image into buffer jb & 1 of each kind; it rotates the same 8 keys of a
+  // staged raw tile into the rotated buffer of that parity.
   const uint32_t smem_base = lds_addr(smem);
   const uint32_t lane_off = 16 * lane;
   auto tile_of = [&](int j) __attribute__((always_inline)) { return j < n_r ? j : kt_l + (j - n_r); };
-  auto copy_share = [&](const unsigned char* g, uint32_t l) __attribute__((always_inline)) {
-    dma16_s<0>(g, lane_off, l);
-    dma16_s<1024>(g, lane_off, l);
-    if constexpr (kPfCopyBytes > 2048) {
-      dma16_s<2048>(g, lane_off, l);
-      dma16_s<3072>(g, lane_off, l);
-    }
+  // j's view: remote (R(f(k)), Eq. (3), or the frequency map's table at k) or base (R(k))
+  auto is_remote = [&](int j) __attribute__((always_inline)) { return REMOTE2 || (FUSED && j < n_r); };
+  // Scalar description of list entry j, formed once when its copies are
+  // issued and kept for its rotation a visit later.  The cos/sin rows of a
+  // tile are contiguous: p(k0) .. p(min(k0 + 63, Lk - 1)) with p = f for the
+  // aliasing remote view (at most 32 rows, as G >= 2 there) and the identity
+  // otherwise (64 rows); key k0 + r reads row f(k0 + r) - f(k0) =
+  // floor((kmod + r) / G), kmod = k0 - G f(k0), or row r.  f is formed on
+  // every entry and selected, so no branch splits the loop body (the
+  // remote-view kernels run with G >= 2).
+  struct Ent {
+    int k0, klim;  // first key; Lk - 1 - k0 (rows past it repeat the last key)
+    int row0, tlim;  // first cos/sin row; index of the last valid row
+    int kmod;
+    int alias, remote;
   };
-  // copy list entry j into buffer jb & 1 (jb = j except for the clamped copies)
-  auto issue_k = [&](int j, int jb) __attribute__((always_inline)) {
-    const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * (kPfCopyBytes / 2);
-    const bool use_rem = REMOTE2 || (FUSED && j < n_r);
-    const unsigned char* gk = (const unsigned char*)((use_rem ? a.krem : a.kloc) + off);
-    copy_share(gk, smem_base + (jb & 1) * kTileBytes + wave * kPfCopyBytes);
+  const uint32_t G_d = gdiv.d;
+  auto ent_of = [&](int j) __attribute__((always_inline)) {
+    Ent e;
+    e.k0 = tile_of(j) * kPfBK;
+    e.klim = Lk - 1 - e.k0;
+    e.remote = is_remote(j);
+    e.alias = e.remote & (a.freq_map == 0);
+    uint32_t f0 = fastdiv_ge2((uint32_t)e.k0, gdiv);
+    const int nlast = min(kPfBK - 1, e.klim);
+    uint32_t km = (uint32_t)e.k0 - G_d * f0;
+    uint32_t fl = fastdiv_ge2(km + (uint32_t)nlast, gdiv);
+    asm volatile("" : "+s"(f0), "+s"(km), "+s"(fl));
+    e.row0 = e.alias ? (int)f0 : e.k0;
+    e.kmod = e.alias ? (int)km : 0;
+    e.tlim = e.alias ? (int)fl : nlast;
+    return e;
+  };
+  const uint32_t krow_bytes = (uint32_t)a.Hkv * (kHeadDim * 2);  // from one key of k to the next
+  const size_t kseq_off = (kv_row0 * a.Hkv + kvh) * kHeadDim;    // the sequence's key 0 in k
+  // raw K copy: lane -> (key, chunk) of each 1 KB copy, in the K tile swizzle
+  const int cp_row = kKeysPerWave * wave + (lane >> 4);  // rows cp_row and cp_row + 4
+  const uint32_t cp_chunk0 = 16 * ((lane & 15) ^ kswz(cp_row));
+  const uint32_t cp_chunk1 = 16 * ((lane & 15) ^ kswz(cp_row + 4));
+  // cos/sin rows: copy h (0, 1) moves rows 32 h + 4 wave .. + 3 of the slice
+  const int tb_row = 4 * wave + (lane >> 4);
+  // copy entry e into buffers jb & 1 (jb = j except for the clamped copies)
+  auto issue_k = [&](const Ent& e, int jb) __attribute__((always_inline)) {
+    const unsigned char* gk =
+        (const unsigned char*)(a.k + kseq_off) + (size_t)e.k0 * krow_bytes;
+    const uint32_t v0 = __umul24((uint32_t)min(cp_row, e.klim), krow_bytes) + cp_chunk0;
+    const uint32_t v1 = __umul24((uint32_t)min(cp_row + 4, e.klim), krow_bytes) + cp_chunk1;
+    const uint32_t l = smem_base + kRawOff + (jb & 1) * kTileBytes + wave * kPfCopyBytes;
+    dma16_s<0>(gk, v0, l);
+    dma16_s<0>(gk, v1, l + 1024);
+    const unsigned char* gt =
+        (const unsigned char*)((e.remote ? a.rtable16 : a.table16) + (size_t)e.row0 * kHalf);
+    const uint32_t lt = smem_base + kTabOff + (jb & 1) * kTabBytes + wave * 1024;
+    dma16_s<0>(gt, (uint32_t)min(tb_row, e.tlim) * 256 + lane_off % 256, lt);
+    if (!e.alias)  // rows 32 .. 63 (the aliasing view needs at most 32)
+      dma16_s<0>(gt, (uint32_t)min(tb_row + 32, e.tlim) * 256 + lane_off % 256, lt + 8192);
   };
   auto issue_v = [&](int j, int jb) __attribute__((always_inline)) {
     const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * (kPfCopyBytes / 2);
     const unsigned char* gv = (const unsigned char*)(a.vt + off);
-    copy_share(gv, smem_base + 2 * kTileBytes + (jb & 1) * kTileBytes + wave * kPfCopyBytes);
+    const uint32_t l = smem_base + kVtOff + (jb & 1) * kTileBytes + wave * kPfCopyBytes;
+    dma16_s<0>(gv, lane_off, l);
+    dma16_s<1024>(gv, lane_off, l);
   };
-  auto kbuf = [&](int j) __attribute__((always_inline)) { return (const unsigned char*)smem + (j & 1) * kTileBytes; };
-  auto vbuf = [&](int j) __attribute__((always_inline)) { return (const unsigned char*)smem + (2 + (j & 1)) * kTileBytes; };
+  // Rotation of the staged raw tile of an entry (buffers jb & 1) to its view
+  // (Sec. 3.2): lane -> key rt_row of the tile, rotate-half pairs of chunks
+  // (rt_c, rt_c + 8), i.e. frequencies i = 8 rt_c .. 8 rt_c + 7, with the
+  // (cos, sin) of the key's position from the staged rows.  Each output is
+  // one v_dot2_f32_bf16 of the pair (x_i, x_{i+64}) with (cos, -sin) or of
+  // (x_{i+64}, x_i) with (cos, sin): exact products, an fp32 sum, then one
+  // rounding to bf16.  The result exists only in LDS.
+  const int rt_row = kKeysPerWave * wave + (lane >> 3);
+  const int rt_c = lane & 7;
+  const int rt_lo = kimg_off(rt_row, rt_c), rt_hi = kimg_off(rt_row, rt_c + 8);
+  struct RotIn {
+    u32x4 xl, xh;  // raw chunks rt_c and rt_c + 8 of key rt_row
+    u32x4 ca, cb;  // bf16 (cos, sin) of frequencies 8 rt_c .. +3 and +4 .. +7
+  };
+  auto rot_load = [&](const Ent& e, int jb) __attribute__((always_inline)) {
+    int fr = (int)fastdiv_ge2((uint32_t)(e.kmod + rt_row), gdiv);
+    asm volatile("" : "+v"(fr));  // formed unconditionally: a select, not a branch
+    const int row = e.alias ? fr : rt_row;
+    const unsigned char* tb = smem + kTabOff + (jb & 1) * kTabBytes + row * 256 + 32 * rt_c;
+    const unsigned char* src = (const unsigned char*)smem + kRawOff + (jb & 1) * kTileBytes;
+    RotIn r;
+    r.xl = *(const u32x4*)(src + rt_lo);
+    r.xh = *(const u32x4*)(src + rt_hi);
+    r.ca = *(const u32x4*)tb;
+    r.cb = *(const u32x4*)(tb + 16);
+    return r;
+  };
+  // pair i (0..7): y_i = x_i cos - x_{i+64} sin, y_{i+64} = x_{i+64} cos + x_i sin
+  auto rot_pair = [&](const RotIn& r, int i, float* ylo, float* yhi) __attribute__((always_inline)) {
+    const uint32_t wl = r.xl[i >> 1], wh = r.xh[i >> 1];
+    const uint32_t cs = i < 4 ? r.ca[i] : r.cb[i - 4];
+    if (i & 1)
+      rot_pair_dot2<true>(wl, wh, cs, ylo[i], yhi[i]);
+    else
+      rot_pair_dot2<false>(wl, wh, cs, ylo[i], yhi[i]);
+  };
+  auto rot_store = [&](int jb, const float* ylo, const float* yhi) __attribute__((always_inline)) {
+    unsigned char* dst = smem + kRotOff + (jb & 1) * kTileBytes;
+    *(bf16x8*)(dst + rt_lo) = pack8(ylo);
+    *(bf16x8*)(dst + rt_hi) = pack8(yhi);
+  };
+  auto rotate = [&](const Ent& e, int jb) __attribute__((always_inline)) {
+    const RotIn r = rot_load(e, jb);
+    float ylo[8], yhi[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) rot_pair(r, i, ylo, yhi);
+    rot_store(jb, ylo, yhi);
+  };
+  auto kbuf = [&](int j) __attribute__((always_inline)) {
+    return (const unsigned char*)smem + kRotOff + (j & 1) * kTileBytes;
+  };
+  auto vbuf = [&](int j) __attribute__((always_inline)) {
+    return (const unsigned char*)smem + kVtOff + (j & 1) * kTileBytes;
+  };
 
   // ---- state.  Scores are log2-domain (q_scale folded into Q) and come out
   // of the MFMA already relative to a per-row reference m_ref: the first
@@ -550,59 +618,143 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     ps = softmax(sc, pb);
   };
 
-  // One pipelined visit: on entry `cur` holds the scores of tile j, this
-  // wave's copies of K(j+1) and V(j) are in flight.  The QK product of tile
-  // j+1 is issued next to the softmax of tile j, then PV of tile j; K(j+2)
-  // and V(j+1) are copied meanwhile.  For the last tile of a segment the
-  // QK product reads whatever the next K buffer holds and is discarded.
-  auto visit = [&](int j, f32x16* cur, f32x16* nxt, int lo, int hi) __attribute__((always_inline)) {
+  // One pipelined visit: on entry `cur` holds the scores of tile j, the
+  // rotated K of list entry j+1 is in LDS, and this wave's copies of raw
+  // K(j+2) (with its cos/sin rows) and V(j) are in flight.  The QK product of
+  // entry j+1 is issued next to the softmax of tile j, then PV of tile j; raw
+  // K(j+3) and V(j+1) are copied meanwhile and raw K(j+2) is rotated.  For the last tile of a
+  // segment the QK product reads whatever the next K buffer holds and is
+  // discarded.
+  // pend describes entry j+2 (formed when its copies were issued); on return
+  // it describes entry j+3.
+  auto visit = [&](int j, f32x16* cur, f32x16* nxt, int lo, int hi, Ent& pend) __attribute__((always_inline)) {
     if (SAFE ? need_mask(j) : (j < lo || j > hi)) mask(j, cur);
-    wait_vmem();      // this wave's copies of K(j+1), V(j)
-    __syncthreads();  // everyone's; QK(j) and PV(j-1) are done everywhere
+    wait_vmem();      // this wave's copies of raw K(j+2), its rows, V(j)
+    __syncthreads();  // everyone's; QK(j), PV(j-1) and the rotation of j+1 are done everywhere
     bf16x8 pb[4];
-    // ask the scheduler to interleave the LDS operand reads with the MFMAs
-    // (0.8% faster fused, vanilla unchanged, measured on one box)
-    __builtin_amdgcn_iglp_opt(0);
-    qk(kbuf(j + 1), nxt);
-    // K(j+2) and V(j+1) go into the buffers QK(j) and PV(j-1) released.
-    // Issued after the QK product, so its operand reads start right after
-    // the barrier; past the list's end the last entry is copied again (into
-    // the free buffer), so no branch splits the loop body.
-    issue_k(min(j + 2, n_steps - 1), j + 2);
-    issue_v(min(j + 1, n_steps - 1), j + 1);
-    float ps = softmax(cur, pb);
-    if (CHECK_LATE)
+    if constexpr (!SAFE) {
+      // The two waves of a SIMD pass the per-tile barrier together, so a
+      // block of VALU work in one wave finds the other at the same point and
+      // the matrix core idles unless each wave feeds it between its own VALU
+      // instructions.  The visit is therefore issued as two interleaved
+      // streams, pinned by scheduling barriers: each MFMA of the QK product
+      // of j+1 is followed by its operand read and one sixteenth of the
+      // softmax of j (two probabilities, their bf16 pair and its row sum);
+      // each MFMA of the PV product of j by its operand read and one
+      // sixteenth of the rotation of j+2.
+      const unsigned char* kb = kbuf(j + 1);
+      auto kop = [&](int m) __attribute__((always_inline)) {
+        const int r = 32 * (m & 1) + kr_lane;
+        return *(const bf16x8*)(kb + kimg_off(r, 2 * (m >> 1) + hl32));
+      };
+      bf16x8 ring[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) ring[m] = kop(m);
+      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+      const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+      bf16x2 pw[16];
+      float ps0 = 0.f, ps1 = 0.f;
+#pragma unroll
+      for (int m = 0; m < 16; ++m) {
+        const int blk = m & 1, st = m >> 1;
+        nxt[blk] = mfma32(ring[m & 3], qop[st], st == 0 ? neg_m : nxt[blk]);
+        if (m + 4 < 16) ring[m & 3] = kop(m + 4);
+        const int q = m >> 2, t = 2 * (m & 3);
+        const float p0 = fast_exp2(cur[q >> 1][8 * (q & 1) + t]);
+        const float p1 = fast_exp2(cur[q >> 1][8 * (q & 1) + t + 1]);
+        pw[m] = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
+        if (m & 1)
+          ps1 = __builtin_amdgcn_fdot2_f32_bf16(pw[m], one, ps1, false);
+        else
+          ps0 = __builtin_amdgcn_fdot2_f32_bf16(pw[m], one, ps0, false);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        pb[q] = (bf16x8){pw[4 * q][0], pw[4 * q][1], pw[4 * q + 1][0], pw[4 * q + 1][1],
+                         pw[4 * q + 2][0], pw[4 * q + 2][1], pw[4 * q + 3][0], pw[4 * q + 3][1]};
+      const float ps = ps0 + ps1;
       late_bad |= __ballot(ps > p_hi);
-    else
+      l_run += ps;
+      const RotIn rin = rot_load(pend, j + 2);
+      // raw K(j+3) with its rows and V(j+1) go into the buffers that the
+      // rotation of j+1 and PV(j-1) released; past the list's end the last
+      // entry is copied again (into the free buffer).
+      const Ent e3 = ent_of(min(j + 3, n_steps - 1));
+      issue_k(e3, j + 3);
+      issue_v(min(j + 1, n_steps - 1), j + 1);
+      const unsigned char* vb = vbuf(j);
+      auto vop = [&](int m) __attribute__((always_inline)) {
+        const int d = 32 * (m & 3) + kr_lane;
+        return *(const bf16x8*)(vb + vtimg_off(d, 2 * (m >> 2) + hl32));
+      };
+#pragma unroll
+      for (int m = 0; m < 4; ++m) ring[m] = vop(m);
+      // the rotated chunks are stored early, so the writes are done well
+      // before the next barrier
+      float ylo[8], yhi[8];
+#pragma unroll
+      for (int m = 0; m < 16; ++m) {
+        acc_o[m & 3] = mfma32(ring[m & 3], pb[m >> 2], acc_o[m & 3]);
+        if (m + 4 < 16) ring[m & 3] = vop(m + 4);
+        if (m >= 1 && m < 9) {
+          rot_pair(rin, m - 1, ylo, yhi);
+          asm volatile("" : "+v"(ylo[m - 1]), "+v"(yhi[m - 1]));  // keep it in this slot
+        }
+        if (m == 9) rot_store(j + 2, ylo, yhi);  // into the buffer QK(j) released
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      pend = e3;
+    } else {
+      __builtin_amdgcn_iglp_opt(0);
+      qk(kbuf(j + 1), nxt);
+      const Ent e3 = ent_of(min(j + 3, n_steps - 1));
+      issue_k(e3, j + 3);
+      issue_v(min(j + 1, n_steps - 1), j + 1);
+      float ps = softmax(cur, pb);
       ref_fix(cur, nxt, pb, ps);
-    l_run += ps;
-    pv(vbuf(j), pb);
+      l_run += ps;
+      pv(vbuf(j), pb);
+      rotate(pend, j + 2);
+      pend = e3;
+    }
   };
   // segment [j, jend): the first tile's scores are in sc_a on entry
-  auto segment = [&](int j, int jend, int lo, int hi) __attribute__((always_inline)) {
+  auto segment = [&](int j, int jend, int lo, int hi, Ent& pend) __attribute__((always_inline)) {
     for (; j + 2 <= jend; j += 2) {
-      visit(j, sc_a, sc_b, lo, hi);
-      visit(j + 1, sc_b, sc_a, lo, hi);
+      visit(j, sc_a, sc_b, lo, hi, pend);
+      visit(j + 1, sc_b, sc_a, lo, hi, pend);
     }
-    if (j < jend) visit(j, sc_a, sc_b, lo, hi);
+    if (j < jend) visit(j, sc_a, sc_b, lo, hi, pend);
   };
 
-  // ---- prologue: the first view's query operand, K(0), V(0), K(1)
+  // ---- prologue: the first view's query operand; raw K(0), K(1) staged and
+  // rotated, V(0) and raw K(2) in flight
   const bool q_remote = n_r > 0 || REMOTE2;
   load_q_operand(qrow, hl32, q_remote ? a.rtable : a.table,
                  q_remote && !a.freq_map ? remote_pos(qp, gdiv) : qp, a.q_scale, qop);
   if (CHECK_LATE && tid == 0) s_bad = 0;  // read after the end-of-block barrier
-  issue_k(0, 0);
-  issue_v(0, 0);
-  if (n_steps > 1) issue_k(1, 1);
-  wait_vmem();
-  __syncthreads();
+  const int last = n_steps - 1;
+  Ent pend = ent_of(0);
+  {
+    const Ent e1 = ent_of(min(1, last));
+    issue_k(pend, 0);
+    issue_k(e1, 1);
+    issue_v(0, 0);
+    wait_vmem();
+    __syncthreads();
+    rotate(pend, 0);
+    rotate(e1, 1);
+  }
+  __syncthreads();  // the rows of buffer 0 are read by every wave
+  pend = ent_of(min(2, last));
+  issue_k(pend, 2);  // into buffers 0
   qk(kbuf(0), sc_a);
 
   if (FUSED && n_r > 0) {
     int lo = 0, hi = 0;
     if (!SAFE) seg1_bounds(lo, hi);
-    segment(0, n_r, lo, hi);
+    segment(0, n_r, lo, hi, pend);
     // segment 2 in the base view: its first tile's K image (in buffer n_r & 1,
     // not overwritten since) is scored again with the base-rotated operand
     load_q_operand(qrow, hl32, a.table, qp, a.q_scale, qop);
@@ -611,7 +763,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   {
     int lo = 0, hi = 0;
     if (!SAFE) seg2_bounds(lo, hi);
-    segment(n_r, n_steps, lo, hi);
+    segment(n_r, n_steps, lo, hi, pend);
   }
   wait_vmem();  // the copies past the list's end
 
@@ -691,72 +843,66 @@ __global__ __launch_bounds__(256) void literal_merge_kernel(MergeArgs a) {
 }
 
 // ---------------------------------------------------------------- launchers
-// Tile images, then the retry counter (256 B) and list (one int per
+// V^T tile images, then the retry counter (256 B) and list (one int per
 // workgroup: at most L query blocks per (b, kv head), since BQ = rows / g can
-// be as small as 1).
+// be as small as 1).  No rotated key is ever stored: K is read raw by the
+// attention kernel.
 static size_t retry_bytes(long long nwg) { return 256 + (size_t)nwg * sizeof(int); }
 
-static size_t image_bytes(bool bifocal, int B, int Hkv, int L) {
+static size_t image_bytes(int B, int Hkv, int L) {
   const size_t tiles = (size_t)(L + kPfBK - 1) / kPfBK;
-  return (size_t)(bifocal ? 3 : 2) * B * Hkv * tiles * kTileBytes;
+  return (size_t)B * Hkv * tiles * kTileBytes;
 }
 
-size_t prefill_workspace_bytes(bool bifocal, int B, int Hkv, int L) {
-  return image_bytes(bifocal, B, Hkv, L) + retry_bytes((long long)B * Hkv * L);
+size_t prefill_workspace_bytes(bool /*bifocal*/, int B, int Hkv, int L) {
+  return image_bytes(B, Hkv, L) + retry_bytes((long long)B * Hkv * L);
 }
 
 // Literal mode workspace: O_A, O_B, O_C (fp32 [B][L][Hq][128] each), then
-// LSE_A, LSE_B, LSE_C (fp32 [B][Hq][L] each), then the tile images at the next
+// LSE_A, LSE_B, LSE_C (fp32 [B][Hq][L] each), then the V^T images at the next
 // 256-byte boundary (the window passes run checked, with no rerun list).
 static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L) {
   const size_t rows = (size_t)B * L * Hq;
   return 3 * rows * kHeadDim * sizeof(float) + round256(3 * rows * sizeof(float)) +
-         image_bytes(true, B, Hkv, L);
+         image_bytes(B, Hkv, L);
 }
 
 // rtable: the remote view's table, nullptr for the aliasing map (then the
 // base table is read at f(p)); with freq_map it is read at p.  With
 // `retry`, the rerun counter and list follow the images (the prep kernel
 // zeroes the counter); without, nothing past the images is touched.
-static hipError_t launch_prep(bool bifocal, const uint16_t* k, const uint16_t* v,
-                              const float2* table, const float2* rtable, int freq_map, int B,
-                              int Hkv, int L, int kv_stride, int G, void* images, bool retry,
-                              PrefillArgs& a, hipStream_t stream) {
+static hipError_t launch_prep(const uint16_t* k, const uint16_t* v, const float2* table,
+                              const float2* rtable, const uint32_t* table16,
+                              const uint32_t* rtable16, int freq_map, int B, int Hkv, int L,
+                              int kv_stride, int G, void* images, bool retry, PrefillArgs& a,
+                              hipStream_t stream) {
   const int n_tiles = (L + kPfBK - 1) / kPfBK;
-  const size_t img = (size_t)B * Hkv * n_tiles * (kTileBytes / 2);  // bf16 elements per image set
-  a.kloc = (const uint16_t*)images;
-  a.vt = a.kloc + img;
-  a.krem = bifocal ? a.vt + img : nullptr;
-  a.retry_count = retry ? (int*)(a.kloc + (bifocal ? 3 : 2) * img) : nullptr;
+  const size_t img = (size_t)B * Hkv * n_tiles * (kTileBytes / 2);  // bf16 elements of the images
+  a.k = k;
+  a.kv_stride = kv_stride;
+  a.vt = (const uint16_t*)images;
+  a.retry_count = retry ? (int*)(a.vt + img) : nullptr;
   a.retry_list = retry ? a.retry_count + 64 : nullptr;
   a.n_tiles = n_tiles;
   a.table = table;
   a.rtable = freq_map ? rtable : table;
+  a.table16 = table16;
+  a.rtable16 = freq_map ? rtable16 : table16;
   a.freq_map = freq_map;
   a.gdiv = make_fastdiv((uint32_t)G);
 
   PrepArgs p = {};
-  p.k = k;
   p.v = v;
-  p.kloc = (uint16_t*)a.kloc;
-  p.krem = (uint16_t*)a.krem;
   p.vt = (uint16_t*)a.vt;
-  p.table = table;
-  p.rtable = a.rtable;
-  p.freq_map = freq_map;
   p.B = B;
   p.Hkv = Hkv;
   p.L = L;
   p.kv_stride = kv_stride;
   p.n_tiles = n_tiles;
-  p.gdiv = a.gdiv;
   p.retry_count = a.retry_count;
   if ((long long)B * Hkv > 65535) return hipErrorInvalidConfiguration;
-  if (bifocal)
-    hipLaunchKernelGGL(prep_kernel<true>, dim3(n_tiles, B * Hkv), dim3(256), 0, stream, p);
-  else
-    hipLaunchKernelGGL(prep_kernel<false>, dim3(n_tiles, B * Hkv), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL(vt_prep_kernel, dim3(n_tiles, B * Hkv), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -810,13 +956,15 @@ static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream
 // recorded on the stream around the attention kernel.
 hipError_t launch_prefill_chunk(bool bifocal, const uint16_t* q, const uint16_t* k,
                                 const uint16_t* v, uint16_t* o, float* lse, const float2* table,
-                                const float2* rtable, int freq_map, int B, int Hq, int Hkv, int L,
-                                int q_start, int Lq, int kv_stride, int G, int w0, float slack,
-                                void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
+                                const float2* rtable, const uint32_t* table16,
+                                const uint32_t* rtable16, int freq_map, int B, int Hq, int Hkv,
+                                int L, int q_start, int Lq, int kv_stride, int G, int w0,
+                                float slack, void* ws, hipStream_t stream, hipEvent_t ev0,
+                                hipEvent_t ev1) {
   PrefillArgs a = {};
   fill_geometry(a, B, Hq, Hkv, L, q_start, Lq, slack);
-  hipError_t e = launch_prep(bifocal, k, v, table, rtable, freq_map, B, Hkv, L, kv_stride, G, ws,
-                             true, a, stream);
+  hipError_t e = launch_prep(k, v, table, rtable, table16, rtable16, freq_map, B, Hkv, L,
+                             kv_stride, G, ws, true, a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
   a.o = o;
@@ -828,18 +976,11 @@ hipError_t launch_prefill_chunk(bool bifocal, const uint16_t* q, const uint16_t*
   return e;
 }
 
-hipError_t launch_prefill(bool bifocal, const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                          uint16_t* o, float* lse, const float2* table, const float2* rtable,
-                          int freq_map, int B, int Hq, int Hkv, int L, int G, int w0, float slack,
-                          void* ws, hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1) {
-  return launch_prefill_chunk(bifocal, q, k, v, o, lse, table, rtable, freq_map, B, Hq, Hkv, L, 0,
-                              L, L, G, w0, slack, ws, stream, ev0, ev1);
-}
-
 // Eq. (7) taken literally: the three window passes, then the merge.
 hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                   uint16_t* o, float* lse, const float2* table,
-                                  const float2* rtable, int freq_map, int B, int Hq, int Hkv,
+                                  const float2* rtable, const uint32_t* table16,
+                                  const uint32_t* rtable16, int freq_map, int B, int Hq, int Hkv,
                                   int L, int G, int w0, float slack, void* ws,
                                   hipStream_t stream) {
   const size_t rows = (size_t)B * L * Hq;
@@ -849,8 +990,8 @@ hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const ui
                  round256(3 * rows * sizeof(float));
   PrefillArgs a = {};
   fill_geometry(a, B, Hq, Hkv, L, 0, L, slack);
-  hipError_t e = launch_prep(true, k, v, table, rtable, freq_map, B, Hkv, L, L, G, images, false,
-                             a, stream);
+  hipError_t e = launch_prep(k, v, table, rtable, table16, rtable16, freq_map, B, Hkv, L, L, G,
+                             images, false, a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
   const int modes[3] = {kModeWinA, kModeWinB, kModeWinC};
@@ -973,8 +1114,8 @@ static void varlen_sizes(int B, int T, int g, long long* nq, long long* nt) {
 size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hkv) {
   long long nq, nt;
   varlen_sizes(B, T, Hq / Hkv, &nq, &nt);
-  return (size_t)(bifocal ? 3 : 2) * Hkv * nt * kTileBytes + (size_t)(nq + nt) * sizeof(int4) +
-         retry_bytes(nq * Hkv);
+  (void)bifocal;  // one V^T image set either way
+  return (size_t)Hkv * nt * kTileBytes + (size_t)(nq + nt) * sizeof(int4) + retry_bytes(nq * Hkv);
 }
 
 // Packed batch: q, o [T][Hq][128], k, v [T][Hkv][128], lse [Hq][T] (optional),
@@ -982,26 +1123,28 @@ size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hk
 // L, G and positions 0 .. L - 1 (table must cover max_len positions).
 hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t* k,
                                  const uint16_t* v, uint16_t* o, float* lse, const float2* table,
-                                 const int32_t* cu, int B, int T, int max_len, int Hq, int Hkv,
+                                 const uint32_t* table16, const int32_t* cu, int B, int T,
+                                 int max_len, int Hq, int Hkv,
                                  int w_pre, int w0, float slack, void* ws, hipStream_t stream,
                                  hipEvent_t ev0, hipEvent_t ev1) {
   long long nq, nt;
   varlen_sizes(B, T, Hq / Hkv, &nq, &nt);
   if (nq * Hkv > 0x7fffffffLL || nt > 0x7fffffffLL || Hkv > 65535)
     return hipErrorInvalidConfiguration;
-  const size_t img = (size_t)Hkv * nt * (kTileBytes / 2);  // bf16 elements per image set
+  const size_t img = (size_t)Hkv * nt * (kTileBytes / 2);  // bf16 elements of the V^T images
   PrefillArgs a = {};
   fill_geometry(a, 1, Hq, Hkv, max_len, 0, T, slack);
-  a.kloc = (const uint16_t*)ws;
-  a.vt = a.kloc + img;
-  a.krem = bifocal ? a.vt + img : nullptr;
-  int4* qwork = (int4*)((uint16_t*)ws + (bifocal ? 3 : 2) * img);
+  a.k = k;
+  a.vt = (const uint16_t*)ws;
+  int4* qwork = (int4*)((uint16_t*)ws + img);
   int4* twork = qwork + nq;
   a.retry_count = (int*)(twork + nt);
   a.retry_list = a.retry_count + 64;
   a.n_tiles = (int)nt;
   a.table = table;
   a.rtable = table;
+  a.table16 = table16;
+  a.rtable16 = table16;
   a.freq_map = 0;
   a.gdiv = make_fastdiv(1);
   a.q = q;
@@ -1026,26 +1169,16 @@ hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t
   if (e != hipSuccess) return e;
 
   PrepArgs p = {};
-  p.k = k;
   p.v = v;
-  p.kloc = (uint16_t*)a.kloc;
-  p.krem = (uint16_t*)a.krem;
   p.vt = (uint16_t*)a.vt;
-  p.table = table;
-  p.rtable = table;
   p.B = 1;
   p.Hkv = Hkv;
   p.L = max_len;
   p.kv_stride = T;
   p.n_tiles = (int)nt;
-  p.gdiv = a.gdiv;
   p.twork = twork;
   p.retry_count = a.retry_count;
-  p.w_pre = w_pre;
-  if (bifocal)
-    hipLaunchKernelGGL(prep_kernel<true>, dim3((unsigned)nt, Hkv), dim3(256), 0, stream, p);
-  else
-    hipLaunchKernelGGL(prep_kernel<false>, dim3((unsigned)nt, Hkv), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL(vt_prep_kernel, dim3((unsigned)nt, Hkv), dim3(256), 0, stream, p);
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
   if (ev0 != nullptr && (e = hipEventRecord(ev0, stream)) != hipSuccess) return e;

@@ -214,7 +214,7 @@ def test_literal_workspace_size_and_rejections():
     n = api.prefill_literal_workspace_bytes(B, Hq, Hkv, L)
     o_bytes = 3 * B * L * Hq * 128 * 4
     lse_bytes = -(-3 * B * Hq * L * 4 // 256) * 256
-    img = 3 * B * Hkv * (-(-L // 64)) * 16384
+    img = B * Hkv * (-(-L // 64)) * 16384  # V^T tile images only: K is read raw
     assert n == o_bytes + lse_bytes + img
     assert api.prefill_literal_workspace_bytes(B, 7, Hkv, L) == 0
     assert api.prefill_literal_workspace_bytes(B, Hq, Hkv, L, 64) == 0
