@@ -154,27 +154,36 @@ __device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
 
 __device__ inline u32x4 load16(const void* p) { return *(const u32x4*)p; }
 
-// One rotate-half pair by two v_dot2_f32_bf16 (exact bf16 products, one fp32
-// rounding): from the raw words wl = (x_a, x_b) and wh = (x_{a+64}, x_{b+64})
-// and cs = (cos, sin) as bf16, with HI selecting element b,
-//   lo = x cos - x' sin,  hi = x' cos + x sin   (x = x_a or x_b, x' its partner).
-// The dot instructions sit in one assembly block with the wait states that a
-// dot result needs before another VALU instruction reads it (the compiler's
-// hazard tracking does not look inside assembly), so the results leave the
-// block ready to use.
-template <bool HI>
-__device__ inline void rot_pair_dot2(uint32_t wl, uint32_t wh, uint32_t cs, float& lo, float& hi) {
-  uint32_t p, q;
-  const uint32_t sp = HI ? 0x07060302u : 0x05040100u;  // (x, x')
-  const uint32_t sq = HI ? 0x03020706u : 0x01000504u;  // (x', x)
-  asm("v_perm_b32 %2, %5, %4, %7\n\t"
-      "v_perm_b32 %3, %5, %4, %8\n\t"
+// Two rotate-half pairs by v_dot2_f32_bf16 (exact bf16 products, one fp32
+// rounding each), rounded to bf16 and packed.  From the raw words
+// wl = (x_a, x_b), wh = (x_{a+64}, x_{b+64}) and the bf16 (cos, sin) of
+// frequencies a and b (cs_a, cs_b):
+//   lo = (x_a cos_a - x_{a+64} sin_a,  x_b cos_b - x_{b+64} sin_b)
+//   hi = (x_{a+64} cos_a + x_a sin_a,  x_{b+64} cos_b + x_b sin_b)
+// The block keeps its own wait states between the permutes and the dot
+// instructions and between the dots and the conversions that read them (the
+// compiler's hazard tracking does not look inside assembly); its results come
+// from ordinary VALU conversions.
+__device__ inline void rot_word_dot2(uint32_t wl, uint32_t wh, uint32_t cs_a, uint32_t cs_b,
+                                     uint32_t& lo, uint32_t& hi) {
+  float a0, a1, b0, b1;
+  uint32_t p0, q0, p1, q1;
+  asm("v_perm_b32 %6, %11, %10, %14\n\t"   // (x_a, x_a+64)
+      "v_perm_b32 %7, %11, %10, %15\n\t"   // (x_a+64, x_a)
+      "v_perm_b32 %8, %11, %10, %16\n\t"   // (x_b, x_b+64)
+      "v_perm_b32 %9, %11, %10, %17\n\t"   // (x_b+64, x_b)
       "s_nop 1\n\t"
-      "v_dot2_f32_bf16 %0, %2, %6, 0 neg_hi:[0,1,0]\n\t"
-      "v_dot2_f32_bf16 %1, %3, %6, 0\n\t"
-      "s_nop 3"
-      : "=&v"(lo), "=&v"(hi), "=&v"(p), "=&v"(q)
-      : "v"(wl), "v"(wh), "v"(cs), "s"(sp), "s"(sq));
+      "v_dot2_f32_bf16 %2, %6, %12, 0 neg_hi:[0,1,0]\n\t"
+      "v_dot2_f32_bf16 %3, %8, %13, 0 neg_hi:[0,1,0]\n\t"
+      "v_dot2_f32_bf16 %4, %7, %12, 0\n\t"
+      "v_dot2_f32_bf16 %5, %9, %13, 0\n\t"
+      "s_nop 2\n\t"
+      "v_cvt_pk_bf16_f32 %0, %2, %3\n\t"
+      "v_cvt_pk_bf16_f32 %1, %4, %5"
+      : "=&v"(lo), "=&v"(hi), "=&v"(a0), "=&v"(a1), "=&v"(b0), "=&v"(b1), "=&v"(p0), "=&v"(q0),
+        "=&v"(p1), "=&v"(q1)
+      : "v"(wl), "v"(wh), "v"(cs_a), "v"(cs_b), "s"(0x05040100u), "s"(0x01000504u),
+        "s"(0x07060302u), "s"(0x03020706u));
 }
 
 // ------------------------------------------------- direct-to-LDS staging

@@ -201,6 +201,63 @@ struct PrefillArgs {
   int* retry_list;
 };
 
+// One workgroup's query block: workgroup -> (b, kv head, q block), longest
+// q blocks first.  When the (b, kv head) groups are a multiple of the 8 XCDs,
+// consecutive work items land on one XCD so a group's K/V tiles stay in that
+// XCD's L2.  A packed batch reads its work item from the plan instead.
+struct Work {
+  int kvh, qblk, q_start, q_end, w0, Lk;  // Lk: keys [0, Lk) of the sequence are valid
+  size_t row_base, lse_base, img_base;    // rows of q/o, lse entries, V^T image elements
+  size_t kv_row0;                         // the sequence's first row of k
+  FastDiv gdiv;
+};
+
+// false: no query block here (an unused entry of a packed batch's plan)
+__device__ inline bool work_of(const PrefillArgs& a, int bid, bool fused, Work& W) {
+  const int n_groups = a.B * a.Hkv;
+  if (a.qwork != nullptr) {
+    // packed batch: the work item's sequence, its G, its tiles; the kv head
+    // follows the XCD (bid & 7) when Hkv divides 8
+    const int item = bid / a.Hkv;
+    W.kvh = bid - item * a.Hkv;
+    const int4 w = a.qwork[item];
+    if (w.y <= 0) return false;
+    const int G = fused ? group_size(w.y, a.w_pre) : 1;
+    W.gdiv = make_fastdiv((uint32_t)G);
+    W.w0 = G > 1 ? a.w0 : INT_MAX;  // G = 1: the unmodified model, as the dense call
+    W.qblk = w.z;
+    W.q_start = 0;
+    W.q_end = w.y;
+    W.row_base = (size_t)w.x;
+    W.lse_base = (size_t)w.x;
+    W.img_base = ((size_t)W.kvh * a.n_tiles + w.w) * (kTileBytes / 2);
+    W.kv_row0 = (size_t)w.x;
+    W.Lk = w.y;
+  } else {
+    int group;
+    if ((n_groups & 7) == 0) {
+      const int work = (bid & 7) * (gridDim.x >> 3) + (bid >> 3);
+      group = work / a.n_qblocks;
+      W.qblk = a.n_qblocks - 1 - (work - group * a.n_qblocks);
+    } else {
+      W.qblk = a.n_qblocks - 1 - bid / n_groups;
+      group = bid - (bid / n_groups) * n_groups;
+    }
+    const int b = group / a.Hkv;
+    W.kvh = group - b * a.Hkv;
+    W.gdiv = a.gdiv;
+    W.w0 = a.w0;
+    W.q_start = a.q_start;
+    W.q_end = a.q_start + a.Lq;  // one past the last query position
+    W.row_base = (size_t)b * a.Lq;
+    W.lse_base = (size_t)b * a.Hq * a.Lq;
+    W.img_base = (size_t)group * a.n_tiles * (kTileBytes / 2);
+    W.kv_row0 = (size_t)b * a.kv_stride;
+    W.Lk = a.L;
+  }
+  return true;
+}
+
 // What one launch of the attention kernel computes.
 //   kModeFused    the bifocal result in one pass: remote-view tiles holding
 //                 pairs with q - k > w0, then base-view tiles of the band
@@ -275,59 +332,17 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const int lane = tid & 63;
   const int hl32 = lane >> 5;  // which 8-wide half of a 16-wide k slice this lane feeds
 
-  // ---- workgroup -> (b, kv head, q block), longest q blocks first.  When the
-  // (b, kv head) groups are a multiple of the 8 XCDs, consecutive work items
-  // land on one XCD so a group's K/V tiles stay in that XCD's L2.
-  const int n_groups = a.B * a.Hkv;
   int bid = blockIdx.x;
   if (SAFE && a.retry_list != nullptr) {  // rerun of the listed blocks only
     if (bid >= *a.retry_count) return;    // uniform, before any barrier
     bid = a.retry_list[bid];
   }
-  int kvh, qblk, q_start, q_end, w0, Lk;  // Lk: keys [0, Lk) of the sequence are valid
-  size_t row_base, lse_base, img_base;  // rows of q/o, lse entries, tile image elements
-  size_t kv_row0;                       // the sequence's first row of k
-  FastDiv gdiv;
-  if (a.qwork != nullptr) {
-    // packed batch: the work item's sequence, its G, its tiles; the kv head
-    // follows the XCD (bid & 7) when Hkv divides 8
-    const int item = bid / a.Hkv;
-    kvh = bid - item * a.Hkv;
-    const int4 w = a.qwork[item];
-    if (w.y <= 0) return;  // no query block here (uniform, before any barrier)
-    const int G = FUSED ? group_size(w.y, a.w_pre) : 1;
-    gdiv = make_fastdiv((uint32_t)G);
-    w0 = G > 1 ? a.w0 : INT_MAX;  // G = 1: the unmodified model, as the dense call
-    qblk = w.z;
-    q_start = 0;
-    q_end = w.y;
-    row_base = (size_t)w.x;
-    lse_base = (size_t)w.x;
-    img_base = ((size_t)kvh * a.n_tiles + w.w) * (kTileBytes / 2);
-    kv_row0 = (size_t)w.x;
-    Lk = w.y;
-  } else {
-    int group;
-    if ((n_groups & 7) == 0) {
-      const int work = (bid & 7) * (gridDim.x >> 3) + (bid >> 3);
-      group = work / a.n_qblocks;
-      qblk = a.n_qblocks - 1 - (work - group * a.n_qblocks);
-    } else {
-      qblk = a.n_qblocks - 1 - bid / n_groups;
-      group = bid - (bid / n_groups) * n_groups;
-    }
-    const int b = group / a.Hkv;
-    kvh = group - b * a.Hkv;
-    gdiv = a.gdiv;
-    w0 = a.w0;
-    q_start = a.q_start;
-    q_end = a.q_start + a.Lq;  // one past the last query position
-    row_base = (size_t)b * a.Lq;
-    lse_base = (size_t)b * a.Hq * a.Lq;
-    img_base = (size_t)group * a.n_tiles * (kTileBytes / 2);
-    kv_row0 = (size_t)b * a.kv_stride;
-    Lk = a.L;
-  }
+  Work W;
+  if (!work_of(a, bid, FUSED, W)) return;  // uniform, before any barrier
+  const int kvh = W.kvh, qblk = W.qblk, q_start = W.q_start, q_end = W.q_end, w0 = W.w0, Lk = W.Lk;
+  const size_t row_base = W.row_base, lse_base = W.lse_base, img_base = W.img_base;
+  const size_t kv_row0 = W.kv_row0;
+  const FastDiv gdiv = W.gdiv;
   const int q0 = q_start + qblk * a.BQ;
   const int q1 = min(q0 + a.BQ, q_end) - 1;
 
@@ -408,7 +423,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     const unsigned char* gt =
         (const unsigned char*)((e.remote ? a.rtable16 : a.table16) + (size_t)e.row0 * kHalf);
     const uint32_t lt = smem_base + kTabOff + (jb & 1) * kTabBytes + wave * 1024;
-    dma16_s<0>(gt, (uint32_t)min(tb_row, e.tlim) * 256 + lane_off % 256, lt);
+    if (4 * wave <= e.tlim)  // rows past the last one are never read
+      dma16_s<0>(gt, (uint32_t)min(tb_row, e.tlim) * 256 + lane_off % 256, lt);
     if (!e.alias)  // rows 32 .. 63 (the aliasing view needs at most 32)
       dma16_s<0>(gt, (uint32_t)min(tb_row + 32, e.tlim) * 256 + lane_off % 256, lt + 8192);
   };
@@ -446,26 +462,26 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     r.cb = *(const u32x4*)(tb + 16);
     return r;
   };
-  // pair i (0..7): y_i = x_i cos - x_{i+64} sin, y_{i+64} = x_{i+64} cos + x_i sin
-  auto rot_pair = [&](const RotIn& r, int i, float* ylo, float* yhi) __attribute__((always_inline)) {
-    const uint32_t wl = r.xl[i >> 1], wh = r.xh[i >> 1];
-    const uint32_t cs = i < 4 ? r.ca[i] : r.cb[i - 4];
-    if (i & 1)
-      rot_pair_dot2<true>(wl, wh, cs, ylo[i], yhi[i]);
-    else
-      rot_pair_dot2<false>(wl, wh, cs, ylo[i], yhi[i]);
+  // word w (0..3) of the rotated chunks: frequencies 8 rt_c + 2w and + 1
+  auto rot_word = [&](const RotIn& r, int w, u32x4& lo, u32x4& hi) __attribute__((always_inline)) {
+    const uint32_t cs_a = w < 2 ? r.ca[2 * w] : r.cb[2 * w - 4];
+    const uint32_t cs_b = w < 2 ? r.ca[2 * w + 1] : r.cb[2 * w - 3];
+    uint32_t l, h;
+    rot_word_dot2(r.xl[w], r.xh[w], cs_a, cs_b, l, h);
+    lo[w] = l;
+    hi[w] = h;
   };
-  auto rot_store = [&](int jb, const float* ylo, const float* yhi) __attribute__((always_inline)) {
+  auto rot_store = [&](int jb, const u32x4& lo, const u32x4& hi) __attribute__((always_inline)) {
     unsigned char* dst = smem + kRotOff + (jb & 1) * kTileBytes;
-    *(bf16x8*)(dst + rt_lo) = pack8(ylo);
-    *(bf16x8*)(dst + rt_hi) = pack8(yhi);
+    *(u32x4*)(dst + rt_lo) = lo;
+    *(u32x4*)(dst + rt_hi) = hi;
   };
   auto rotate = [&](const Ent& e, int jb) __attribute__((always_inline)) {
     const RotIn r = rot_load(e, jb);
-    float ylo[8], yhi[8];
+    u32x4 lo, hi;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) rot_pair(r, i, ylo, yhi);
-    rot_store(jb, ylo, yhi);
+    for (int w = 0; w < 4; ++w) rot_word(r, w, lo, hi);
+    rot_store(jb, lo, hi);
   };
   auto kbuf = [&](int j) __attribute__((always_inline)) {
     return (const unsigned char*)smem + kRotOff + (j & 1) * kTileBytes;
@@ -690,18 +706,15 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       };
 #pragma unroll
       for (int m = 0; m < 4; ++m) ring[m] = vop(m);
-      // the rotated chunks are stored early, so the writes are done well
-      // before the next barrier
-      float ylo[8], yhi[8];
+      // the rotated words in units 1, 4, 7, 10; stored early, so the writes
+      // are done well before the next barrier
+      u32x4 rlo, rhi;
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
         acc_o[m & 3] = mfma32(ring[m & 3], pb[m >> 2], acc_o[m & 3]);
         if (m + 4 < 16) ring[m & 3] = vop(m + 4);
-        if (m >= 1 && m < 9) {
-          rot_pair(rin, m - 1, ylo, yhi);
-          asm volatile("" : "+v"(ylo[m - 1]), "+v"(yhi[m - 1]));  // keep it in this slot
-        }
-        if (m == 9) rot_store(j + 2, ylo, yhi);  // into the buffer QK(j) released
+        if (m % 3 == 1 && m < 12) rot_word(rin, m / 3, rlo, rhi);
+        if (m == 11) rot_store(j + 2, rlo, rhi);  // into the buffer QK(j) released
         __builtin_amdgcn_sched_barrier(0);
       }
       pend = e3;
