@@ -25,6 +25,21 @@
  *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
  *    stream).  Arguments are validated on the host before anything is
  *    launched; on any error nothing is written and nothing is launched.
+ *  - Where a call allocates or waits.  The library keeps per-device caches
+ *    that a call may have to build or grow; only then does it allocate and
+ *    wait, and a later call with the same or a smaller shape does neither:
+ *      - the RoPE cos/sin table (per device and rope_theta, grown by
+ *        doubling to cover the call's positions): every prefill and decode
+ *        entry point; growing allocates and waits for `stream`;
+ *      - the prefill scratch (per device and stream): jl_bifocal_prefill,
+ *        jl_rope_attention, their _map, _chunk and _varlen forms; growing
+ *        waits for `stream`, frees the old buffer and allocates;
+ *      - the frequency-map table (one per device): jl_bifocal_prefill_map
+ *        with JL_REMOTE_FREQ; a new (rope_theta, L, w_pretrained) waits for
+ *        the whole device, then rebuilds the table in place, or in a buffer
+ *        of at least twice the capacity when L does not fit.
+ *    The literal and decode entry points use the caller's workspace and
+ *    allocate nothing else.  jl_release_caches frees every cache.
  *  - Thread safety: calls may come from several host threads; the library's
  *    only shared state (a per-device cache of cos/sin tables) is guarded by a
  *    mutex.  Calls that share output buffers must be ordered by the caller.
@@ -247,7 +262,8 @@ size_t jl_decode_workspace_bytes(int B, int Hq, int Hkv, int max_len, int head_d
  *            16-byte aligned; its contents on entry do not matter.
  * G is taken per sequence from L = kv_lens[b] on the device, so one cache
  * serves every length and G change without being rewritten.
- * Requires Hq % Hkv == 0 and Hq / Hkv <= 8.
+ * Requires Hq % Hkv == 0 and Hq / Hkv <= 8; max_len > 8388608 (2^23)
+ * returns JL_ERR_UNSUPPORTED.
  */
 int jl_bifocal_decode(const void* q, const void* k_cache, const void* v_cache,
                       const int32_t* kv_lens, int max_len, void* o, int B, int Hq, int Hkv,

@@ -63,6 +63,7 @@ hipError_t launch_debug_tiles(int L, int BQ, int BK, int w0, int nqb, int nkt, i
 namespace {
 
 constexpr int kHeadDim = 128;
+constexpr int kDecodeMaxLen = 1 << 23;  // 512-byte table rows, 32-bit offsets
 thread_local std::string t_detail;
 // how far (log2 units) a prefill tile's score maximum may lie from the softmax
 // reference before the reference moves; the debug entry lowers it so tests
@@ -476,6 +477,10 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
   int st = check_common(B, Hq, Hkv, head_dim, theta);
   if (st != JL_OK) return st;
   if (max_len < 1) return fail(JL_ERR_INVALID_ARG, "max_len must be >= 1 (got %d)", max_len);
+  // the split kernel addresses cos/sin table rows with 32-bit byte offsets
+  if (max_len > kDecodeMaxLen)
+    return fail(JL_ERR_UNSUPPORTED, "decode max_len %d exceeds %d positions", max_len,
+                kDecodeMaxLen);
   if (bifocal && w_pre < 1)
     return fail(JL_ERR_INVALID_ARG, "w_pretrained must be >= 1 (got %d)", w_pre);
   if (bifocal && w0 < 0) return fail(JL_ERR_INVALID_ARG, "w_local must be >= 0 (got %d)", w0);

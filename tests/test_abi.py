@@ -177,9 +177,26 @@ def _decode(q=A, kc=A, vc=A, lens=A2, max_len=1024, o=A, B=2, Hq=8, Hkv=2, d=128
     (dict(q=MIS), api.JL_ERR_INVALID_ARG),
     (dict(ws=None), api.JL_ERR_WORKSPACE),
     (dict(ws_bytes=16), api.JL_ERR_WORKSPACE),
+    (dict(max_len=(1 << 23) + 16), api.JL_ERR_UNSUPPORTED),  # table rows past 32-bit offsets
 ])
 def test_decode_rejects_before_launch(kw, code):
     assert _decode(**kw) == code
+
+
+def test_decode_length_limit_is_exact():
+    # 2^23 positions is the last length the split kernel's 32-bit table
+    # offsets cover; the check rejects one step past it on the host, for the
+    # dense, paged and frequency-map forms alike
+    L = api.lib()
+    assert _decode(max_len=(1 << 23) + 1) == api.JL_ERR_UNSUPPORTED
+    assert "8388608" in L.jl_last_error().decode()
+    ws = 1 << 40  # any size: the length check comes first
+    rc = L.jl_bifocal_decode_paged(A, A, A, A2, (1 << 23) // 64 + 1, 64, 10, A2, A, 1, 8, 2, 128,
+                                   1e6, 64, 8, A, ws, None)
+    assert rc == api.JL_ERR_UNSUPPORTED
+    rc = L.jl_bifocal_decode_map(A, A, A, A2, (1 << 23) + 1, A, 1, 8, 2, 128, 1e6, 64, 8, 1, A,
+                                 ws, None)
+    assert rc == api.JL_ERR_UNSUPPORTED
 
 
 def test_workspace_size_is_positive_and_monotone():
