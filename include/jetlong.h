@@ -164,6 +164,35 @@ int jl_rope_attention_chunk(const void* q, const void* k_cache, const void* v_ca
                             int max_len, int head_dim, double rope_theta, void* stream);
 
 /*
+ * jl_bifocal_prefill_chunk over paged caches (Sec. 3.2: the raw cache is
+ * read, never rewritten, whatever G the chunk's length gives).
+ *   k_pages, v_pages bf16 [n_pages, page_size, Hkv, head_dim] device pools
+ *   block_table int32 [B, max_pages] (device): key x of sequence b is row
+ *               x % page_size of page block_table[b][x / page_size]
+ * The pages of keys [0, q_start + n_queries) must be written (the chunk's own
+ * keys included); entries outside [0, n_pages) are clamped into the pool
+ * (garbage in, no fault).  The output equals jl_bifocal_prefill_chunk's on a
+ * dense cache holding the same rows, bit for bit.  page_size must be a power
+ * of two, max_pages, n_pages >= 1, and q_start + n_queries <=
+ * max_pages * page_size (else JL_ERR_INVALID_ARG); page_size < 64 (a page
+ * must hold whole 64-key tiles) or more than 4096 pages per sequence (the
+ * attention kernel keeps the list in LDS) -> JL_ERR_UNSUPPORTED.  q, o, lse,
+ * scratch and the other arguments and errors as in jl_bifocal_prefill_chunk.
+ */
+int jl_bifocal_prefill_chunk_paged(const void* q, const void* k_pages, const void* v_pages,
+                                   const int32_t* block_table, int max_pages, int page_size,
+                                   int n_pages, void* o, float* lse, int B, int Hq, int Hkv,
+                                   int q_start, int n_queries, int head_dim, double rope_theta,
+                                   int w_pretrained, int w_local, void* stream);
+
+/* The vanilla counterpart of jl_bifocal_prefill_chunk_paged. */
+int jl_rope_attention_chunk_paged(const void* q, const void* k_pages, const void* v_pages,
+                                  const int32_t* block_table, int max_pages, int page_size,
+                                  int n_pages, void* o, float* lse, int B, int Hq, int Hkv,
+                                  int q_start, int n_queries, int head_dim, double rope_theta,
+                                  void* stream);
+
+/*
  * Packed (variable-length) bifocal prefill: B independent sequences of
  * different lengths in one call, each computed exactly as jl_bifocal_prefill
  * would compute it alone -- its own L, G = max(1, ceil(L / w_pretrained))

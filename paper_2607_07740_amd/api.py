@@ -57,6 +57,12 @@ def lib() -> ctypes.CDLL:
         L.jl_rope_attention_chunk.restype = i32
         L.jl_rope_attention_chunk.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
                                               i32, dbl, vp]
+        L.jl_bifocal_prefill_chunk_paged.restype = i32
+        L.jl_bifocal_prefill_chunk_paged.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, i32,
+                                                     i32, i32, i32, i32, i32, dbl, i32, i32, vp]
+        L.jl_rope_attention_chunk_paged.restype = i32
+        L.jl_rope_attention_chunk_paged.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, i32,
+                                                    i32, i32, i32, i32, i32, dbl, vp]
         L.jl_bifocal_prefill_varlen.restype = i32
         L.jl_bifocal_prefill_varlen.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
                                                 i32, dbl, i32, i32, vp]
@@ -207,6 +213,40 @@ def prefill_chunk(q, k_cache, v_cache, *, q_start: int, w_pretrained: int = 1, w
                                               _stream(stream)))
     else:
         _check(lib().jl_rope_attention_chunk(*args, _stream(stream)))
+    return (out, lse) if want_lse else out
+
+
+def prefill_chunk_paged(q, k_pages, v_pages, block_table, *, q_start: int,
+                        w_pretrained: int = 1, w_local: int = 0, rope_theta: float = 1e6,
+                        bifocal: bool = True, out=None, lse=None, want_lse: bool = False,
+                        stream=None):
+    """jl_bifocal_prefill_chunk_paged / jl_rope_attention_chunk_paged: q [B, n, Hq, 128] raw
+    queries at positions q_start .. q_start + n - 1, pools [n_pages, page_size, Hkv, 128] raw,
+    block_table int32 [B, max_pages] on the device."""
+    import torch
+    B, n, Hq, D = q.shape
+    n_pages, page_size, Hkv, _ = k_pages.shape
+    if k_pages.shape != (n_pages, page_size, Hkv, D) or v_pages.shape != k_pages.shape:
+        raise ValueError("page pools must be [n_pages, page_size, Hkv, D]")
+    if block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError("block_table must be [B, max_pages]")
+    max_pages = block_table.shape[1]
+    if out is None:
+        out = torch.empty_like(q)
+    want_lse = want_lse or lse is not None
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, n), dtype=torch.float32, device=q.device)
+    args = [_dev(q, "q", torch.bfloat16), _dev(k_pages, "k_pages", torch.bfloat16),
+            _dev(v_pages, "v_pages", torch.bfloat16),
+            _dev(block_table, "block_table", torch.int32), max_pages, page_size, n_pages,
+            _dev(out, "out", torch.bfloat16),
+            _dev(lse, "lse", torch.float32) if lse is not None else None, B, Hq, Hkv,
+            int(q_start), n, D, float(rope_theta)]
+    if bifocal:
+        _check(lib().jl_bifocal_prefill_chunk_paged(*args, int(w_pretrained), int(w_local),
+                                                    _stream(stream)))
+    else:
+        _check(lib().jl_rope_attention_chunk_paged(*args, _stream(stream)))
     return (out, lse) if want_lse else out
 
 

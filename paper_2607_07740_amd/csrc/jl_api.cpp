@@ -25,7 +25,8 @@ hipError_t launch_prefill_chunk(bool bifocal, const uint16_t* q, const uint16_t*
                                 const uint32_t* rtable16, int freq_map, int B, int Hq, int Hkv,
                                 int L, int q_start, int Lq, int kv_stride, int G, int w0,
                                 float slack, void* ws, hipStream_t stream, hipEvent_t ev0,
-                                hipEvent_t ev1);
+                                hipEvent_t ev1, const int32_t* block_table, int max_pages,
+                                int page_shift, int n_pages);
 size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hkv);
 hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t* k,
                                  const uint16_t* v, uint16_t* o, float* lse, const float2* table,
@@ -63,7 +64,11 @@ hipError_t launch_debug_tiles(int L, int BQ, int BK, int w0, int nqb, int nkt, i
 namespace {
 
 constexpr int kHeadDim = 128;
-constexpr int kDecodeMaxLen = 1 << 23;  // 512-byte table rows, 32-bit offsets
+constexpr int kDecodeMaxLen = 1 << 23;
+// paged chunked prefill: a page holds whole 64-key tiles, and one sequence's
+// page list fits the attention kernel's LDS table
+constexpr int kPagedPrefillMinPage = 64;
+constexpr int kPagedPrefillMaxPages = 4096;  // 512-byte table rows, 32-bit offsets
 thread_local std::string t_detail;
 // how far (log2 units) a prefill tile's score maximum may lie from the softmax
 // reference before the reference moves; the debug entry lowers it so tests
@@ -332,7 +337,8 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
                    int B, int Hq, int Hkv, int L, int head_dim, double theta, int w_pre, int w0,
                    void* stream, bool literal = false, void* ws = nullptr, size_t ws_bytes = 0,
                    int remote_map = JL_REMOTE_ALIAS, int q_start = 0, int Lq = -1,
-                   int kv_stride = -1) {
+                   int kv_stride = -1, const int32_t* block_table = nullptr, int max_pages = 0,
+                   int page_shift = 0, int n_pages = 0) {
   // a chunk: queries q_start .. q_start + Lq - 1 over keys [0, L) of a cache
   // with kv_stride rows per sequence; the full prefill has Lq = kv_stride = L
   if (Lq < 0) Lq = L;
@@ -398,7 +404,8 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   hipError_t e = jl::launch_prefill_chunk(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,
                                           (const uint16_t*)v, (uint16_t*)o, lse, tab.f32, rtab.f32,
                                           tab.f16, rtab.f16, freq_map, B, Hq, Hkv, L, q_start, Lq,
-                                          kv_stride, G, w0, slack, scratch, s, ev0, ev1);
+                                          kv_stride, G, w0, slack, scratch, s, ev0, ev1,
+                                          block_table, max_pages, page_shift, n_pages);
   if (e != hipSuccess) return hip_fail(e, "prefill launch");
   return ok();
 }
@@ -565,6 +572,63 @@ static int prefill_chunk(bool bifocal, const void* q, const void* k_cache, const
   return prefill_common(bifocal, q, k_cache, v_cache, o, lse, B, Hq, Hkv, q_start + n_queries,
                         head_dim, theta, w_pre, w0, stream, false, nullptr, 0, JL_REMOTE_ALIAS,
                         q_start, n_queries, max_len);
+}
+
+// A chunk over paged pools: the same call with key k of sequence b in page
+// block_table[b][k / page_size].  Pages hold whole 64-key tiles, and the
+// attention kernel keeps one sequence's page list in LDS.
+static int prefill_chunk_paged(bool bifocal, const void* q, const void* k_pages,
+                               const void* v_pages, const int32_t* block_table, int max_pages,
+                               int page_size, int n_pages, void* o, float* lse, int B, int Hq,
+                               int Hkv, int q_start, int n_queries, int head_dim, double theta,
+                               int w_pre, int w0, void* stream) {
+  if (!aligned4(block_table))
+    return fail(JL_ERR_INVALID_ARG, "block_table must be non-null and 4-byte aligned");
+  if (page_size < 1 || page_size > (1 << 20) || (page_size & (page_size - 1)) != 0)
+    return fail(JL_ERR_INVALID_ARG, "page_size must be a power of two in [64, 2^20] (got %d)",
+                page_size);
+  if (page_size < kPagedPrefillMinPage)
+    return fail(JL_ERR_UNSUPPORTED, "paged prefill needs page_size >= %d (got %d)",
+                kPagedPrefillMinPage, page_size);
+  if (max_pages < 1 || n_pages < 1)
+    return fail(JL_ERR_INVALID_ARG, "max_pages and n_pages must be >= 1 (got %d, %d)", max_pages,
+                n_pages);
+  if (q_start < 0) return fail(JL_ERR_INVALID_ARG, "q_start must be >= 0 (got %d)", q_start);
+  if (n_queries < 1) return fail(JL_ERR_INVALID_ARG, "n_queries must be >= 1 (got %d)", n_queries);
+  const long long L = (long long)q_start + n_queries;
+  if (L > (long long)max_pages * page_size)
+    return fail(JL_ERR_INVALID_ARG, "q_start + n_queries (%lld) exceeds max_pages * page_size",
+                L);
+  if (L > 0x7fffffffLL) return fail(JL_ERR_INVALID_ARG, "q_start + n_queries too large");
+  const long long pages = (L + page_size - 1) / page_size;
+  if (pages > kPagedPrefillMaxPages)
+    return fail(JL_ERR_UNSUPPORTED, "paged prefill reads %lld pages per sequence (at most %d)",
+                pages, kPagedPrefillMaxPages);
+  int page_shift = 0;
+  while ((1 << page_shift) < page_size) ++page_shift;
+  return prefill_common(bifocal, q, k_pages, v_pages, o, lse, B, Hq, Hkv, (int)L, head_dim,
+                        theta, w_pre, w0, stream, false, nullptr, 0, JL_REMOTE_ALIAS, q_start,
+                        n_queries, (int)L, block_table, max_pages, page_shift, n_pages);
+}
+
+int jl_bifocal_prefill_chunk_paged(const void* q, const void* k_pages, const void* v_pages,
+                                   const int32_t* block_table, int max_pages, int page_size,
+                                   int n_pages, void* o, float* lse, int B, int Hq, int Hkv,
+                                   int q_start, int n_queries, int head_dim, double rope_theta,
+                                   int w_pretrained, int w_local, void* stream) {
+  return prefill_chunk_paged(true, q, k_pages, v_pages, block_table, max_pages, page_size,
+                             n_pages, o, lse, B, Hq, Hkv, q_start, n_queries, head_dim,
+                             rope_theta, w_pretrained, w_local, stream);
+}
+
+int jl_rope_attention_chunk_paged(const void* q, const void* k_pages, const void* v_pages,
+                                  const int32_t* block_table, int max_pages, int page_size,
+                                  int n_pages, void* o, float* lse, int B, int Hq, int Hkv,
+                                  int q_start, int n_queries, int head_dim, double rope_theta,
+                                  void* stream) {
+  return prefill_chunk_paged(false, q, k_pages, v_pages, block_table, max_pages, page_size,
+                             n_pages, o, lse, B, Hq, Hkv, q_start, n_queries, head_dim,
+                             rope_theta, 1, 0, stream);
 }
 
 int jl_bifocal_prefill_chunk(const void* q, const void* k_cache, const void* v_cache, void* o,

@@ -109,7 +109,18 @@ struct PrepArgs {
   // batches.
   const int4* twork;
   int* retry_count;  // zeroed here for the attention kernel that follows
+  // paged caches (nullptr otherwise): v is a pool [n_pages][page][Hkv][128]
+  // and key k of sequence b sits in page block_table[b][k >> page_shift]
+  const int32_t* block_table;
+  int max_pages, page_shift, n_pages;
 };
+
+// Pool row of key k0 (the first key of a tile; pages hold whole tiles) in
+// page `page`, clamped into the pool.
+__device__ inline size_t paged_row(int page, int n_pages, int page_shift, int k0) {
+  page = page < 0 ? 0 : (page >= n_pages ? n_pages - 1 : page);
+  return ((size_t)page << page_shift) + (size_t)(k0 & ((1 << page_shift) - 1));
+}
 
 // One workgroup per (tile, b * Hkv + kvh), or per (tile work item, kvh) for a
 // packed batch.  Keys past the sequence's length are written as zeros.
@@ -138,7 +149,14 @@ __global__ __launch_bounds__(256) void vt_prep_kernel(PrepArgs a) {
   const int t = threadIdx.x;
   const int k0 = tile * kPfBK;
   const size_t row = (size_t)a.Hkv * kHeadDim;
-  const uint16_t* vseq = a.v + (seq_row * a.Hkv + kvh) * kHeadDim;
+  // the tile's first key row: paged pools hold whole tiles in a page
+  size_t trow = seq_row + k0;
+  if (a.block_table != nullptr) {
+    const int b = blockIdx.y / a.Hkv;
+    trow = paged_row(a.block_table[(size_t)b * a.max_pages + (k0 >> a.page_shift)], a.n_pages,
+                     a.page_shift, k0);
+  }
+  const uint16_t* vtile = a.v + (trow * a.Hkv + kvh) * kHeadDim;
 
   // V tile -> LDS, zeros past L
 #pragma unroll
@@ -146,7 +164,7 @@ __global__ __launch_bounds__(256) void vt_prep_kernel(PrepArgs a) {
     const int idx = t + 256 * i;  // 64 keys x 16 chunks
     const int r = idx >> 4, c = idx & 15;
     u32x4 w = u32x4{0, 0, 0, 0};
-    if (k0 + r < L) w = load16(vseq + (size_t)(k0 + r) * row + 8 * c);
+    if (k0 + r < L) w = load16(vtile + (size_t)r * row + 8 * c);
     *(u32x4*)(sv + r * kHeadDim + 8 * c) = w;
   }
   __syncthreads();
@@ -174,7 +192,7 @@ struct PrefillArgs {
   float* lse;
   const float2* table;   // [positions][64] (cos, sin) of p * omega_i
   const float2* rtable;  // remote view: table read at f(p), or the frequency map's table at p
-  const uint32_t* table16;   // the same tables in fp16 pairs (cos low, sin high): key rotation
+  const uint32_t* table16;   // the same tables as bf16 pairs (cos low, sin high): key rotation
   const uint32_t* rtable16;
   int freq_map;          // 0: Eq. (3) aliasing, 1: Sec. 4.5 frequency interpolation
   const uint16_t* k;     // raw (pre-RoPE) keys, [B][kv_stride][Hkv][128] or packed [T][Hkv][128]
@@ -199,14 +217,21 @@ struct PrefillArgs {
   // a counter and the workgroup indices; nullptr where unused
   int* retry_count;
   int* retry_list;
+  // paged caches (nullptr otherwise): k is a pool [n_pages][page][Hkv][128],
+  // pages of at least 64 keys, so a tile lies in one page
+  const int32_t* block_table;
+  int max_pages, page_shift, n_pages;
 };
+
+// Most pages of one sequence a paged prefill block looks up (LDS table)
+constexpr int kMaxSeqPages = 4096;
 
 // One workgroup's query block: workgroup -> (b, kv head, q block), longest
 // q blocks first.  When the (b, kv head) groups are a multiple of the 8 XCDs,
 // consecutive work items land on one XCD so a group's K/V tiles stay in that
 // XCD's L2.  A packed batch reads its work item from the plan instead.
 struct Work {
-  int kvh, qblk, q_start, q_end, w0, Lk;  // Lk: keys [0, Lk) of the sequence are valid
+  int b, kvh, qblk, q_start, q_end, w0, Lk;  // Lk: keys [0, Lk) of the sequence are valid
   size_t row_base, lse_base, img_base;    // rows of q/o, lse entries, V^T image elements
   size_t kv_row0;                         // the sequence's first row of k
   FastDiv gdiv;
@@ -219,6 +244,7 @@ __device__ inline bool work_of(const PrefillArgs& a, int bid, bool fused, Work& 
     // packed batch: the work item's sequence, its G, its tiles; the kv head
     // follows the XCD (bid & 7) when Hkv divides 8
     const int item = bid / a.Hkv;
+    W.b = 0;
     W.kvh = bid - item * a.Hkv;
     const int4 w = a.qwork[item];
     if (w.y <= 0) return false;
@@ -244,6 +270,7 @@ __device__ inline bool work_of(const PrefillArgs& a, int bid, bool fused, Work& 
       group = bid - (bid / n_groups) * n_groups;
     }
     const int b = group / a.Hkv;
+    W.b = b;
     W.kvh = group - b * a.Hkv;
     W.gdiv = a.gdiv;
     W.w0 = a.w0;
@@ -313,7 +340,7 @@ __device__ inline float sum8(bf16x8 p, float acc) {
 // itself; the SAFE launch that follows reruns only the listed blocks with the
 // per-tile check, which moves the reference as needed.  Window modes always
 // run SAFE.
-template <int MODE, bool SAFE>
+template <int MODE, bool SAFE, bool PAGED = false>
 __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   constexpr bool CHECK_LATE = !SAFE;
   // The visit list has at most two segments: the fused kernel's remote tiles
@@ -326,6 +353,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // LDS: raw K tiles, rotated K tiles and V^T images, two buffers each
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kSmemBytes];
   __shared__ int s_bad;
+  __shared__ int s_pages[PAGED ? kMaxSeqPages : 1];  // paged caches: the sequence's pages
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -415,6 +443,16 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   auto issue_k = [&](const Ent& e, int jb) __attribute__((always_inline)) {
     const unsigned char* gk =
         (const unsigned char*)(a.k + kseq_off) + (size_t)e.k0 * krow_bytes;
+    if constexpr (PAGED) {  // the tile's page (clamped already; a page holds whole tiles)
+      const int page = __builtin_amdgcn_readfirstlane(s_pages[e.k0 >> a.page_shift]);
+      const size_t prow = ((size_t)page << a.page_shift) + (e.k0 & ((1 << a.page_shift) - 1));
+      const uint64_t p = (uint64_t)(a.k + (prow * a.Hkv + kvh) * kHeadDim);
+      // the copy takes its base in SGPRs: keep the (uniform) address there.
+      // readfirstlane returns int: widen each half as unsigned (no sign fill)
+      const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+      const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p);
+      gk = (const unsigned char*)(((uint64_t)hi << 32) | lo);
+    }
     const uint32_t v0 = __umul24((uint32_t)min(cp_row, e.klim), krow_bytes) + cp_chunk0;
     const uint32_t v1 = __umul24((uint32_t)min(cp_row + 4, e.klim), krow_bytes) + cp_chunk1;
     const uint32_t l = smem_base + kRawOff + (jb & 1) * kTileBytes + wave * kPfCopyBytes;
@@ -748,6 +786,14 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
                  q_remote && !a.freq_map ? remote_pos(qp, gdiv) : qp, a.q_scale, qop);
   if (CHECK_LATE && tid == 0) s_bad = 0;  // read after the end-of-block barrier
   const int last = n_steps - 1;
+  if constexpr (PAGED) {  // the sequence's page list, clamped into the pool
+    const int np = min((Lk + (1 << a.page_shift) - 1) >> a.page_shift, kMaxSeqPages);
+    for (int i = tid; i < np; i += kPfThreads) {
+      const int pg = a.block_table[(size_t)W.b * a.max_pages + i];
+      s_pages[i] = pg < 0 ? 0 : (pg >= a.n_pages ? a.n_pages - 1 : pg);
+    }
+    __syncthreads();
+  }
   Ent pend = ent_of(0);
   {
     const Ent e1 = ent_of(min(1, last));
@@ -885,11 +931,20 @@ size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L) {
 // base table is read at f(p)); with freq_map it is read at p.  With
 // `retry`, the rerun counter and list follow the images (the prep kernel
 // zeroes the counter); without, nothing past the images is touched.
+struct Paging {
+  const int32_t* block_table;  // nullptr: dense caches
+  int max_pages, page_shift, n_pages;
+};
+
 static hipError_t launch_prep(const uint16_t* k, const uint16_t* v, const float2* table,
                               const float2* rtable, const uint32_t* table16,
                               const uint32_t* rtable16, int freq_map, int B, int Hkv, int L,
                               int kv_stride, int G, void* images, bool retry, PrefillArgs& a,
-                              hipStream_t stream) {
+                              hipStream_t stream, Paging pg = Paging{nullptr, 0, 0, 0}) {
+  a.block_table = pg.block_table;
+  a.max_pages = pg.max_pages;
+  a.page_shift = pg.page_shift;
+  a.n_pages = pg.n_pages;
   const int n_tiles = (L + kPfBK - 1) / kPfBK;
   const size_t img = (size_t)B * Hkv * n_tiles * (kTileBytes / 2);  // bf16 elements of the images
   a.k = k;
@@ -914,6 +969,10 @@ static hipError_t launch_prep(const uint16_t* k, const uint16_t* v, const float2
   p.kv_stride = kv_stride;
   p.n_tiles = n_tiles;
   p.retry_count = a.retry_count;
+  p.block_table = pg.block_table;
+  p.max_pages = pg.max_pages;
+  p.page_shift = pg.page_shift;
+  p.n_pages = pg.n_pages;
   if ((long long)B * Hkv > 65535) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL(vt_prep_kernel, dim3(n_tiles, B * Hkv), dim3(256), 0, stream, p);
   return hipGetLastError();
@@ -937,12 +996,12 @@ static void fill_geometry(PrefillArgs& a, int B, int Hq, int Hkv, int L, int q_s
 
 // The fused and vanilla modes: the fast pass over the grid, then the checked
 // pass over the blocks it listed (same grid size; the rest exit at once).
-template <int MODE>
+template <int MODE, bool PAGED = false>
 static hipError_t launch_fast_then_checked(const PrefillArgs& a, dim3 grid, hipStream_t stream) {
-  hipLaunchKernelGGL((prefill_kernel<MODE, false>), grid, dim3(kPfThreads), 0, stream, a);
+  hipLaunchKernelGGL((prefill_kernel<MODE, false, PAGED>), grid, dim3(kPfThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((prefill_kernel<MODE, true>), grid, dim3(kPfThreads), 0, stream, a);
+  hipLaunchKernelGGL((prefill_kernel<MODE, true, PAGED>), grid, dim3(kPfThreads), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -952,6 +1011,11 @@ static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream
   const dim3 grid((unsigned)nwg), block(kPfThreads);
   PrefillArgs w = a;
   w.retry_list = nullptr;  // the window passes check every tile
+  if (a.block_table != nullptr) {  // paged caches: the chunk entry points only
+    if (mode == kModeFused) return launch_fast_then_checked<kModeFused, true>(a, grid, stream);
+    if (mode == kModeVanilla) return launch_fast_then_checked<kModeVanilla, true>(a, grid, stream);
+    return hipErrorInvalidValue;
+  }
   switch (mode) {
     case kModeFused: return launch_fast_then_checked<kModeFused>(a, grid, stream);
     case kModeVanilla: return launch_fast_then_checked<kModeVanilla>(a, grid, stream);
@@ -973,11 +1037,13 @@ hipError_t launch_prefill_chunk(bool bifocal, const uint16_t* q, const uint16_t*
                                 const uint32_t* rtable16, int freq_map, int B, int Hq, int Hkv,
                                 int L, int q_start, int Lq, int kv_stride, int G, int w0,
                                 float slack, void* ws, hipStream_t stream, hipEvent_t ev0,
-                                hipEvent_t ev1) {
+                                hipEvent_t ev1, const int32_t* block_table, int max_pages,
+                                int page_shift, int n_pages) {
   PrefillArgs a = {};
   fill_geometry(a, B, Hq, Hkv, L, q_start, Lq, slack);
   hipError_t e = launch_prep(k, v, table, rtable, table16, rtable16, freq_map, B, Hkv, L,
-                             kv_stride, G, ws, true, a, stream);
+                             kv_stride, G, ws, true, a, stream,
+                             Paging{block_table, max_pages, page_shift, n_pages});
   if (e != hipSuccess) return e;
   a.q = q;
   a.o = o;

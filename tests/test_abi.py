@@ -93,6 +93,48 @@ def test_prefill_chunk_rejects_bad_ranges(q_start, n, max_len):
         assert L.jl_last_error().decode() != ""
 
 
+def _chunk_paged(bifocal=True, **kw):
+    a = dict(table=A2, max_pages=8, page_size=64, n_pages=20, B=1, Hq=8, Hkv=2, q_start=100,
+             n=60, d=128)
+    a.update(kw)
+    args = [A, A, A, a["table"], a["max_pages"], a["page_size"], a["n_pages"], A, None, a["B"],
+            a["Hq"], a["Hkv"], a["q_start"], a["n"], a["d"], 1e6]
+    L = api.lib()
+    if bifocal:
+        return L.jl_bifocal_prefill_chunk_paged(*args, 64, 8, None)
+    return L.jl_rope_attention_chunk_paged(*args, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(table=None), api.JL_ERR_INVALID_ARG),
+    (dict(table=MIS), api.JL_ERR_INVALID_ARG),
+    (dict(page_size=0), api.JL_ERR_INVALID_ARG),
+    (dict(page_size=96), api.JL_ERR_INVALID_ARG),
+    (dict(page_size=1 << 21), api.JL_ERR_INVALID_ARG),
+    (dict(page_size=32), api.JL_ERR_UNSUPPORTED),  # a page must hold whole 64-key tiles
+    (dict(max_pages=0), api.JL_ERR_INVALID_ARG),
+    (dict(n_pages=0), api.JL_ERR_INVALID_ARG),
+    (dict(q_start=-1), api.JL_ERR_INVALID_ARG),
+    (dict(n=0), api.JL_ERR_INVALID_ARG),
+    (dict(q_start=500, n=13), api.JL_ERR_INVALID_ARG),  # 513 keys > 8 pages of 64
+    (dict(B=0), api.JL_ERR_INVALID_ARG),
+    (dict(d=64), api.JL_ERR_UNSUPPORTED),
+])
+def test_prefill_chunk_paged_rejects_before_launch(kw, code):
+    for bif in (True, False):
+        assert _chunk_paged(bif, **kw) == code, kw
+        assert api.lib().jl_last_error().decode() != ""
+
+
+def test_prefill_chunk_paged_page_count_limit_is_exact():
+    # one sequence's page list must fit the attention kernel's 4096-entry LDS
+    # table; B = 0 makes a call that passes the page checks fail just after
+    big = dict(max_pages=5000, page_size=64, q_start=0, B=0)
+    assert _chunk_paged(n=4096 * 64, **big) == api.JL_ERR_INVALID_ARG
+    assert _chunk_paged(n=4096 * 64 + 1, **big) == api.JL_ERR_UNSUPPORTED
+    assert "4096" in api.lib().jl_last_error().decode()
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(T=0), api.JL_ERR_INVALID_ARG),
     (dict(max_seqlen=0), api.JL_ERR_INVALID_ARG),
