@@ -299,6 +299,29 @@ int jl_bifocal_decode(const void* q, const void* k_cache, const void* v_cache,
                       int head_dim, double rope_theta, int w_pretrained, int w_local,
                       void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * jl_bifocal_decode for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments and results, bit for bit, without the
+ * workspace: the split states and the fp32 cos/sin table live in one fixed
+ * device array that the library holds on each device it runs on until the
+ * process ends (88 MiB: the table of positions [0, 131072) and 24 MiB of
+ * states).  No call allocates or frees device memory.
+ *   max_len > 131072, or split states above 24 MiB
+ *   (jl_decode_workspace_bytes(B, Hq, Hkv, max_len, 128) > 25165824)
+ *     -> JL_ERR_UNSUPPORTED, checked on the host before any device work.
+ * The first call on a device for a given rope_theta builds the table and
+ * waits for it on `stream` (make that call outside graph capture); later
+ * calls with that theta launch the two decode kernels only.  Every call on a
+ * device shares that device's array, so calls that overlap on one device
+ * (other streams, other threads) race; serialise them.  Other requirements
+ * and errors as in jl_bifocal_decode.
+ */
+int jl_bifocal_decode_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                              const int32_t* kv_lens, int max_len, void* o, int B, int Hq,
+                              int Hkv, int head_dim, double rope_theta, int w_pretrained,
+                              int w_local, void* stream);
+
 /* Vanilla RoPE decode with the same kernels (base rotation for every key). */
 int jl_rope_attention_decode(const void* q, const void* k_cache, const void* v_cache,
                              const int32_t* kv_lens, int max_len, void* o, int B, int Hq,

@@ -86,6 +86,9 @@ def lib() -> ctypes.CDLL:
         L.jl_bifocal_decode.restype = i32
         L.jl_bifocal_decode.argtypes = [vp, vp, vp, vp, i32, vp, i32, i32, i32, i32, dbl, i32, i32,
                                         vp, sz, vp]
+        L.jl_bifocal_decode_noalloc.restype = i32
+        L.jl_bifocal_decode_noalloc.argtypes = [vp, vp, vp, vp, i32, vp, i32, i32, i32, i32, dbl,
+                                                i32, i32, vp]
         L.jl_rope_attention_decode.restype = i32
         L.jl_rope_attention_decode.argtypes = [vp, vp, vp, vp, i32, vp, i32, i32, i32, i32, dbl,
                                                vp, sz, vp]
@@ -352,6 +355,27 @@ def _decode(bifocal, q, k_cache, v_cache, kv_lens, w_pretrained, w_local, rope_t
                                        _stream(stream)))
     else:
         _check(lib().jl_rope_attention_decode(*args, *ws, _stream(stream)))
+    return out
+
+
+def bifocal_decode_noalloc(q, k_cache, v_cache, kv_lens, *, w_pretrained: int, w_local: int,
+                           rope_theta: float = 1e6, out=None, stream=None):
+    """jl_bifocal_decode_noalloc: jl_bifocal_decode without a workspace; the library's
+    fixed per-device array holds the split states and the cos/sin table."""
+    import torch
+    B, Hq, D = q.shape
+    _, max_len, Hkv, _ = k_cache.shape
+    if k_cache.shape != (B, max_len, Hkv, D) or v_cache.shape != k_cache.shape:
+        raise ValueError("caches must be [B, max_len, Hkv, D]")
+    if kv_lens.shape != (B,):
+        raise ValueError("kv_lens must be [B]")
+    if out is None:
+        out = torch.empty_like(q)
+    _check(lib().jl_bifocal_decode_noalloc(
+        _dev(q, "q", torch.bfloat16), _dev(k_cache, "k_cache", torch.bfloat16),
+        _dev(v_cache, "v_cache", torch.bfloat16), _dev(kv_lens, "kv_lens", torch.int32),
+        max_len, _dev(out, "out", torch.bfloat16), B, Hq, Hkv, D, float(rope_theta),
+        int(w_pretrained), int(w_local), _stream(stream)))
     return out
 
 

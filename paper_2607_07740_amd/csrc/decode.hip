@@ -22,6 +22,8 @@
 // window state and the remote-only state of Sec. 3.3.  The reduce kernel
 // merges all (split, view) states of a head with the max-shifted,
 // linear-space rule of Eq. (7) in fp32.
+#include <mutex>
+
 #include "jl_device.h"
 
 namespace jl {
@@ -811,6 +813,63 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
   if (ev1 != nullptr && (e = hipEventRecord(ev1, stream)) != hipSuccess) return e;
   hipLaunchKernelGGL(decode_reduce_kernel, dim3(B * Hq, 4), dim3(256), 0, stream, a, o);
   return hipGetLastError();
+}
+
+// ------------------------------------- fixed device scratch (no allocation)
+// For callers that cannot allocate device memory (code under graph capture,
+// tight serving loops): one file-scope array per device holds the fp32
+// cos/sin table of positions [0, kNoAllocMaxLen) and the split states.  The
+// array lives as long as the process.  Calls on one device share it, and each
+// keeps the last call's contents (the table stays, the states are rewritten
+// in full by every call), so calls that overlap on one device race.
+constexpr int kNoAllocMaxLen = 1 << 17;
+constexpr size_t kNoAllocTableBytes = (size_t)kNoAllocMaxLen * kHalf * sizeof(float2);  // 64 MiB
+constexpr size_t kNoAllocStateBytes = (size_t)24 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocTableBytes + kNoAllocStateBytes];
+
+hipError_t launch_build_table(float2* table, uint32_t* table16, int n_pos, const double* omega,
+                              hipStream_t stream);
+
+int noalloc_decode_max_len() { return kNoAllocMaxLen; }
+size_t noalloc_decode_state_bytes() { return kNoAllocStateBytes; }
+
+namespace {
+struct NoAllocDevice {
+  unsigned char* ptr = nullptr;  // this device's copy of `scratch`
+  double theta = 0.0;            // rope_theta of the table it holds (0: none yet)
+};
+std::mutex g_noalloc_mu;
+NoAllocDevice g_noalloc[64];
+}  // namespace
+
+// The current device's table and state regions.  The first call on a device
+// looks the array's address up (with that device current); the first call
+// for a new theta builds the table from omega and waits for it, so that a
+// call on any stream may read it afterwards.
+hipError_t noalloc_decode_buffers(double theta, const double* omega, hipStream_t stream,
+                                  const float2** table, float** states) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  NoAllocDevice& d = g_noalloc[dev];
+  if (d.ptr == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress((void**)&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    d.ptr = (unsigned char*)p;
+  }
+  if (d.theta != theta) {
+    d.theta = 0.0;
+    e = launch_build_table((float2*)d.ptr, nullptr, kNoAllocMaxLen, omega, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return e;
+    d.theta = theta;
+  }
+  *table = (const float2*)d.ptr;
+  *states = (float*)(d.ptr + kNoAllocTableBytes);
+  return hipSuccess;
 }
 
 }  // namespace jl

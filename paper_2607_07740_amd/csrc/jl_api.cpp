@@ -52,6 +52,10 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
                          hipStream_t stream, hipEvent_t ev0, hipEvent_t ev1,
                          const int32_t* block_table, int max_pages, int n_pages, int page_shift,
                          const double* freq_og);
+int noalloc_decode_max_len();
+size_t noalloc_decode_state_bytes();
+hipError_t noalloc_decode_buffers(double theta, const double* omega, hipStream_t stream,
+                                  const float2** table, float** states);
 hipError_t launch_build_table(float2* table, uint32_t* table16, int n_pos, const double* omega,
                               hipStream_t stream);
 hipError_t launch_debug_schedule(const int32_t* lengths, int nl, const int32_t* positions, int np,
@@ -135,6 +139,11 @@ struct Tables {
 // A larger request doubles the capacity (waiting for the stream once); the
 // superseded table is kept until jl_release_caches (calls in flight on other
 // streams may still read it), so the retired total stays below the live one.
+// omega_i = theta^(-2i/d), i < d/2 (Sec. 2, the RoPE frequencies)
+void rope_omega(double theta, double* omega) {
+  for (int i = 0; i < kHeadDim / 2; ++i) omega[i] = std::pow(theta, -2.0 * i / (double)kHeadDim);
+}
+
 int get_table(double theta, int n_pos, hipStream_t stream, Tables* out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -154,8 +163,8 @@ int get_table(double theta, int n_pos, hipStream_t stream, Tables* out) {
   float2* p = nullptr;
   e = hipMalloc(&p, table_bytes(cap));
   if (e != hipSuccess) return hip_fail(e, "hipMalloc(rope table)");
-  double omega[64];
-  for (int i = 0; i < 64; ++i) omega[i] = std::pow(theta, -2.0 * i / (double)kHeadDim);
+  double omega[kHeadDim / 2];
+  rope_omega(theta, omega);
   e = jl::launch_build_table(p, const_cast<uint32_t*>(table16_of(p, cap)), (int)cap, omega, stream);
   if (e == hipSuccess) e = hipStreamSynchronize(stream);  // usable from any stream afterwards
   if (e != hipSuccess) {
@@ -461,7 +470,8 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
                   const int32_t* kv_lens, int max_len, void* o, int B, int Hq, int Hkv,
                   int head_dim, double theta, int w_pre, int w0, void* ws, size_t ws_bytes,
                   void* stream, const int32_t* block_table = nullptr, int max_pages = 0,
-                  int page_size = 0, int n_pages = 0, int remote_map = JL_REMOTE_ALIAS) {
+                  int page_size = 0, int n_pages = 0, int remote_map = JL_REMOTE_ALIAS,
+                  bool noalloc = false) {
   int page_shift = 0;
   if (remote_map != JL_REMOTE_ALIAS && remote_map != JL_REMOTE_FREQ)
     return fail(JL_ERR_INVALID_ARG, "remote_map must be JL_REMOTE_ALIAS or JL_REMOTE_FREQ (got %d)",
@@ -495,12 +505,32 @@ int decode_common(bool bifocal, const void* q, const void* kc, const void* vc,
     return fail(JL_ERR_INVALID_ARG, "q, k_cache, v_cache, o must be non-null and 16-byte aligned");
   if (!aligned4(kv_lens)) return fail(JL_ERR_INVALID_ARG, "kv_lens must be non-null and aligned");
   if (Hq / Hkv > 8) return fail(JL_ERR_UNSUPPORTED, "decode GQA group %d > 8", Hq / Hkv);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (noalloc) {  // the fixed scratch: bounded sizes, no allocation, no timing events
+    if (max_len > jl::noalloc_decode_max_len())
+      return fail(JL_ERR_UNSUPPORTED, "no-alloc decode: max_len %d exceeds %d", max_len,
+                  jl::noalloc_decode_max_len());
+    const size_t states = jl::decode_workspace_bytes(B, Hq, Hkv, max_len);
+    if (states > jl::noalloc_decode_state_bytes())
+      return fail(JL_ERR_UNSUPPORTED, "no-alloc decode: %zu bytes of split states exceed %zu",
+                  states, jl::noalloc_decode_state_bytes());
+    double omega[kHeadDim / 2];
+    rope_omega(theta, omega);
+    const float2* table = nullptr;
+    float* st_ws = nullptr;
+    hipError_t e = jl::noalloc_decode_buffers(theta, omega, s, &table, &st_ws);
+    if (e != hipSuccess) return hip_fail(e, "no-alloc decode scratch");
+    e = jl::launch_decode(bifocal, (const uint16_t*)q, (const uint16_t*)kc, (const uint16_t*)vc,
+                          kv_lens, max_len, (uint16_t*)o, table, B, Hq, Hkv, w_pre, w0, st_ws, s,
+                          nullptr, nullptr, block_table, max_pages, n_pages, page_shift, nullptr);
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+    return ok();
+  }
   const size_t need = jl::decode_map_workspace_bytes(B, Hq, Hkv, max_len, freq);
   if (ws == nullptr || ws_bytes < need)
     return fail(JL_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   if (!aligned16(ws)) return fail(JL_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
   Tables tab{};
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   st = get_table(theta, max_len, s, &tab);
   if (st != JL_OK) return st;
   double og[128];
@@ -701,6 +731,15 @@ int jl_bifocal_decode(const void* q, const void* k_cache, const void* v_cache,
                       void* workspace, size_t workspace_bytes, void* stream) {
   return decode_common(true, q, k_cache, v_cache, kv_lens, max_len, o, B, Hq, Hkv, head_dim,
                        rope_theta, w_pretrained, w_local, workspace, workspace_bytes, stream);
+}
+
+int jl_bifocal_decode_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                              const int32_t* kv_lens, int max_len, void* o, int B, int Hq,
+                              int Hkv, int head_dim, double rope_theta, int w_pretrained,
+                              int w_local, void* stream) {
+  return decode_common(true, q, k_cache, v_cache, kv_lens, max_len, o, B, Hq, Hkv, head_dim,
+                       rope_theta, w_pretrained, w_local, nullptr, 0, stream, nullptr, 0, 0, 0,
+                       JL_REMOTE_ALIAS, true);
 }
 
 int jl_rope_attention_decode(const void* q, const void* k_cache, const void* v_cache,

@@ -241,6 +241,23 @@ def test_decode_length_limit_is_exact():
     assert rc == api.JL_ERR_UNSUPPORTED
 
 
+def test_noalloc_decode_bounds_are_checked_on_the_host():
+    # the fixed array holds the table of 131072 positions and 24 MiB of split
+    # states; larger calls are refused before any device work
+    L = api.lib()
+    args = lambda B, Hq, Hkv, n: (A, A, A, A2, n, A, B, Hq, Hkv, 128, 1e6, 64, 8, None)
+    assert L.jl_bifocal_decode_noalloc(*args(1, 8, 2, 131073)) == api.JL_ERR_UNSUPPORTED
+    assert "131072" in L.jl_last_error().decode()
+    big = api.decode_workspace_bytes(64, 64, 8, 131072)
+    assert big > 24 << 20
+    assert L.jl_bifocal_decode_noalloc(*args(64, 64, 8, 131072)) == api.JL_ERR_UNSUPPORTED
+    assert "states" in L.jl_last_error().decode()
+    # the usual checks come first
+    assert L.jl_bifocal_decode_noalloc(*args(0, 8, 2, 1024)) == api.JL_ERR_INVALID_ARG
+    assert L.jl_bifocal_decode_noalloc(A, A, A, None, 1024, A, 1, 8, 2, 128, 1e6, 64, 8,
+                                       None) == api.JL_ERR_INVALID_ARG
+
+
 def test_workspace_size_is_positive_and_monotone():
     a = api.decode_workspace_bytes(1, 32, 8, 131072)
     b = api.decode_workspace_bytes(8, 32, 8, 131072)
