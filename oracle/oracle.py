@@ -18,6 +18,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "jl_oracle.c")
 _LIB = os.path.join(_HERE, "libjloracle.so")
+# JETLONG_ORACLE_LIB may name a prebuilt variant (the sanitizer build); it is loaded as is
+_LIB_OVERRIDE = os.environ.get("JETLONG_ORACLE_LIB")
 
 _lib = None
 
@@ -35,8 +37,11 @@ def build(force: bool = False) -> str:
 def _load():
     global _lib
     if _lib is None:
-        build()  # compiles when the library is missing or older than the source
-        lib = ctypes.CDLL(_LIB)
+        if _LIB_OVERRIDE:
+            lib = ctypes.CDLL(_LIB_OVERRIDE)
+        else:
+            build()  # compiles when the library is missing or older than the source
+            lib = ctypes.CDLL(_LIB)
         i64, i32, dbl, vp = ctypes.c_int64, ctypes.c_int, ctypes.c_double, ctypes.c_void_p
         lib.jlo_group_size.restype = i64
         lib.jlo_group_size.argtypes = [i64, i64]

@@ -11,7 +11,8 @@ import os
 import re
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libjetlong.so")
+# JETLONG_LIB may name another build of the same library (the host-sanitizer build)
+LIB_PATH = os.environ.get("JETLONG_LIB") or os.path.join(HERE, "libjetlong.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "jetlong.h")
 
 JL_OK, JL_ERR_INVALID_ARG, JL_ERR_UNSUPPORTED, JL_ERR_WORKSPACE, JL_ERR_HIP = range(5)
