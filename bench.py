@@ -329,8 +329,11 @@ def main() -> int:
 
     # e[0..3]: whole prefill and decode calls; e[4..7]: the attention kernel
     # and the decode split kernel alone, recorded by the library on the same
-    # stream right around those launches
+    # stream right around those launches -- on even steps only: the records
+    # inside a call add gaps of their own, so the whole-call decode time after
+    # a prefill comes from the odd steps (every step when there is only one)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(args.steps)]
+    inner = [i % 2 == 0 for i in range(args.steps)]
     for e in ev:
         for x in e:
             x.record(stream)  # creates the HIP events before they are handed over
@@ -338,8 +341,12 @@ def main() -> int:
     t0 = time.perf_counter()
     for i in range(args.steps):
         e = ev[i]
-        api.debug_kernel_events(0, e[4], e[5])
-        api.debug_kernel_events(1, e[6], e[7])
+        if inner[i]:
+            api.debug_kernel_events(0, e[4], e[5])
+            api.debug_kernel_events(1, e[6], e[7])
+        else:
+            api.debug_kernel_events(0)
+            api.debug_kernel_events(1)
         e[0].record(stream)
         prefill()
         e[1].record(stream)
@@ -352,9 +359,10 @@ def main() -> int:
     api.debug_kernel_events(1)
 
     pre_ms = [e[0].elapsed_time(e[1]) for e in ev]
-    dec_ms = [e[2].elapsed_time(e[3]) for e in ev]
-    attn_ms = [e[4].elapsed_time(e[5]) for e in ev]
-    split_ms = [e[6].elapsed_time(e[7]) for e in ev]
+    plain = [e for e, x in zip(ev, inner) if not x] or ev
+    dec_ms = [e[2].elapsed_time(e[3]) for e in plain]
+    attn_ms = [e[4].elapsed_time(e[5]) for e, x in zip(ev, inner) if x]
+    split_ms = [e[6].elapsed_time(e[7]) for e, x in zip(ev, inner) if x]
     pre_avg = sum(pre_ms) / len(pre_ms)
     dec_avg = sum(dec_ms) / len(dec_ms)
     attn_avg = sum(attn_ms) / len(attn_ms)
@@ -384,9 +392,9 @@ def main() -> int:
     # decode per call as a model issues it: one layer's call after another on
     # the stream with no host synchronisation in between (alternating the two
     # caches, so no call finds the previous one's K/V in the Infinity Cache);
-    # batches of vanilla and bifocal calls interleave
-    # the split kernel of the middle call of each bifocal batch is timed with
-    # events the library records on the stream right around it
+    # batches of vanilla and bifocal calls interleave.  A third batch per
+    # repetition, not part of the call timings, times the split kernel of its
+    # middle call with events the library records on the stream right around it
     sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(args.decode_reps)]
     for x, y in sev:
@@ -405,7 +413,8 @@ def main() -> int:
     torch.cuda.synchronize()
     for r in range(args.decode_reps):
         dv_.append(timed(lambda: decode_batch(False)) / args.decode_batch)
-        db_.append(timed(lambda: decode_batch(True, sev[r])) / args.decode_batch)
+        db_.append(timed(lambda: decode_batch(True)) / args.decode_batch)
+        decode_batch(True, sev[r])  # the split kernel timed alone, outside the call timings
     med = lambda x: sorted(x)[len(x) // 2] if x else float("nan")
     dec_med = med(db_)
     dec_gbps = (kv_bytes + io_bytes) / (dec_med * 1e-3) / 1e9

@@ -10,30 +10,30 @@
 //  1. vt_prep_kernel transposes V into the byte image of each 64-key tile that
 //     the attention kernel reads in the PV product (a call-scoped buffer; the
 //     caller's K and V are only read).
-//  2. prefill_kernel stages raw (pre-RoPE) K tiles in LDS with direct-to-LDS
-//     copies and rotates each staged tile in registers to the view of its
-//     visit: k_loc = R(k) x_k on band tiles, k_rem = R(f(k)) x_k on remote
-//     tiles (Sec. 3.2, Eqs. (4)-(6): the cache keeps unrotated keys and the
-//     rotation is formed on the fly).  The rotated tile lives only in LDS, for
-//     the QK product of that visit; no rotated key is ever written to memory.
-//     The eight waves of a workgroup share the rotation of a tile: each
-//     rotates its own 8 keys, one rotate-half pair of 16-byte chunks per lane.
+//  2. prefill_kernel reads raw (pre-RoPE) K tiles from memory straight into
+//     registers, 8 keys per wave, with the cos/sin rows of their positions,
+//     and rotates them to the view of the visit: k_loc = R(k) x_k on band
+//     tiles, k_rem = R(f(k)) x_k on remote tiles (Sec. 3.2, Eqs. (4)-(6): the
+//     cache keeps unrotated keys and the rotation is formed on the fly).  The
+//     rotated tile lives only in LDS, for the QK product of that visit; no
+//     rotated key is ever written to memory.  Each wave rotates its own 8
+//     keys, one rotate-half pair of 16-byte chunks per lane.
 //
 // Work decomposition: a workgroup is 8 wave64s and owns 256 query rows =
 // (head hl = r / BQ, position q0 + r % BQ) for the g = Hq/Hkv query heads
 // sharing one kv head (GQA packing), BQ = 256 / g.  One workgroup fills a CU
-// (64 KB of LDS), so every SIMD runs two waves; each K/V tile copied into LDS
-// serves 256 rows (a 4-wave, 128-row build is 3% slower: twice the tile
-// traffic from L2 and into LDS per flop).  A wave owns 32 rows; a
+// (two waves per SIMD at 256 VGPRs each; 64 KB of LDS), and each rotated K
+// tile and V^T image in LDS serves its 256 rows.  A wave owns 32 rows; a
 // lane owns one query column of S^T = K Q^T (v_mfma_f32_32x32x16_bf16, lanes l
 // and l + 32 split the column's 16 accumulator rows), and O^T += V^T P^T takes
-// P^T straight from the S^T accumulator registers.  K images and V^T images
-// of 64-key tiles are double-buffered separately.  The loop is software
-// pipelined: while the softmax of tile j runs on the VALU, the QK product of
-// tile j+1 is already on the matrix cores, followed by PV of tile j; all
-// waves copy their share of K(j+2) and V(j+1) into LDS meanwhile.  The O^T
-// accumulator (4 x 16 fp32 per lane) stays in VGPRs, and each segment's loop
-// is unrolled twice so the two score buffers alternate without copies.
+// P^T straight from the S^T accumulator registers.  Rotated K tiles and V^T
+// images of 64-key tiles are double-buffered separately.  The loop is
+// software pipelined: while the softmax of tile j runs on the VALU, the QK
+// product of tile j+1 is already on the matrix cores, followed by PV of tile
+// j; meanwhile each wave copies its share of V(j+1) into LDS and rotates its
+// 8 keys of K(j+2).  The O^T accumulator (4 x 16 fp32 per lane) stays in
+// VGPRs, and each segment's loop is unrolled twice so the two score buffers
+// alternate without copies.
 //
 // Softmax runs in the log2 domain against a per-row reference m (initially 0)
 // that the QK product subtracts itself: its first k-step accumulates onto -m.
@@ -59,12 +59,9 @@ constexpr int kPfThreads = 64 * kPfWaves;
 constexpr int kPfRows = 32 * kPfWaves;  // query rows per workgroup: 32 per wave
 constexpr int kPfBK = 64;               // keys per tile
 constexpr int kTileBytes = kPfBK * kHeadDim * 2;  // one K tile or one V^T image: 16 KB
-constexpr int kTabBytes = kPfBK * kHalf * 4;  // a tile's cos/sin rows in fp16: 16 KB
-// LDS: raw K tiles (two buffers), rotated K tiles (two), V^T images (two) and
-// the cos/sin rows of the staged raw tiles (two)
-constexpr int kRawOff = 0, kRotOff = 2 * kTileBytes, kVtOff = 4 * kTileBytes;
-constexpr int kTabOff = 6 * kTileBytes;
-constexpr int kSmemBytes = kTabOff + 2 * kTabBytes;  // 128 KB
+// LDS: rotated K tiles (two buffers) and V^T images (two)
+constexpr int kRotOff = 0, kVtOff = 2 * kTileBytes;
+constexpr int kSmemBytes = 4 * kTileBytes;  // 64 KB
 constexpr int kPfCopyBytes = kTileBytes / kPfWaves;  // each wave's share of a tile copy: 8 keys
 constexpr int kKeysPerWave = kPfBK / kPfWaves;
 #ifndef JL_SCHED_QK
@@ -391,17 +388,16 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const int kt_l = FROM_ZERO ? 0 : vr.kt_l;
   const int n_steps = n_r + (n_kt - kt_l);
 
-  // ---- staging.  For list entry j each wave copies 8 keys (2 KB) of the raw
-  // K tile, its share of the tile's cos/sin rows and its share of the V^T
-  // image into buffer jb & 1 of each kind; it rotates the same 8 keys of a
-  // staged raw tile into the rotated buffer of that parity.
+  // ---- staging.  For list entry j each wave copies its eighth (2 KB) of the
+  // V^T image into buffer jb & 1, and rotates 8 keys of the raw K tile, read
+  // from memory, into the rotated buffer of that parity.
   const uint32_t smem_base = lds_addr(smem);
   const uint32_t lane_off = 16 * lane;
   auto tile_of = [&](int j) __attribute__((always_inline)) { return j < n_r ? j : kt_l + (j - n_r); };
   // j's view: remote (R(f(k)), Eq. (3), or the frequency map's table at k) or base (R(k))
   auto is_remote = [&](int j) __attribute__((always_inline)) { return REMOTE2 || (FUSED && j < n_r); };
-  // Scalar description of list entry j, formed once when its copies are
-  // issued and kept for its rotation a visit later.  The cos/sin rows of a
+  // Scalar description of list entry j, formed a visit before its
+  // rotation.  The cos/sin rows of a
   // tile are contiguous: p(k0) .. p(min(k0 + 63, Lk - 1)) with p = f for the
   // aliasing remote view (at most 32 rows, as G >= 2 there) and the identity
   // otherwise (64 rows); key k0 + r reads row f(k0 + r) - f(k0) =
@@ -431,41 +427,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     e.tlim = e.alias ? (int)fl : nlast;
     return e;
   };
-  const uint32_t krow_bytes = (uint32_t)a.Hkv * (kHeadDim * 2);  // from one key of k to the next
-  const size_t kseq_off = (kv_row0 * a.Hkv + kvh) * kHeadDim;    // the sequence's key 0 in k
-  // raw K copy: lane -> (key, chunk) of each 1 KB copy, in the K tile swizzle
-  const int cp_row = kKeysPerWave * wave + (lane >> 4);  // rows cp_row and cp_row + 4
-  const uint32_t cp_chunk0 = 16 * ((lane & 15) ^ kswz(cp_row));
-  const uint32_t cp_chunk1 = 16 * ((lane & 15) ^ kswz(cp_row + 4));
-  // cos/sin rows: copy h (0, 1) moves rows 32 h + 4 wave .. + 3 of the slice
-  const int tb_row = 4 * wave + (lane >> 4);
-  // copy entry e into buffers jb & 1 (jb = j except for the clamped copies)
-  auto issue_k = [&](const Ent& e, int jb) __attribute__((always_inline)) {
-    const unsigned char* gk =
-        (const unsigned char*)(a.k + kseq_off) + (size_t)e.k0 * krow_bytes;
-    if constexpr (PAGED) {  // the tile's page (clamped already; a page holds whole tiles)
-      const int page = __builtin_amdgcn_readfirstlane(s_pages[e.k0 >> a.page_shift]);
-      const size_t prow = ((size_t)page << a.page_shift) + (e.k0 & ((1 << a.page_shift) - 1));
-      const uint64_t p = (uint64_t)(a.k + (prow * a.Hkv + kvh) * kHeadDim);
-      // the copy takes its base in SGPRs: keep the (uniform) address there.
-      // readfirstlane returns int: widen each half as unsigned (no sign fill)
-      const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
-      const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p);
-      gk = (const unsigned char*)(((uint64_t)hi << 32) | lo);
-    }
-    const uint32_t v0 = __umul24((uint32_t)min(cp_row, e.klim), krow_bytes) + cp_chunk0;
-    const uint32_t v1 = __umul24((uint32_t)min(cp_row + 4, e.klim), krow_bytes) + cp_chunk1;
-    const uint32_t l = smem_base + kRawOff + (jb & 1) * kTileBytes + wave * kPfCopyBytes;
-    dma16_s<0>(gk, v0, l);
-    dma16_s<0>(gk, v1, l + 1024);
-    const unsigned char* gt =
-        (const unsigned char*)((e.remote ? a.rtable16 : a.table16) + (size_t)e.row0 * kHalf);
-    const uint32_t lt = smem_base + kTabOff + (jb & 1) * kTabBytes + wave * 1024;
-    if (4 * wave <= e.tlim)  // rows past the last one are never read
-      dma16_s<0>(gt, (uint32_t)min(tb_row, e.tlim) * 256 + lane_off % 256, lt);
-    if (!e.alias)  // rows 32 .. 63 (the aliasing view needs at most 32)
-      dma16_s<0>(gt, (uint32_t)min(tb_row + 32, e.tlim) * 256 + lane_off % 256, lt + 8192);
-  };
+  const size_t kseq_off = (kv_row0 * a.Hkv + kvh) * kHeadDim;  // the sequence's key 0 in k
   auto issue_v = [&](int j, int jb) __attribute__((always_inline)) {
     const size_t off = img_base + (size_t)tile_of(j) * (kTileBytes / 2) + wave * (kPfCopyBytes / 2);
     const unsigned char* gv = (const unsigned char*)(a.vt + off);
@@ -473,11 +435,12 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     dma16_s<0>(gv, lane_off, l);
     dma16_s<1024>(gv, lane_off, l);
   };
-  // Rotation of the staged raw tile of an entry (buffers jb & 1) to its view
-  // (Sec. 3.2): lane -> key rt_row of the tile, rotate-half pairs of chunks
-  // (rt_c, rt_c + 8), i.e. frequencies i = 8 rt_c .. 8 rt_c + 7, with the
-  // (cos, sin) of the key's position from the staged rows.  Each output is
-  // one v_dot2_f32_bf16 of the pair (x_i, x_{i+64}) with (cos, -sin) or of
+  // Rotation of an entry's raw K tile to its view (Sec. 3.2): lane -> key
+  // rt_row of the tile, rotate-half pairs of chunks (rt_c, rt_c + 8), i.e.
+  // frequencies i = 8 rt_c .. 8 rt_c + 7, with the (cos, sin) of the key's
+  // position.  The raw chunks and the cos/sin row go from memory straight
+  // into registers (rows past the sequence repeat its last key).  Each output
+  // is one v_dot2_f32_bf16 of the pair (x_i, x_{i+64}) with (cos, -sin) or of
   // (x_{i+64}, x_i) with (cos, sin): exact products, an fp32 sum, then one
   // rounding to bf16.  The result exists only in LDS.
   const int rt_row = kKeysPerWave * wave + (lane >> 3);
@@ -487,17 +450,26 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     u32x4 xl, xh;  // raw chunks rt_c and rt_c + 8 of key rt_row
     u32x4 ca, cb;  // bf16 (cos, sin) of frequencies 8 rt_c .. +3 and +4 .. +7
   };
-  auto rot_load = [&](const Ent& e, int jb) __attribute__((always_inline)) {
+  auto rot_load = [&](const Ent& e) __attribute__((always_inline)) {
     int fr = (int)fastdiv_ge2((uint32_t)(e.kmod + rt_row), gdiv);
     asm volatile("" : "+v"(fr));  // formed unconditionally: a select, not a branch
-    const int row = e.alias ? fr : rt_row;
-    const unsigned char* tb = smem + kTabOff + (jb & 1) * kTabBytes + row * 256 + 32 * rt_c;
-    const unsigned char* src = (const unsigned char*)smem + kRawOff + (jb & 1) * kTileBytes;
+    const int row = min(e.alias ? fr : rt_row, e.tlim);
+    const int key = min(rt_row, e.klim);
+    const uint16_t* kr;
+    if constexpr (PAGED) {  // the tile's page (clamped already; a page holds whole tiles)
+      const int page = __builtin_amdgcn_readfirstlane(s_pages[e.k0 >> a.page_shift]);
+      const size_t prow = ((size_t)page << a.page_shift) + (e.k0 & ((1 << a.page_shift) - 1));
+      kr = a.k + ((prow + key) * a.Hkv + kvh) * kHeadDim;
+    } else {
+      kr = a.k + kseq_off + (size_t)(e.k0 + key) * ((size_t)a.Hkv * kHeadDim);
+    }
+    const uint32_t* tr =
+        (e.remote ? a.rtable16 : a.table16) + (size_t)(e.row0 + row) * kHalf + 8 * rt_c;
     RotIn r;
-    r.xl = *(const u32x4*)(src + rt_lo);
-    r.xh = *(const u32x4*)(src + rt_hi);
-    r.ca = *(const u32x4*)tb;
-    r.cb = *(const u32x4*)(tb + 16);
+    r.xl = load16(kr + 8 * rt_c);
+    r.xh = load16(kr + 64 + 8 * rt_c);
+    r.ca = load16(tr);
+    r.cb = load16(tr + 4);
     return r;
   };
   // word w (0..3) of the rotated chunks: frequencies 8 rt_c + 2w and + 1
@@ -514,8 +486,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     *(u32x4*)(dst + rt_lo) = lo;
     *(u32x4*)(dst + rt_hi) = hi;
   };
-  auto rotate = [&](const Ent& e, int jb) __attribute__((always_inline)) {
-    const RotIn r = rot_load(e, jb);
+  auto rotate = [&](const RotIn& r, int jb) __attribute__((always_inline)) {
     u32x4 lo, hi;
 #pragma unroll
     for (int w = 0; w < 4; ++w) rot_word(r, w, lo, hi);
@@ -683,10 +654,15 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // it describes entry j+3.
   auto visit = [&](int j, f32x16* cur, f32x16* nxt, int lo, int hi, Ent& pend) __attribute__((always_inline)) {
     if (SAFE ? need_mask(j) : (j < lo || j > hi)) mask(j, cur);
-    wait_vmem();      // this wave's copies of raw K(j+2), its rows, V(j)
+    wait_vmem();      // this wave's copy of V(j)
     __syncthreads();  // everyone's; QK(j), PV(j-1) and the rotation of j+1 are done everywhere
     bf16x8 pb[4];
+    // V(j+1) into the buffer PV(j-1) released
+    issue_v(min(j + 1, n_steps - 1), j + 1);
     if constexpr (!SAFE) {
+      // raw K(j+2) and its cos/sin row into registers: they land while
+      // QK(j+1) and the softmax of j run
+      const RotIn rin = rot_load(pend);
       // The two waves of a SIMD pass the per-tile barrier together, so a
       // block of VALU work in one wave finds the other at the same point and
       // the matrix core idles unless each wave feeds it between its own VALU
@@ -730,13 +706,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       const float ps = ps0 + ps1;
       late_bad |= __ballot(ps > p_hi);
       l_run += ps;
-      const RotIn rin = rot_load(pend, j + 2);
-      // raw K(j+3) with its rows and V(j+1) go into the buffers that the
-      // rotation of j+1 and PV(j-1) released; past the list's end the last
-      // entry is copied again (into the free buffer).
+      // past the list's end the last entry is rotated (and V copied) again
       const Ent e3 = ent_of(min(j + 3, n_steps - 1));
-      issue_k(e3, j + 3);
-      issue_v(min(j + 1, n_steps - 1), j + 1);
       const unsigned char* vb = vbuf(j);
       auto vop = [&](int m) __attribute__((always_inline)) {
         const int d = 32 * (m & 3) + kr_lane;
@@ -760,13 +731,12 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       __builtin_amdgcn_iglp_opt(0);
       qk(kbuf(j + 1), nxt);
       const Ent e3 = ent_of(min(j + 3, n_steps - 1));
-      issue_k(e3, j + 3);
-      issue_v(min(j + 1, n_steps - 1), j + 1);
       float ps = softmax(cur, pb);
       ref_fix(cur, nxt, pb, ps);
       l_run += ps;
+      const RotIn rin = rot_load(pend);  // loaded late: short-lived registers
       pv(vbuf(j), pb);
-      rotate(pend, j + 2);
+      rotate(rin, j + 2);
       pend = e3;
     }
   };
@@ -779,8 +749,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     if (j < jend) visit(j, sc_a, sc_b, lo, hi, pend);
   };
 
-  // ---- prologue: the first view's query operand; raw K(0), K(1) staged and
-  // rotated, V(0) and raw K(2) in flight
+  // ---- prologue: the first view's query operand; K(0), K(1) rotated into
+  // their buffers, V(0) in flight
   const bool q_remote = n_r > 0 || REMOTE2;
   load_q_operand(qrow, hl32, q_remote ? a.rtable : a.table,
                  q_remote && !a.freq_map ? remote_pos(qp, gdiv) : qp, a.q_scale, qop);
@@ -797,17 +767,13 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   Ent pend = ent_of(0);
   {
     const Ent e1 = ent_of(min(1, last));
-    issue_k(pend, 0);
-    issue_k(e1, 1);
     issue_v(0, 0);
-    wait_vmem();
-    __syncthreads();
-    rotate(pend, 0);
-    rotate(e1, 1);
+    const RotIn r0 = rot_load(pend), r1 = rot_load(e1);
+    rotate(r0, 0);
+    rotate(r1, 1);
   }
   __syncthreads();  // the rows of buffer 0 are read by every wave
   pend = ent_of(min(2, last));
-  issue_k(pend, 2);  // into buffers 0
   qk(kbuf(0), sc_a);
 
   if (FUSED && n_r > 0) {
