@@ -258,6 +258,9 @@ def main() -> int:
                          "configurations (64K, 1.7B-like 128K, within-window, B=8 decode; 0 skips)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--zero-inputs", action="store_true",
+                    help="diagnostic: time the main workloads on all-zero Q, K, V (the matrix "
+                         "cores then draw far less power); not a benchmark result")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB three times (the "
                          "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -298,6 +301,9 @@ def main() -> int:
     # a second cache with the same contents, alternated so consecutive decode
     # calls cannot be served from the 256 MB Infinity Cache
     caches.append((caches[0][0].clone(), caches[0][1].clone()))
+    if args.zero_inputs:
+        for t in (q, k, v, dqd) + caches[0] + caches[1]:
+            t.zero_()
     lens_d = torch.from_numpy(dlens).cuda()
     dout = torch.empty_like(dqd)
     ws = torch.empty(api.decode_workspace_bytes(wd.B, wd.Hq, wd.Hkv, wd.L), dtype=torch.uint8,
@@ -415,6 +421,7 @@ def main() -> int:
         dv_.append(timed(lambda: decode_batch(False)) / args.decode_batch)
         db_.append(timed(lambda: decode_batch(True)) / args.decode_batch)
         decode_batch(True, sev[r])  # the split kernel timed alone, outside the call timings
+    torch.cuda.synchronize()
     med = lambda x: sorted(x)[len(x) // 2] if x else float("nan")
     dec_med = med(db_)
     dec_gbps = (kv_bytes + io_bytes) / (dec_med * 1e-3) / 1e9
@@ -581,7 +588,7 @@ def main() -> int:
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic",
+        "data": "zeros (diagnostic)" if args.zero_inputs else "synthetic",
         "config": config_block(wp, wd, dlens, api.group_size(wp.L, wp.w_pretrained)),
         "prefill_ms": round(pre_avg, 3),
         "prefill_mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
