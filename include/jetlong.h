@@ -376,6 +376,22 @@ int jl_bifocal_decode_paged(const void* q, const void* k_pages, const void* v_pa
                             int head_dim, double rope_theta, int w_pretrained, int w_local,
                             void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * jl_bifocal_decode_paged with a choice of remote map, as jl_bifocal_decode_map
+ * offers it for dense caches: remote_map JL_REMOTE_ALIAS is
+ * jl_bifocal_decode_paged bit for bit, JL_REMOTE_FREQ the Sec. 4.5 frequency
+ * map with each sequence's factor from its own kv_len.  The workspace must
+ * hold jl_decode_map_workspace_bytes(B, Hq, Hkv, max_pages * page_size,
+ * head_dim, remote_map) bytes.  Other arguments and errors as in
+ * jl_bifocal_decode_paged; remote_map outside {0, 1} -> JL_ERR_INVALID_ARG.
+ */
+int jl_bifocal_decode_paged_map(const void* q, const void* k_pages, const void* v_pages,
+                                const int32_t* block_table, int max_pages, int page_size,
+                                int n_pages, const int32_t* kv_lens, void* o, int B, int Hq,
+                                int Hkv, int head_dim, double rope_theta, int w_pretrained,
+                                int w_local, int remote_map, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
 /* The vanilla counterpart of jl_bifocal_decode_paged. */
 int jl_rope_attention_decode_paged(const void* q, const void* k_pages, const void* v_pages,
                                    const int32_t* block_table, int max_pages, int page_size,

@@ -96,6 +96,9 @@ def lib() -> ctypes.CDLL:
         L.jl_bifocal_decode_paged.restype = i32
         L.jl_bifocal_decode_paged.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, i32, i32, i32,
                                               i32, dbl, i32, i32, vp, sz, vp]
+        L.jl_bifocal_decode_paged_map.restype = i32
+        L.jl_bifocal_decode_paged_map.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, i32,
+                                                  i32, i32, i32, dbl, i32, i32, i32, vp, sz, vp]
         L.jl_rope_attention_decode_paged.restype = i32
         L.jl_rope_attention_decode_paged.argtypes = [vp, vp, vp, vp, i32, i32, i32, vp, vp, i32,
                                                      i32, i32, i32, dbl, vp, sz, vp]
@@ -425,10 +428,11 @@ def rope_attention_decode(q, k_cache, v_cache, kv_lens, *, rope_theta: float = 1
 
 def decode_paged(q, k_pages, v_pages, block_table, kv_lens, *, w_pretrained: int = 1,
                  w_local: int = 0, rope_theta: float = 1e6, bifocal: bool = True, out=None,
-                 workspace=None, stream=None):
+                 workspace=None, stream=None, remote_map: str = "alias"):
     """jl_bifocal_decode_paged / jl_rope_attention_decode_paged: q [B, Hq, 128] raw,
     pools [n_pages, page_size, Hkv, 128] raw, block_table int32 [B, max_pages],
-    kv_lens int32 [B]."""
+    kv_lens int32 [B].  remote_map "freq" calls jl_bifocal_decode_paged_map with
+    JL_REMOTE_FREQ (Sec. 4.5)."""
     import torch
     B, Hq, D = q.shape
     n_pages, page_size, Hkv, _ = k_pages.shape
@@ -439,9 +443,14 @@ def decode_paged(q, k_pages, v_pages, block_table, kv_lens, *, w_pretrained: int
     if kv_lens.shape != (B,):
         raise ValueError("kv_lens must be [B]")
     max_pages = block_table.shape[1]
+    if remote_map not in REMOTE_MAPS:
+        raise ValueError("remote_map must be one of %s" % sorted(REMOTE_MAPS))
     if out is None:
         out = torch.empty_like(q)
-    need = decode_workspace_bytes(B, Hq, Hkv, max_pages * page_size, D)
+    if remote_map != "alias" and bifocal:
+        need = decode_map_workspace_bytes(B, Hq, Hkv, max_pages * page_size, D, remote_map)
+    else:
+        need = decode_workspace_bytes(B, Hq, Hkv, max_pages * page_size, D)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
     args = [_dev(q, "q", torch.bfloat16), _dev(k_pages, "k_pages", torch.bfloat16),
@@ -449,7 +458,10 @@ def decode_paged(q, k_pages, v_pages, block_table, kv_lens, *, w_pretrained: int
             max_pages, page_size, n_pages, _dev(kv_lens, "kv_lens", torch.int32),
             _dev(out, "out", torch.bfloat16), B, Hq, Hkv, D, float(rope_theta)]
     ws = [_dev(workspace, "workspace"), workspace.numel() * workspace.element_size()]
-    if bifocal:
+    if bifocal and remote_map != "alias":
+        _check(lib().jl_bifocal_decode_paged_map(*args, int(w_pretrained), int(w_local),
+                                                 REMOTE_MAPS[remote_map], *ws, _stream(stream)))
+    elif bifocal:
         _check(lib().jl_bifocal_decode_paged(*args, int(w_pretrained), int(w_local), *ws,
                                              _stream(stream)))
     else:

@@ -761,6 +761,18 @@ int jl_bifocal_decode_paged(const void* q, const void* k_pages, const void* v_pa
                        block_table, max_pages, page_size, n_pages);
 }
 
+int jl_bifocal_decode_paged_map(const void* q, const void* k_pages, const void* v_pages,
+                                const int32_t* block_table, int max_pages, int page_size,
+                                int n_pages, const int32_t* kv_lens, void* o, int B, int Hq,
+                                int Hkv, int head_dim, double rope_theta, int w_pretrained,
+                                int w_local, int remote_map, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  if (block_table == nullptr) return fail(JL_ERR_INVALID_ARG, "block_table must be non-null");
+  return decode_common(true, q, k_pages, v_pages, kv_lens, 0, o, B, Hq, Hkv, head_dim,
+                       rope_theta, w_pretrained, w_local, workspace, workspace_bytes, stream,
+                       block_table, max_pages, page_size, n_pages, remote_map);
+}
+
 int jl_rope_attention_decode_paged(const void* q, const void* k_pages, const void* v_pages,
                                    const int32_t* block_table, int max_pages, int page_size,
                                    int n_pages, const int32_t* kv_lens, void* o, int B, int Hq,

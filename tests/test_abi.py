@@ -241,6 +241,17 @@ def test_decode_length_limit_is_exact():
     assert rc == api.JL_ERR_UNSUPPORTED
 
 
+@pytest.mark.parametrize("remote_map", [-1, 2])
+def test_paged_decode_map_rejects_unknown_remote_map(remote_map):
+    L = api.lib()
+    rc = L.jl_bifocal_decode_paged_map(A, A, A, A2, 4, 64, 10, A2, A, 1, 8, 2, 128, 1e6, 64, 8,
+                                       remote_map, A, 1 << 30, None)
+    assert rc == api.JL_ERR_INVALID_ARG
+    assert "remote_map" in L.jl_last_error().decode()
+    assert L.jl_bifocal_decode_paged_map(A, A, A, None, 4, 64, 10, A2, A, 1, 8, 2, 128, 1e6, 64,
+                                         8, 1, A, 1 << 30, None) == api.JL_ERR_INVALID_ARG
+
+
 def test_noalloc_decode_bounds_are_checked_on_the_host():
     # the fixed array holds the table of 131072 positions and 24 MiB of split
     # states; larger calls are refused before any device work

@@ -98,3 +98,34 @@ def test_paged_table_entries_out_of_range_are_clamped():
     vc = np.stack([np.concatenate([vp[p] for p in clamped[b]]) for b in range(B)])
     want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=16, w_local=4)
     assert_close(to_f64(out), want, what="clamped pages")
+
+
+@pytest.mark.parametrize("page_size", [16, 128])
+def test_paged_freq_map_decode(page_size):
+    """jl_bifocal_decode_paged_map: the frequency map (Sec. 4.5) on shuffled
+    pages equals the dense frequency-map decode bit for bit and matches the
+    oracle, across factors s = L / w_pretrained; the alias choice is the plain
+    paged decode."""
+    Hq, Hkv, w_pre, w0 = 8, 2, 96, 20
+    max_len = 4 * w_pre + 40
+    lens = [1, w0 + 1, w_pre, w_pre + 1, 2 * w_pre + 1, 3 * w_pre + 7, max_len]
+    B = len(lens)
+    q, kc, vc, lens = synth.decode_inputs(B, Hq, Hkv, max_len, lens, seed=page_size + 7,
+                                          nan_tail=True)
+    kp, vp, table = _paginate(kc, vc, lens, page_size, seed=page_size + 1)
+    ld = torch.from_numpy(np.asarray(lens, dtype=np.int32)).cuda()
+    say("paged freq-map decode page_size=%d" % page_size)
+    paged = api.decode_paged(to_dev(q), to_dev(kp), to_dev(vp), torch.from_numpy(table).cuda(),
+                             ld, w_pretrained=w_pre, w_local=w0, remote_map="freq")
+    dense = api.bifocal_decode(to_dev(q), to_dev(kc), to_dev(vc), ld, w_pretrained=w_pre,
+                               w_local=w0, remote_map="freq")
+    alias_map = api.decode_paged(to_dev(q), to_dev(kp), to_dev(vp),
+                                 torch.from_numpy(table).cuda(), ld, w_pretrained=w_pre,
+                                 w_local=w0, remote_map="alias")
+    alias = _paged(True, q, kp, vp, table, lens, w_pre, w0)
+    torch.cuda.synchronize()
+    assert torch.equal(paged.view(torch.int16), dense.view(torch.int16))
+    assert torch.equal(alias_map.view(torch.int16), alias.view(torch.int16))
+    want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=w0,
+                          bifocal=True, remote_map="freq")
+    assert_close(to_f64(paged), want, what="paged freq map %d" % page_size)
