@@ -219,6 +219,22 @@ int jl_bifocal_prefill_varlen(const void* q, const void* k, const void* v, void*
                               int Hq, int Hkv, int head_dim, double rope_theta, int w_pretrained,
                               int w_local, void* stream);
 
+/*
+ * jl_bifocal_prefill_varlen with a choice of remote map (Sec. 4.5, Tab. 6),
+ * as jl_bifocal_prefill_map offers it for one sequence.  JL_REMOTE_ALIAS is
+ * jl_bifocal_prefill_varlen bit for bit; JL_REMOTE_FREQ gives every sequence
+ * the frequency map of its own length: factor s = max(1, L / w_pretrained),
+ * positions unchanged, each sequence equal bit for bit to jl_bifocal_prefill_map
+ * on that sequence alone.  The per-sequence tables (768 bytes per token) are
+ * built on the device into the library scratch.  Other arguments and errors
+ * as in jl_bifocal_prefill_varlen; remote_map outside {0, 1} ->
+ * JL_ERR_INVALID_ARG.
+ */
+int jl_bifocal_prefill_varlen_map(const void* q, const void* k, const void* v, void* o,
+                                  float* lse, const int32_t* cu_seqlens, int B, int total_tokens,
+                                  int max_seqlen, int Hq, int Hkv, int head_dim, double rope_theta,
+                                  int w_pretrained, int w_local, int remote_map, void* stream);
+
 /* The vanilla counterpart of jl_bifocal_prefill_varlen (base rotation only). */
 int jl_rope_attention_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
                              const int32_t* cu_seqlens, int B, int total_tokens, int max_seqlen,

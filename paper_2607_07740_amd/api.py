@@ -67,6 +67,9 @@ def lib() -> ctypes.CDLL:
         L.jl_bifocal_prefill_varlen.restype = i32
         L.jl_bifocal_prefill_varlen.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
                                                 i32, dbl, i32, i32, vp]
+        L.jl_bifocal_prefill_varlen_map.restype = i32
+        L.jl_bifocal_prefill_varlen_map.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32,
+                                                    i32, i32, dbl, i32, i32, i32, vp]
         L.jl_rope_attention_varlen.restype = i32
         L.jl_rope_attention_varlen.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
                                                i32, dbl, vp]
@@ -259,9 +262,12 @@ def prefill_chunk_paged(q, k_pages, v_pages, block_table, *, q_start: int,
 
 def prefill_varlen(q, k, v, cu_seqlens, *, max_seqlen: int, w_pretrained: int = 1,
                    w_local: int = 0, rope_theta: float = 1e6, bifocal: bool = True, out=None,
-                   lse=None, want_lse: bool = False, stream=None):
+                   lse=None, want_lse: bool = False, stream=None, remote_map: str = "alias"):
     """jl_bifocal_prefill_varlen / jl_rope_attention_varlen: packed sequences, q [T, Hq, 128],
-    k, v [T, Hkv, 128], cu_seqlens int32 [B + 1] on the device; lse is [Hq, T]."""
+    k, v [T, Hkv, 128], cu_seqlens int32 [B + 1] on the device; lse is [Hq, T].
+    remote_map "freq" calls jl_bifocal_prefill_varlen_map with JL_REMOTE_FREQ (Sec. 4.5)."""
+    if remote_map not in REMOTE_MAPS:
+        raise ValueError("remote_map must be one of %s" % sorted(REMOTE_MAPS))
     import torch
     T, Hq, D = q.shape
     Hkv = k.shape[1]
@@ -280,7 +286,10 @@ def prefill_varlen(q, k, v, cu_seqlens, *, max_seqlen: int, w_pretrained: int = 
             _dev(lse, "lse", torch.float32) if lse is not None else None,
             _dev(cu_seqlens, "cu_seqlens", torch.int32), B, T, int(max_seqlen), Hq, Hkv, D,
             float(rope_theta)]
-    if bifocal:
+    if bifocal and remote_map != "alias":
+        _check(lib().jl_bifocal_prefill_varlen_map(*args, int(w_pretrained), int(w_local),
+                                                   REMOTE_MAPS[remote_map], _stream(stream)))
+    elif bifocal:
         _check(lib().jl_bifocal_prefill_varlen(*args, int(w_pretrained), int(w_local),
                                                _stream(stream)))
     else:

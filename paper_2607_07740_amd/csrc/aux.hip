@@ -45,6 +45,57 @@ hipError_t launch_build_table(float2* table, uint32_t* table16, int n_pos, const
   return hipGetLastError();
 }
 
+// The frequency map's tables for a packed batch (Sec. 4.5): row seq0 + p of
+// sequence (seq0, L) holds (cos, sin)(p omega'_i), omega'_i = (1 - gamma_i)
+// omega_i / s + gamma_i omega_i, s = max(1, L / w_pretrained), in fp32 and as
+// bf16 pairs, like the base tables.  omega'_i is formed in fp64 with the
+// operations, in the order, that the host uses for a single sequence, so each
+// sequence's rows equal the table of a call on that sequence alone.  One
+// workgroup per key-tile entry of the packed batch's plan.
+struct PackedFreqArgs {
+  const int4* twork;  // per key tile: (seq0, L, tile, tile0); L <= 0 marks an unused entry
+  float2* table;
+  uint32_t* table16;
+  int w_pre;
+  double omega[kHalf];
+  double gamma[kHalf];
+};
+
+__global__ __launch_bounds__(256) void packed_freq_table_kernel(PackedFreqArgs a) {
+#pragma clang fp contract(off)
+  const int4 w = a.twork[blockIdx.x];
+  if (w.y <= 0) return;
+  const double s = fmax(1.0, (double)w.y / (double)a.w_pre);
+  for (int idx = threadIdx.x; idx < 64 * kHalf; idx += 256) {
+    const int p = w.z * 64 + (idx >> 6);
+    if (p >= w.y) continue;
+    const int i = idx & (kHalf - 1);
+    const double om = (1.0 - a.gamma[i]) * a.omega[i] / s + a.gamma[i] * a.omega[i];
+    double sn, cs;
+    sincos((double)p * om, &sn, &cs);
+    const size_t r = ((size_t)w.x + p) * kHalf + i;
+    a.table[r] = make_float2((float)cs, (float)sn);
+    a.table16[r] = bf16_bits_rne(cs) | (bf16_bits_rne(sn) << 16);
+  }
+}
+
+// og: omega_i (64) then gamma_i (64), as the host computes them
+hipError_t launch_packed_freq_table(const int4* twork, int nt, int w_pre, const double* og,
+                                    float2* table, uint32_t* table16, hipStream_t stream) {
+  PackedFreqArgs a;
+  a.twork = twork;
+  a.table = table;
+  a.table16 = table16;
+  a.w_pre = w_pre;
+  for (int i = 0; i < kHalf; ++i) {
+    a.omega[i] = og[i];
+    a.gamma[i] = og[kHalf + i];
+  }
+  if (nt <= 0) return hipSuccess;
+  hipLaunchKernelGGL(packed_freq_table_kernel, dim3((unsigned)nt), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
 __global__ void debug_schedule_kernel(const int32_t* lengths, int nl, const int32_t* positions,
                                       int np, int w, int32_t* gout, int32_t* fout,
                                       int32_t* dout) {

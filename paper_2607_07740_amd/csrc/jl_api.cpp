@@ -27,13 +27,13 @@ hipError_t launch_prefill_chunk(bool bifocal, const uint16_t* q, const uint16_t*
                                 float slack, void* ws, hipStream_t stream, hipEvent_t ev0,
                                 hipEvent_t ev1, const int32_t* block_table, int max_pages,
                                 int page_shift, int n_pages);
-size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hkv);
+size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hkv, bool freq);
 hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t* k,
                                  const uint16_t* v, uint16_t* o, float* lse, const float2* table,
                                  const uint32_t* table16, const int32_t* cu, int B, int T,
                                  int max_len, int Hq, int Hkv,
                                  int w_pre, int w0, float slack, void* ws, hipStream_t stream,
-                                 hipEvent_t ev0, hipEvent_t ev1);
+                                 hipEvent_t ev0, hipEvent_t ev1, const double* freq_og);
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L);
 hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                   uint16_t* o, float* lse, const float2* table,
@@ -210,7 +210,7 @@ void freq_map_omegas(double theta, int L, int w_pre, double* out) {
 }
 
 // One frequency-map table per device, for the last (theta, L, w_pretrained)
-// used: [L][64] (cos, sin) of p * omega'_i (fp32, then fp16 as in the base
+// used: [L][64] (cos, sin) of p * omega'_i (fp32, then bf16 pairs as in the base
 // table), held in a buffer of cap >= L positions.  A new configuration that
 // fits is rebuilt in place; one that does not replaces the buffer with one of
 // at least twice the capacity.  Either way the device is synchronised first,
@@ -423,9 +423,14 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
 // rows of the T-row tensors; every sequence is prefilled with its own length.
 int prefill_varlen(bool bifocal, const void* q, const void* k, const void* v, void* o, float* lse,
                    const int32_t* cu, int B, int T, int max_seqlen, int Hq, int Hkv,
-                   int head_dim, double theta, int w_pre, int w0, void* stream) {
+                   int head_dim, double theta, int w_pre, int w0, void* stream,
+                   int remote_map = JL_REMOTE_ALIAS) {
   int st = check_common(B, Hq, Hkv, head_dim, theta);
   if (st != JL_OK) return st;
+  if (remote_map != JL_REMOTE_ALIAS && remote_map != JL_REMOTE_FREQ)
+    return fail(JL_ERR_INVALID_ARG, "remote_map must be JL_REMOTE_ALIAS or JL_REMOTE_FREQ (got %d)",
+                remote_map);
+  const bool freq = bifocal && remote_map == JL_REMOTE_FREQ;
   if (T < 1) return fail(JL_ERR_INVALID_ARG, "total_tokens must be >= 1 (got %d)", T);
   if (max_seqlen < 1)
     return fail(JL_ERR_INVALID_ARG, "max_seqlen must be >= 1 (got %d)", max_seqlen);
@@ -451,15 +456,17 @@ int prefill_varlen(bool bifocal, const void* q, const void* k, const void* v, vo
   const float slack = (float)g_rescale_log2.load();
   std::lock_guard<std::mutex> launch_lock(g_prefill_mu);
   void* scratch = nullptr;
-  st = get_scratch(s, jl::prefill_varlen_workspace_bytes(bifocal, B, T, Hq, Hkv), &scratch);
+  st = get_scratch(s, jl::prefill_varlen_workspace_bytes(bifocal, B, T, Hq, Hkv, freq), &scratch);
   if (st != JL_OK) return st;
+  double og[128];
+  if (freq) freq_map_ramp(theta, w_pre, og);
   hipEvent_t ev0, ev1;
   timing_events(0, &ev0, &ev1);
   hipError_t e = jl::launch_prefill_varlen(bifocal, (const uint16_t*)q, (const uint16_t*)k,
                                            (const uint16_t*)v, (uint16_t*)o, lse, tab.f32, tab.f16,
                                            cu, B, T,
                                            max_len, Hq, Hkv, w_pre, w0, slack, scratch, s, ev0,
-                                           ev1);
+                                           ev1, freq ? og : nullptr);
   if (e != hipSuccess) return hip_fail(e, "varlen prefill launch");
   return ok();
 }
@@ -682,6 +689,14 @@ int jl_bifocal_prefill_varlen(const void* q, const void* k, const void* v, void*
                               int w_local, void* stream) {
   return prefill_varlen(true, q, k, v, o, lse, cu_seqlens, B, total_tokens, max_seqlen, Hq, Hkv,
                         head_dim, rope_theta, w_pretrained, w_local, stream);
+}
+
+int jl_bifocal_prefill_varlen_map(const void* q, const void* k, const void* v, void* o,
+                                  float* lse, const int32_t* cu_seqlens, int B, int total_tokens,
+                                  int max_seqlen, int Hq, int Hkv, int head_dim, double rope_theta,
+                                  int w_pretrained, int w_local, int remote_map, void* stream) {
+  return prefill_varlen(true, q, k, v, o, lse, cu_seqlens, B, total_tokens, max_seqlen, Hq, Hkv,
+                        head_dim, rope_theta, w_pretrained, w_local, stream, remote_map);
 }
 
 int jl_rope_attention_varlen(const void* q, const void* k, const void* v, void* o, float* lse,

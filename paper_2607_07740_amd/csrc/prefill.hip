@@ -192,6 +192,8 @@ struct PrefillArgs {
   const uint32_t* table16;   // the same tables as bf16 pairs (cos low, sin high): key rotation
   const uint32_t* rtable16;
   int freq_map;          // 0: Eq. (3) aliasing, 1: Sec. 4.5 frequency interpolation
+  int rtab_packed;       // packed batch with the frequency map: the remote tables hold
+                         // each sequence's own rows, from the sequence's first row on
   const uint16_t* k;     // raw (pre-RoPE) keys, [B][kv_stride][Hkv][128] or packed [T][Hkv][128]
   const uint16_t* vt;    // V^T tile images from vt_prep_kernel
   int kv_stride;         // rows per sequence in k (dense batches)
@@ -231,6 +233,7 @@ struct Work {
   int b, kvh, qblk, q_start, q_end, w0, Lk;  // Lk: keys [0, Lk) of the sequence are valid
   size_t row_base, lse_base, img_base;    // rows of q/o, lse entries, V^T image elements
   size_t kv_row0;                         // the sequence's first row of k
+  size_t rtab_row;                        // the sequence's row 0 in the remote tables
   FastDiv gdiv;
 };
 
@@ -255,6 +258,7 @@ __device__ inline bool work_of(const PrefillArgs& a, int bid, bool fused, Work& 
     W.lse_base = (size_t)w.x;
     W.img_base = ((size_t)W.kvh * a.n_tiles + w.w) * (kTileBytes / 2);
     W.kv_row0 = (size_t)w.x;
+    W.rtab_row = a.rtab_packed ? (size_t)w.x : 0;
     W.Lk = w.y;
   } else {
     int group;
@@ -277,6 +281,7 @@ __device__ inline bool work_of(const PrefillArgs& a, int bid, bool fused, Work& 
     W.lse_base = (size_t)b * a.Hq * a.Lq;
     W.img_base = (size_t)group * a.n_tiles * (kTileBytes / 2);
     W.kv_row0 = (size_t)b * a.kv_stride;
+    W.rtab_row = 0;
     W.Lk = a.L;
   }
   return true;
@@ -367,6 +372,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   const int kvh = W.kvh, qblk = W.qblk, q_start = W.q_start, q_end = W.q_end, w0 = W.w0, Lk = W.Lk;
   const size_t row_base = W.row_base, lse_base = W.lse_base, img_base = W.img_base;
   const size_t kv_row0 = W.kv_row0;
+  const float2* rtable = a.rtable + W.rtab_row * kHalf;
+  const uint32_t* rtable16 = a.rtable16 + W.rtab_row * kHalf;
   const FastDiv gdiv = W.gdiv;
   const int q0 = q_start + qblk * a.BQ;
   const int q1 = min(q0 + a.BQ, q_end) - 1;
@@ -464,7 +471,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       kr = a.k + kseq_off + (size_t)(e.k0 + key) * ((size_t)a.Hkv * kHeadDim);
     }
     const uint32_t* tr =
-        (e.remote ? a.rtable16 : a.table16) + (size_t)(e.row0 + row) * kHalf + 8 * rt_c;
+        (e.remote ? rtable16 : a.table16) + (size_t)(e.row0 + row) * kHalf + 8 * rt_c;
     RotIn r;
     r.xl = load16(kr + 8 * rt_c);
     r.xh = load16(kr + 64 + 8 * rt_c);
@@ -752,7 +759,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   // ---- prologue: the first view's query operand; K(0), K(1) rotated into
   // their buffers, V(0) in flight
   const bool q_remote = n_r > 0 || REMOTE2;
-  load_q_operand(qrow, hl32, q_remote ? a.rtable : a.table,
+  load_q_operand(qrow, hl32, q_remote ? rtable : a.table,
                  q_remote && !a.freq_map ? remote_pos(qp, gdiv) : qp, a.q_scale, qop);
   if (CHECK_LATE && tid == 0) s_bad = 0;  // read after the end-of-block barrier
   const int last = n_steps - 1;
@@ -1156,12 +1163,24 @@ static void varlen_sizes(int B, int T, int g, long long* nq, long long* nt) {
 
 // Scratch of a packed batch: the tile images of nt tiles per kv head (kv head
 // h's at h * nt), then the query-block and tile work lists.
-size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hkv) {
+// Scratch of a packed call: the V^T images, the two work lists, the rerun
+// list, then (frequency map only) the per-sequence remote tables, fp32 and
+// bf16, one row per token.
+static size_t varlen_lists_end(int B, int T, int Hq, int Hkv) {
   long long nq, nt;
   varlen_sizes(B, T, Hq / Hkv, &nq, &nt);
-  (void)bifocal;  // one V^T image set either way
   return (size_t)Hkv * nt * kTileBytes + (size_t)(nq + nt) * sizeof(int4) + retry_bytes(nq * Hkv);
 }
+
+size_t prefill_varlen_workspace_bytes(bool bifocal, int B, int T, int Hq, int Hkv, bool freq) {
+  (void)bifocal;  // one V^T image set either way
+  const size_t base = varlen_lists_end(B, T, Hq, Hkv);
+  if (!freq) return base;
+  return round256(base) + (size_t)T * kHalf * (sizeof(float2) + sizeof(uint32_t));
+}
+
+hipError_t launch_packed_freq_table(const int4* twork, int nt, int w_pre, const double* og,
+                                    float2* table, uint32_t* table16, hipStream_t stream);
 
 // Packed batch: q, o [T][Hq][128], k, v [T][Hkv][128], lse [Hq][T] (optional),
 // cu: B + 1 device int32.  Each sequence is prefilled as a call with its own
@@ -1171,7 +1190,7 @@ hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t
                                  const uint32_t* table16, const int32_t* cu, int B, int T,
                                  int max_len, int Hq, int Hkv,
                                  int w_pre, int w0, float slack, void* ws, hipStream_t stream,
-                                 hipEvent_t ev0, hipEvent_t ev1) {
+                                 hipEvent_t ev0, hipEvent_t ev1, const double* freq_og) {
   long long nq, nt;
   varlen_sizes(B, T, Hq / Hkv, &nq, &nt);
   if (nq * Hkv > 0x7fffffffLL || nt > 0x7fffffffLL || Hkv > 65535)
@@ -1212,6 +1231,17 @@ hipError_t launch_prefill_varlen(bool bifocal, const uint16_t* q, const uint16_t
   hipLaunchKernelGGL(varlen_plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, pl);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (bifocal && freq_og != nullptr) {  // each sequence's frequency-map rows, at its own rows
+    unsigned char* rt = (unsigned char*)ws + round256(varlen_lists_end(B, T, Hq, Hkv));
+    float2* rt32 = (float2*)rt;
+    uint32_t* rt16 = (uint32_t*)(rt + (size_t)T * kHalf * sizeof(float2));
+    e = launch_packed_freq_table(twork, (int)nt, w_pre, freq_og, rt32, rt16, stream);
+    if (e != hipSuccess) return e;
+    a.rtable = rt32;
+    a.rtable16 = rt16;
+    a.freq_map = 1;
+    a.rtab_packed = 1;
+  }
 
   PrepArgs p = {};
   p.v = v;

@@ -242,6 +242,15 @@ def test_decode_length_limit_is_exact():
 
 
 @pytest.mark.parametrize("remote_map", [-1, 2])
+def test_varlen_map_rejects_unknown_remote_map(remote_map):
+    L = api.lib()
+    rc = L.jl_bifocal_prefill_varlen_map(A, A, A, A, None, A2, 3, 300, 200, 8, 2, 128, 1e6, 64, 8,
+                                         remote_map, None)
+    assert rc == api.JL_ERR_INVALID_ARG
+    assert "remote_map" in L.jl_last_error().decode()
+
+
+@pytest.mark.parametrize("remote_map", [-1, 2])
 def test_paged_decode_map_rejects_unknown_remote_map(remote_map):
     L = api.lib()
     rc = L.jl_bifocal_decode_paged_map(A, A, A, A2, 4, 64, 10, A2, A, 1, 8, 2, 128, 1e6, 64, 8,

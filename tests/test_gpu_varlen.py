@@ -155,3 +155,42 @@ def test_varlen_mixed_long_batch_equals_per_sequence():
     want, _ = O.prefill_rows(q[None, :32768], k[None, :32768], v[None, :32768], rows, theta=1e6,
                              w_pretrained=w, w_local=w0)
     assert_close(to_f64(out)[rows[:, 2], rows[:, 1]], want, what="32K rows")
+
+
+@pytest.mark.parametrize("g", [1, 4])
+def test_varlen_freq_map_per_sequence(g):
+    """jl_bifocal_prefill_varlen_map with the frequency map (Sec. 4.5): each
+    sequence takes the map of its own length (factors 1 .. 5.2 here), its rows
+    and LSE bit-identical to jl_bifocal_prefill_map on that sequence alone and
+    matching the oracle's frequency map; the alias choice is the plain varlen
+    call bit for bit."""
+    Hkv, w, w0 = 2, 100, 30
+    lens = [300, 1, 0, 64, 65, 517, 100, 129, 37]
+    q, k, v, cu = _pack(lens, g * Hkv, Hkv, seed=20 + g)
+    T = int(cu[-1])
+    qd, kd, vd, cud = to_dev(q), to_dev(k), to_dev(v), torch.from_numpy(cu).cuda()
+    say("varlen freq-map prefill g=%d T=%d" % (g, T))
+    out = torch.full_like(qd, float("nan"))
+    lse = torch.full((q.shape[1], T), float("nan"), device="cuda")
+    api.prefill_varlen(qd, kd, vd, cud, max_seqlen=max(lens), w_pretrained=w, w_local=w0,
+                       out=out, lse=lse, remote_map="freq")
+    alias_map = api.prefill_varlen(qd, kd, vd, cud, max_seqlen=max(lens), w_pretrained=w,
+                                   w_local=w0, remote_map="alias")
+    alias = api.prefill_varlen(qd, kd, vd, cud, max_seqlen=max(lens), w_pretrained=w,
+                               w_local=w0)
+    torch.cuda.synchronize()
+    assert torch.equal(alias_map.view(torch.int16), alias.view(torch.int16))
+    o, ls = to_f64(out), lse.cpu().numpy()
+    for s, L in enumerate(lens):
+        if L == 0:
+            continue
+        a, b = cu[s], cu[s + 1]
+        one, one_lse = api.bifocal_prefill(to_dev(q[None, a:b]), to_dev(k[None, a:b]),
+                                           to_dev(v[None, a:b]), w_pretrained=w, w_local=w0,
+                                           want_lse=True, remote_map="freq")
+        torch.cuda.synchronize()
+        assert torch.equal(out[a:b].view(torch.int16), one[0].view(torch.int16)), s
+        assert torch.equal(lse[:, a:b], one_lse[0]), s
+        want, _ = O.prefill(q[None, a:b], k[None, a:b], v[None, a:b], theta=1e6, w_pretrained=w,
+                            w_local=w0, remote_map="freq")
+        assert_close(o[a:b], want[0], what="freq seq %d L=%d" % (s, L))
