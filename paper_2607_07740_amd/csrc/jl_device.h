@@ -201,13 +201,7 @@ __device__ inline uint32_t lds_addr(const void* p) {
 // read that follows the copy.
 // The compiler loads M0 itself (operand constraint); the s_nop is the wait
 // state an LDS-bound load needs after an M0 write.
-__device__ inline void dma16(const void* gptr, uint32_t lds_base) {
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(gptr), "{m0}"(lds_base)
-               : "memory");
-}
-// Same copy with a wave-uniform 64-bit base in scalar registers and a 32-bit
+// The base is wave-uniform and 64-bit, in scalar registers, with a 32-bit
 // per-lane byte offset; imm is added to both the global and the LDS address.
 template <int imm = 0>
 __device__ inline void dma16_s(const void* sbase, uint32_t voff, uint32_t lds_base) {

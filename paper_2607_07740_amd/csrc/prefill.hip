@@ -64,17 +64,9 @@ constexpr int kRotOff = 0, kVtOff = 2 * kTileBytes;
 constexpr int kSmemBytes = 4 * kTileBytes;  // 64 KB
 constexpr int kPfCopyBytes = kTileBytes / kPfWaves;  // each wave's share of a tile copy: 8 keys
 constexpr int kKeysPerWave = kPfBK / kPfWaves;
-#ifndef JL_SCHED_QK
-#define JL_SCHED_QK 5
-#endif
-#ifndef JL_SCHED_PV
-#define JL_SCHED_PV 5
-#endif
-constexpr int kSchedValuQK = JL_SCHED_QK;  // VALU instructions issued per QK MFMA
-constexpr int kSchedValuPV = JL_SCHED_PV;  // and per PV MFMA
 
 // LDS layouts.
-//   K tile (raw and rotated alike): key r (0..63) at r * 256; its 16-byte
+//   rotated K tile: key r (0..63) at r * 256; its 16-byte
 //              chunk c (d = 8c .. 8c+7) sits in slot c ^ kswz(r), with
 //              kswz(r) = (r & 15) >> 1 | (r & 1) << 3 a permutation of 0..15.
 //              16 lanes reading 16 consecutive keys at one chunk (the QK

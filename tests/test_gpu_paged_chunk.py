@@ -151,3 +151,27 @@ def test_out_of_range_table_entries_are_clamped():
     torch.cuda.synchronize()
     assert torch.equal(out.view(torch.int16), want.view(torch.int16))
     assert torch.equal(lse.view(torch.int32), want_lse.view(torch.int32))
+
+
+def test_paged_chunk_checked_pass_equals_dense():
+    """With the rescale bound lowered to 2^3 nearly every block of the chunk
+    goes through the checked rerun, whose paged instance must give the dense
+    chunk's bits too, and the oracle's values."""
+    B, Hq, Hkv, T, P, page_size, w_pre, w0 = 1, 8, 2, 900, 400, 128, 200, 50
+    q, k, v = synth.prefill_inputs(B, Hq, Hkv, T, 128, seed=31, outlier_channels=8)
+    kp, vp, table = _pool(k, v, page_size, seed=6)
+    old = api.debug_prefill_rescale_log2(3.0)
+    try:
+        say("paged chunk, checked pass on every block")
+        out, lse = _paged_chunk(q[:, P:], kp, vp, table, P, w_pre, w0)
+        want, want_lse = api.prefill_chunk(to_dev(q[:, P:]), to_dev(k), to_dev(v), q_start=P,
+                                           w_pretrained=w_pre, w_local=w0, want_lse=True)
+        torch.cuda.synchronize()
+    finally:
+        api.debug_prefill_rescale_log2(old)
+    assert torch.equal(out.view(torch.int16), want.view(torch.int16))
+    assert torch.equal(lse.view(torch.int32), want_lse.view(torch.int32))
+    rows = np.array([[0, h, x] for h in range(Hq) for x in range(P, T, 13)], dtype=np.int64)
+    ref, _ = O.prefill_rows(q, k, v, rows, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    assert_close(to_f64(out)[rows[:, 0], rows[:, 2] - P, rows[:, 1]], ref,
+                 what="paged chunk, checked pass")
