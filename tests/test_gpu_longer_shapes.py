@@ -1,0 +1,72 @@
+"""Lengths past the benchmark's 128K: a 256K prefill (G = 8) and a 512K decode
+(G = 16) with few heads, against the fp64 oracle on sampled rows, and with a
+planted remote needle that lines up only under the aliasing map of Eq. (3)."""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2607_07740_amd import api, synth
+from parity_util import (assert_close, prefill_block_q, rows_for, sample_positions, say, to_dev,
+                         to_f64)
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+THETA = 1e6
+
+
+def _needle(q, k, b, h, g, qs, ks, G, gain=4.0):
+    """Key ks of kv head h // g becomes gain R(f(qs) - f(ks)) x_q[qs] (bf16)."""
+    xq = synth.bf16_to_f32(q[b, qs, h]).astype(np.float64)
+    shift = qs // G - ks // G
+    k[b, ks, h // g] = synth.bf16_bits((gain * O.rope_rotate(xq, shift, THETA)).astype(np.float32))
+
+
+def test_prefill_256k_g8_sampled_rows_and_needle():
+    B, Hq, Hkv, L, w_pre, w0 = 1, 4, 1, 262144, 32768, 4096
+    G = api.group_size(L, w_pre)
+    assert G == 8
+    say("generating 256K prefill inputs")
+    q, k, v = synth.prefill_inputs(B, Hq, Hkv, L, 128, seed=256)
+    qs, ks = L - 1, 12345  # a remote needle for head 2
+    _needle(q, k, 0, 2, Hq // Hkv, qs, ks, G)
+    say("prefill L=%d G=%d" % (L, G))
+    out = api.bifocal_prefill(to_dev(q), to_dev(k), to_dev(v), w_pretrained=w_pre, w_local=w0)
+    torch.cuda.synchronize()
+    o = to_f64(out)
+    assert np.isfinite(o).all()
+    pos = sample_positions(L, w0, w_pre, G, prefill_block_q(Hq, Hkv), 24, seed=3)
+    rows = rows_for(B, Hq, pos)
+    say("oracle on %d rows" % len(rows))
+    want, _ = O.prefill_rows(q, k, v, rows, theta=THETA, w_pretrained=w_pre, w_local=w0)
+    assert_close(o[rows[:, 0], rows[:, 2], rows[:, 1]], want, what="prefill 256K G=8")
+    # the needle row is the needle's value row: the oracle's exactly, the kernel's too
+    vk = synth.bf16_to_f32(v[0, ks, 0]).astype(np.float64)
+    got = o[0, qs, 2]
+    ref, _ = O.prefill_rows(q, k, v, np.array([[0, 2, qs]], dtype=np.int64), theta=THETA,
+                            w_pretrained=w_pre, w_local=w0)
+    say("needle: oracle %.2e, gpu %.2e from V[k*]" % (np.abs(ref[0] - vk).max(),
+                                                      np.abs(got - vk).max()))
+    assert np.abs(ref[0] - vk).max() < 1e-6
+    assert np.abs(got - vk).max() < 2e-2
+
+
+def test_decode_512k_g16():
+    B, Hq, Hkv, max_len, w_pre, w0 = 2, 8, 1, 524288, 32768, 4096
+    lens = [max_len, 300001]
+    assert api.group_size(max_len, w_pre) == 16
+    say("generating 512K decode inputs")
+    q, kc, vc, ln = synth.decode_inputs(B, Hq, Hkv, max_len, lens, seed=512, nan_tail=True)
+    # a remote needle for head 3 of sequence 0 (its query sits at max_len - 1)
+    xq = synth.bf16_to_f32(q[0, 3]).astype(np.float64)
+    shift = (max_len - 1) // 16 - 4567 // 16
+    kc[0, 4567, 0] = synth.bf16_bits((4.0 * O.rope_rotate(xq, shift, THETA)).astype(np.float32))
+    say("decode B=%d max_len=%d" % (B, max_len))
+    out = api.bifocal_decode(to_dev(q), to_dev(kc), to_dev(vc), torch.from_numpy(ln).cuda(),
+                             w_pretrained=w_pre, w_local=w0)
+    torch.cuda.synchronize()
+    want, _, _ = O.decode(q, kc, vc, ln, theta=THETA, w_pretrained=w_pre, w_local=w0)
+    assert_close(to_f64(out), want, what="decode 512K G=16")
+    vk = synth.bf16_to_f32(vc[0, 4567, 0]).astype(np.float64)
+    assert np.abs(want[0, 3] - vk).max() < 1e-6
+    assert np.abs(to_f64(out)[0, 3] - vk).max() < 2e-2
