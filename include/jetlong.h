@@ -92,9 +92,10 @@ int64_t jl_group_size(int64_t L, int64_t w_pretrained);
  * rotation, older keys the remote one.  When G == 1 the output equals
  * jl_rope_attention bit for bit (the method reduces to the base model).
  * Requires Hq % Hkv == 0, 256 % (Hq / Hkv) == 0 and B * Hkv <= 65535.
- * K is read raw: each staged 64-key tile is rotated in registers to the view
- * of its visit (R(k) x_k on the band, R(f(k)) x_k beyond it, Sec. 3.2) and
- * kept only in on-chip memory; no rotated key is written anywhere.
+ * K is read raw: the keys of each 64-key tile are loaded into registers and
+ * rotated to the view of the visit (R(k) x_k on the band, R(f(k)) x_k beyond
+ * it, Sec. 3.2); the rotated tile is kept only in on-chip memory and no
+ * rotated key is written anywhere.
  * Memory: V is transposed into a library-owned scratch buffer of
  * B * Hkv * ceil(L / 64) * 16 KB bytes of tile images plus
  * 4 * B * Hkv * L + 256 bytes for the list of blocks the checked pass reruns,

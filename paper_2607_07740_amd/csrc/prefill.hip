@@ -779,8 +779,9 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     int lo = 0, hi = 0;
     if (!SAFE) seg1_bounds(lo, hi);
     segment(0, n_r, lo, hi, pend);
-    // segment 2 in the base view: its first tile's K image (in buffer n_r & 1,
-    // not overwritten since) is scored again with the base-rotated operand
+    // segment 2 in the base view: its first tile, already rotated to the base
+    // view (buffer n_r & 1, not overwritten since), is scored again with the
+    // base-rotated query operand
     load_q_operand(qrow, hl32, a.table, qp, a.q_scale, qop);
     qk(kbuf(n_r), sc_a);
   }
