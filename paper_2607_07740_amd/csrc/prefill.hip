@@ -37,7 +37,7 @@
 //
 // Softmax runs in the log2 domain against a per-row reference m (initially 0)
 // that the QK product subtracts itself: its first k-step accumulates onto -m.
-// The common path is exp2, convert and a dot product for the row sum.  A
+// The common path is exp2, convert, and fp32 adds for the row sum.  A
 // first, fast pass never moves the reference: it only notes, per tile, whether
 // a row's probability sum passed 2^64 and, at the end, whether a row's total
 // fell below 2^-64; a block that trips either writes nothing and is listed.
@@ -314,18 +314,6 @@ __device__ inline void load_q_operand(const uint16_t* qrow, int half, const floa
   }
 }
 
-// Row sum of 8 bf16 probabilities (one P^T operand) added to acc.
-__device__ inline float sum8(bf16x8 p, float acc) {
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const bf16x2 pair = {p[2 * i], p[2 * i + 1]};
-    acc = __builtin_amdgcn_fdot2_f32_bf16(pair, one, acc, false);
-  }
-  return acc;
-}
-
 
 // SAFE = false (fused and vanilla modes): the fast pass.  It never waits on
 // the softmax reference check; instead it records, without a branch, whether
@@ -587,19 +575,25 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
   };
 
-  // P^T operands and their row sum (of the rounded probabilities that the PV
-  // product uses); the scores are already relative to the reference
+  // P^T operands and their row sum; the scores are already relative to the
+  // reference.  The sum is of the fp32 probabilities, in two chains (even and
+  // odd entries) in the order the fast pass adds them, so a block that needs
+  // no reference move gets the same l from either pass.
   auto softmax = [&](const f32x16* sc, bf16x8* pb) __attribute__((always_inline)) {
-    float psum = 0.f;
+    float ps0 = 0.f, ps1 = 0.f;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       float p[8];
 #pragma unroll
       for (int t = 0; t < 8; ++t) p[t] = fast_exp2(sc[q >> 1][8 * (q & 1) + t]);
       pb[q] = pack8(p);
-      psum = sum8(pb[q], psum);
+#pragma unroll
+      for (int t = 0; t < 8; t += 2) {
+        ps0 += p[t];
+        ps1 += p[t + 1];
+      }
     }
-    return psum;
+    return ps0 + ps1;
   };
   // Reference check, after the tile's softmax: the reference moves when a
   // tile probability in a column could exceed 2^slack (their sum does: exp2
@@ -668,9 +662,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       // instructions.  The visit is therefore issued as two interleaved
       // streams, pinned by scheduling barriers: each MFMA of the QK product
       // of j+1 is followed by its operand read and one sixteenth of the
-      // softmax of j (two probabilities, their bf16 pair and its row sum);
+      // softmax of j (two probabilities, and the bf16 pair and row-sum adds
+      // of the previous sixteenth, so nothing waits on an exp2 just issued);
       // each MFMA of the PV product of j by its operand read and one
-      // sixteenth of the rotation of j+2.
+      // sixteenth of the rotation of j+2.  The row sum adds the fp32
+      // probabilities (dot instructions do not overlap the matrix cores).
       const unsigned char* kb = kbuf(j + 1);
       auto kop = [&](int m) __attribute__((always_inline)) {
         const int r = 32 * (m & 1) + kr_lane;
@@ -680,9 +676,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
       for (int m = 0; m < 4; ++m) ring[m] = kop(m);
       typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-      const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
       bf16x2 pw[16];
-      float ps0 = 0.f, ps1 = 0.f;
+      float ps0 = 0.f, ps1 = 0.f, e0 = 0.f, e1 = 0.f;
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
         const int blk = m & 1, st = m >> 1;
@@ -691,13 +686,18 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
         const int q = m >> 2, t = 2 * (m & 3);
         const float p0 = fast_exp2(cur[q >> 1][8 * (q & 1) + t]);
         const float p1 = fast_exp2(cur[q >> 1][8 * (q & 1) + t + 1]);
-        pw[m] = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
-        if (m & 1)
-          ps1 = __builtin_amdgcn_fdot2_f32_bf16(pw[m], one, ps1, false);
-        else
-          ps0 = __builtin_amdgcn_fdot2_f32_bf16(pw[m], one, ps0, false);
+        if (m > 0) {
+          pw[m - 1] = __builtin_convertvector((f32x2){e0, e1}, bf16x2);
+          ps0 += e0;
+          ps1 += e1;
+        }
+        e0 = p0;
+        e1 = p1;
         __builtin_amdgcn_sched_barrier(0);
       }
+      pw[15] = __builtin_convertvector((f32x2){e0, e1}, bf16x2);
+      ps0 += e0;
+      ps1 += e1;
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         pb[q] = (bf16x8){pw[4 * q][0], pw[4 * q][1], pw[4 * q + 1][0], pw[4 * q + 1][1],
