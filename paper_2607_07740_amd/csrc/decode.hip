@@ -42,7 +42,7 @@ constexpr int kDecOffDummy = kDecOffTab2 + kDecTile * kDecTabRow;  // + 16 offse
 constexpr int kDecOffPages = kDecOffDummy + 1024;                  // + landing slot for padding copies
 constexpr int kDecPageCap = 2048;  // paged caches: page indices of up to this many steps in LDS
 constexpr int kDecSmem = kDecOffPages + kDecPageCap * 4;
-constexpr int kDecCopies = 5;  // copies per wave and step (padded to a fixed count)
+constexpr int kDecCopies = 5;  // copies per step of wave 0: four K/V (padded to a fixed count) + rows
 constexpr int kStateFloats = 132;  // m, l, 2 pad, O[128]
 
 struct DecodeArgs {
@@ -326,11 +326,12 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     const uint32_t buf = smem_base + (jb % kDecBufs) * kDecBufBytes;
     const unsigned char* kstep = kbase + row0 * kv_row_bytes;
     const unsigned char* vstep = vbase + row0 * kv_row_bytes;
-    {
+    if (wave == 0) {
       // the cos/sin rows that rotate the query columns for this step: q - k0
       // (lanes 0..31) and f(q) - f(k0) (lanes 32..63) of the table, or the
-      // step's row pair of the frequency map; one copy, by wave 0
-      const uint32_t dst = wave == 0 ? buf + 2 * kDecImgBytes : smem_base + kDecOffDummy;
+      // step's row pair of the frequency map; one copy, by wave 0 alone (the
+      // other waves wait for one copy fewer per step)
+      const uint32_t dst = buf + 2 * kDecImgBytes;
       if (FREQ) {
         // two half-wave copies (each lane's LDS slot is fixed by its lane id):
         // the base row from the table, the step's row of the frequency map
@@ -428,9 +429,13 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     // cache rows of the steps copied at the end of this iteration, looked up
     // now so the block-table reads are long done by then
     const int page4 = step_page(2 * it + 4), page5 = step_page(2 * it + 5);
-    // this wave's copies of steps 2it, 2it+1 (the next pair may fly); the
-    // frequency map copies its query rows in two instructions
-    wait_vmem_n<2 * (kDecCopies + (FREQ ? 1 : 0))>();
+    // this wave's copies of steps 2it, 2it+1 (the next pair may fly): four
+    // K/V copies per step, and in wave 0 the step's query cos/sin rows too
+    // (two instructions with the frequency map)
+    if (wave == 0)
+      wait_vmem_n<2 * (kDecCopies + (FREQ ? 1 : 0))>();
+    else
+      wait_vmem_n<2 * (kDecCopies - 1)>();
     __syncthreads();  // everyone's copies (and the offset table)
     const int j = 2 * it + par;
     if (head_on && j < n_steps) {
