@@ -37,7 +37,7 @@
 //
 // Softmax runs in the log2 domain against a per-row reference m (initially 0)
 // that the QK product subtracts itself: its first k-step accumulates onto -m.
-// The common path is exp2, convert, and fp32 adds for the row sum.  A
+// The common path is exp2, convert and a dot product for the row sum.  A
 // first, fast pass never moves the reference: it only notes, per tile, whether
 // a row's probability sum passed 2^64 and, at the end, whether a row's total
 // fell below 2^-64; a block that trips either writes nothing and is listed.
@@ -288,6 +288,9 @@ __device__ inline bool work_of(const PrefillArgs& a, int bid, bool fused, Work& 
 //                 keys in the remote view, C = band in the remote view.
 //                 They write normalised fp32 O_X and the natural-log LSE_X.
 enum PrefillMode : int { kModeFused = 0, kModeVanilla = 1, kModeWinA = 2, kModeWinB = 3, kModeWinC = 4 };
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ inline bf16x2 bf16_one2() { return bf16x2{(__bf16)1.0f, (__bf16)1.0f}; }
 
 // Load one query row's B operand: 8 k-steps of 8 bf16 (d = 16 s + 8 half + j),
 // rotated to position pos and scaled.  Pairs (s, s + 4) are rotate-half partners.
@@ -575,10 +578,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
     }
   };
 
-  // P^T operands and their row sum; the scores are already relative to the
-  // reference.  The sum is of the fp32 probabilities, in two chains (even and
-  // odd entries) in the order the fast pass adds them, so a block that needs
-  // no reference move gets the same l from either pass.
+  // P^T operands and their row sum: the sum of the rounded probabilities the
+  // PV product uses, by dot products of their bf16 pairs in two chains (even
+  // and odd pairs), in the order the fast pass forms it, so a block that needs
+  // no reference move gets the same l from either pass.  The scores are
+  // already relative to the reference.
   auto softmax = [&](const f32x16* sc, bf16x8* pb) __attribute__((always_inline)) {
     float ps0 = 0.f, ps1 = 0.f;
 #pragma unroll
@@ -588,9 +592,12 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       for (int t = 0; t < 8; ++t) p[t] = fast_exp2(sc[q >> 1][8 * (q & 1) + t]);
       pb[q] = pack8(p);
 #pragma unroll
-      for (int t = 0; t < 8; t += 2) {
-        ps0 += p[t];
-        ps1 += p[t + 1];
+      for (int u = 0; u < 4; ++u) {
+        const bf16x2 pair = {pb[q][2 * u], pb[q][2 * u + 1]};
+        if (u & 1)
+          ps1 = __builtin_amdgcn_fdot2_f32_bf16(pair, bf16_one2(), ps1, false);
+        else
+          ps0 = __builtin_amdgcn_fdot2_f32_bf16(pair, bf16_one2(), ps0, false);
       }
     }
     return ps0 + ps1;
@@ -662,11 +669,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       // instructions.  The visit is therefore issued as two interleaved
       // streams, pinned by scheduling barriers: each MFMA of the QK product
       // of j+1 is followed by its operand read and one sixteenth of the
-      // softmax of j (two probabilities, and the bf16 pair and row-sum adds
-      // of the previous sixteenth, so nothing waits on an exp2 just issued);
-      // each MFMA of the PV product of j by its operand read and one
-      // sixteenth of the rotation of j+2.  The row sum adds the fp32
-      // probabilities (dot instructions do not overlap the matrix cores).
+      // softmax of j (two probabilities, and the bf16 pair of the previous
+      // sixteenth, so nothing waits on an exp2 just issued); each MFMA of the
+      // PV product of j by its operand read, one bf16 pair's dot product for
+      // the row sum (kept out of the QK stream, where it holds up the matrix
+      // cores more) and, on four of them, a quarter of the rotation of j+2.
       const unsigned char* kb = kbuf(j + 1);
       auto kop = [&](int m) __attribute__((always_inline)) {
         const int r = 32 * (m & 1) + kr_lane;
@@ -675,9 +682,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       bf16x8 ring[4];
 #pragma unroll
       for (int m = 0; m < 4; ++m) ring[m] = kop(m);
-      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
       bf16x2 pw[16];
-      float ps0 = 0.f, ps1 = 0.f, e0 = 0.f, e1 = 0.f;
+      float e0 = 0.f, e1 = 0.f;
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
         const int blk = m & 1, st = m >> 1;
@@ -686,25 +692,16 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
         const int q = m >> 2, t = 2 * (m & 3);
         const float p0 = fast_exp2(cur[q >> 1][8 * (q & 1) + t]);
         const float p1 = fast_exp2(cur[q >> 1][8 * (q & 1) + t + 1]);
-        if (m > 0) {
-          pw[m - 1] = __builtin_convertvector((f32x2){e0, e1}, bf16x2);
-          ps0 += e0;
-          ps1 += e1;
-        }
+        if (m > 0) pw[m - 1] = __builtin_convertvector((f32x2){e0, e1}, bf16x2);
         e0 = p0;
         e1 = p1;
         __builtin_amdgcn_sched_barrier(0);
       }
       pw[15] = __builtin_convertvector((f32x2){e0, e1}, bf16x2);
-      ps0 += e0;
-      ps1 += e1;
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         pb[q] = (bf16x8){pw[4 * q][0], pw[4 * q][1], pw[4 * q + 1][0], pw[4 * q + 1][1],
                          pw[4 * q + 2][0], pw[4 * q + 2][1], pw[4 * q + 3][0], pw[4 * q + 3][1]};
-      const float ps = ps0 + ps1;
-      late_bad |= __ballot(ps > p_hi);
-      l_run += ps;
       // past the list's end the last entry is rotated (and V copied) again
       const Ent e3 = ent_of(min(j + 3, n_steps - 1));
       const unsigned char* vb = vbuf(j);
@@ -717,14 +714,22 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       // the rotated words in units 1, 4, 7, 10; stored early, so the writes
       // are done well before the next barrier
       u32x4 rlo, rhi;
+      float ps0 = 0.f, ps1 = 0.f;
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
         acc_o[m & 3] = mfma32(ring[m & 3], pb[m >> 2], acc_o[m & 3]);
         if (m + 4 < 16) ring[m & 3] = vop(m + 4);
+        if (m & 1)
+          ps1 = __builtin_amdgcn_fdot2_f32_bf16(pw[m], bf16_one2(), ps1, false);
+        else
+          ps0 = __builtin_amdgcn_fdot2_f32_bf16(pw[m], bf16_one2(), ps0, false);
         if (m % 3 == 1 && m < 12) rot_word(rin, m / 3, rlo, rhi);
         if (m == 11) rot_store(j + 2, rlo, rhi);  // into the buffer QK(j) released
         __builtin_amdgcn_sched_barrier(0);
       }
+      const float ps = ps0 + ps1;
+      late_bad |= __ballot(ps > p_hi);
+      l_run += ps;
       pend = e3;
     } else {
       __builtin_amdgcn_iglp_opt(0);
