@@ -486,8 +486,8 @@ def main() -> int:
         freq_map()
         ft = [timed(freq_map) for _ in range(args.freq_reps)]
         fm = {"freq_map_prefill_ms": round(med(ft), 3)}
-        # decode with the frequency map: its rows are built per call from the
-        # device lengths (included), interleaved with the Eq. (3) decode
+        # decode with the frequency map: the kernel forms its rows from the
+        # device lengths, interleaved with the Eq. (3) decode
         fws = torch.empty(api.decode_map_workspace_bytes(wd.B, wd.Hq, wd.Hkv, wd.L, wd.d, "freq"),
                           dtype=torch.uint8, device="cuda")
 

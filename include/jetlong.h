@@ -346,10 +346,8 @@ int jl_rope_attention_decode(const void* q, const void* k_cache, const void* v_c
                              size_t workspace_bytes, void* stream);
 
 /*
- * Bytes of workspace jl_bifocal_decode_map needs: jl_decode_workspace_bytes
- * for JL_REMOTE_ALIAS; for JL_REMOTE_FREQ that, rounded up to 256, plus
- * B * (16 + ceil(max_len / 16)) * 512 bytes of per-sequence cos/sin rows.
- * Returns 0 for invalid arguments.
+ * Bytes of workspace jl_bifocal_decode_map needs: jl_decode_workspace_bytes,
+ * for either remote map.  Returns 0 for invalid arguments.
  */
 size_t jl_decode_map_workspace_bytes(int B, int Hq, int Hkv, int max_len, int head_dim,
                                      int remote_map);
@@ -363,8 +361,8 @@ size_t jl_decode_map_workspace_bytes(int B, int Hq, int Hkv, int max_len, int he
  *               gamma_i omega_i (YaRN's ramp, alpha = 1, beta = 32, no
  *               temperature), with s = max(1, kv_lens[b] / w_pretrained) per
  *               sequence, so a ragged batch mixes factors the way it mixes G.
- *               Each call first builds the rows it needs on the device (the
- *               lengths live there) into the workspace.
+ *               Each workgroup forms the cos/sin rows it needs from its
+ *               sequence's length (which lives on the device).
  *   workspace   at least jl_decode_map_workspace_bytes(..., remote_map) bytes,
  *               16-byte aligned, contents on entry irrelevant.
  * Other arguments, requirements and errors as in jl_bifocal_decode.

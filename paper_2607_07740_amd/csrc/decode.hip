@@ -60,11 +60,11 @@ struct DecodeArgs {
   int max_pages, n_pages, page_shift;
   int chunk, n_split, n_hgroups;  // n_split: split slots per (b, kv-head group)
   int balanced;  // split counts from the actual lengths (B <= 64), else from max_len
-  // frequency-interpolation remote map (Sec. 4.5): per sequence, frow_stride
-  // rows of 64 (cos, sin) pairs -- rows 0..15 rotate by t omega'_i, then per
-  // 16-key step m the row R'(q - 16 m) (omega')
-  const float2* frows;
-  int frow_stride;
+  // frequency-interpolation remote map (Sec. 4.5): omega_i and the ramp
+  // gamma_i of each frequency pair; every workgroup forms the cos/sin rows it
+  // needs from them and its sequence's length
+  double fomega[kHalf];
+  double fgamma[kHalf];
   int n_target;  // balanced: workgroups of the grid (one wave of them fills the GPU)
   int w_pre, w0;
   float q_scale;
@@ -233,6 +233,28 @@ __device__ inline f32x4 mfma16k16(bf16x4 a, bf16x4 b, f32x4 c) {
 //   apart): slot s holds frequencies 2 s, 2 s + 1
 // RMODE: 0 the vanilla kernel, 1 bifocal with the Eq. (3) map, 2 bifocal with
 // the frequency map (remote rotations at unchanged positions by omega').
+// The Sec. 4.5 map of a sequence of n keys: s = max(1, n / w_pretrained) and
+// omega'_i = (1 - gamma_i) omega_i / s + gamma_i omega_i (freq_map_omega);
+// the (cos, sin) of pos * omega'_i (freq_map_cs), with the angle formed and
+// reduced modulo 2 pi in fp64 (exact to ~1e-11 rad at 1.3e5 rad) and its sine
+// and cosine taken in fp32, within an ulp or two of the fp64 result rounded
+// to fp32.
+__device__ inline double freq_map_omega(const DecodeArgs& a, int n, int i) {
+#pragma clang fp contract(off)
+  const double om = a.fomega[i];
+  const double sc = fmax(1.0, (double)n / (double)a.w_pre);
+  return (1.0 - a.fgamma[i]) * om / sc + a.fgamma[i] * om;
+}
+__device__ inline float2 freq_map_cs(double omf, int pos) {
+#pragma clang fp contract(off)
+  const double two_pi = 6.283185307179586476925286766559;
+  double ang = (double)pos * omf;
+  ang -= two_pi * rint(ang * (1.0 / two_pi));
+  float sn, cs;
+  sincosf((float)ang, &sn, &cs);
+  return make_float2(cs, sn);
+}
+
 template <int RMODE>
 __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs a) {
   constexpr bool BIFOCAL = RMODE != 0;
@@ -264,7 +286,9 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
   const FastDiv gdiv = make_fastdiv((uint32_t)G);
   const int qpos = kv_len - 1;
   const int fq = BIFOCAL ? remote_pos(qpos, gdiv) : qpos;
-  const float2* frows_b = FREQ ? a.frows + (size_t)b * a.frow_stride * kHalf : nullptr;
+  // the frequency map's omega'_i of this lane's frequency (wave 0 forms the
+  // step rows, lane i taking frequency i)
+  const double omf_lane = FREQ ? freq_map_omega(a, kv_len, lane) : 0.0;
   const int n_steps = (s_all - split + ns - 1) / ns;
   const int n_iter = (n_steps + 1) / 2;
 
@@ -333,12 +357,11 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
       // other waves wait for one copy fewer per step)
       const uint32_t dst = buf + 2 * kDecImgBytes;
       if (FREQ) {
-        // two half-wave copies (each lane's LDS slot is fixed by its lane id):
-        // the base row from the table, the step's row of the frequency map
-        if (lane < 32)
-          dma16_s(a.table, (uint32_t)(qpos - k0) * 512 + 16 * lane, dst);
-        else
-          dma16_s(frows_b, (uint32_t)(kDecTile + k0 / kDecTile) * 512 + 16 * (lane - 32), dst);
+        // the base row copied by lanes 0..31; the frequency map's row R'(q -
+        // k0) formed here, lane i taking frequency i, and stored beside it
+        if (lane < 32) dma16_s(a.table, (uint32_t)(qpos - k0) * 512 + 16 * lane, dst);
+        const float2 cs = freq_map_cs(omf_lane, qpos - k0);
+        *(float2*)(smem + (dst - smem_base) + 512 + 8 * lane) = cs;
       } else {
         const int fk0 = BIFOCAL ? remote_pos(k0, gdiv) : k0;
         const int row = lane < 32 ? qpos - k0 : fq - fk0;
@@ -372,9 +395,13 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     for (int i = threadIdx.x; i < kDecTile * 32; i += kDecThreads) {
       const int r = i >> 5, s = i & 31;
       *(float4*)(tab + r * kDecTabRow + 16 * s) = *(const float4*)(a.table + r * kHalf + 2 * s);
-      if (FREQ)
+      if (FREQ) {
+        // the frequency map's rows t omega'_i, t = 0..15
+        const float2 c0 = freq_map_cs(freq_map_omega(a, kv_len, 2 * s), r),
+                     c1 = freq_map_cs(freq_map_omega(a, kv_len, 2 * s + 1), r);
         *(float4*)(tab + (kDecOffTab2 - kDecOffTab) + r * kDecTabRow + 16 * s) =
-            *(const float4*)(frows_b + r * kHalf + 2 * s);
+            make_float4(c0.x, c0.y, c1.x, c1.y);
+      }
     }
   }
   const unsigned char* tab = smem + kDecOffTab;
@@ -430,10 +457,9 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     // now so the block-table reads are long done by then
     const int page4 = step_page(2 * it + 4), page5 = step_page(2 * it + 5);
     // this wave's copies of steps 2it, 2it+1 (the next pair may fly): four
-    // K/V copies per step, and in wave 0 the step's query cos/sin rows too
-    // (two instructions with the frequency map)
+    // K/V copies per step, and in wave 0 the step's query cos/sin row too
     if (wave == 0)
-      wait_vmem_n<2 * (kDecCopies + (FREQ ? 1 : 0))>();
+      wait_vmem_n<2 * kDecCopies>();
     else
       wait_vmem_n<2 * (kDecCopies - 1)>();
     __syncthreads();  // everyone's copies (and the offset table)
@@ -698,52 +724,8 @@ size_t decode_workspace_bytes(int B, int Hq, int Hkv, int max_len) {
   return (size_t)B * Hq * n_split * kStateFloats * sizeof(float);
 }
 
-// Rows of the frequency map per sequence: 16 offset rows, then one row per
-// 16-key step.
-static int freq_row_stride(int max_len) { return kDecTile + (max_len + kDecTile - 1) / kDecTile; }
-static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
-
-size_t decode_map_workspace_bytes(int B, int Hq, int Hkv, int max_len, bool freq) {
-  const size_t states = decode_workspace_bytes(B, Hq, Hkv, max_len);
-  if (!freq) return states;
-  return round256(states) + (size_t)B * freq_row_stride(max_len) * kHalf * sizeof(float2);
-}
-
-struct FreqRowsArgs {
-  float2* frows;
-  const int32_t* kv_lens;
-  int max_len, w_pre, stride;
-  double omega[kHalf];  // omega_i = theta^(-2i/d)
-  double gamma[kHalf];  // the ramp of pair i: 0 below alpha turns in the window, 1 above beta
-};
-
-// The frequency map of each sequence from its own length (Sec. 4.5):
-// s = max(1, L / w_pretrained), omega'_i = (1 - gamma_i) omega_i / s +
-// gamma_i omega_i.  The angle is formed and reduced modulo 2 pi in fp64
-// (exact to ~1e-11 rad at 1.3e5 rad), then its sine and cosine are taken in
-// fp32, within an ulp or two of the fp64 result rounded to fp32.
-__global__ __launch_bounds__(256) void decode_freq_rows_kernel(FreqRowsArgs a) {
-#pragma clang fp contract(off)
-  const int b = blockIdx.y;
-  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-  const int row = (int)(idx >> 6), i = (int)(idx & 63);
-  if (row >= a.stride) return;
-  const int n = clamp_len(a.kv_lens[b], a.max_len);
-  const double om = a.omega[i];
-  const double sc = fmax(1.0, (double)n / (double)a.w_pre);
-  const double omf = (1.0 - a.gamma[i]) * om / sc + a.gamma[i] * om;
-  int pos = row;
-  if (row >= kDecTile) {
-    const int m = row - kDecTile;
-    if (m * kDecTile >= n) return;  // no such step
-    pos = n - 1 - m * kDecTile;
-  }
-  const double two_pi = 6.283185307179586476925286766559;
-  double ang = (double)pos * omf;
-  ang -= two_pi * rint(ang * (1.0 / two_pi));
-  float sn, cs;
-  sincosf((float)ang, &sn, &cs);
-  a.frows[((size_t)b * a.stride + row) * kHalf + i] = make_float2(cs, sn);
+size_t decode_map_workspace_bytes(int B, int Hq, int Hkv, int max_len, bool /*freq*/) {
+  return decode_workspace_bytes(B, Hq, Hkv, max_len);
 }
 
 // block_table == nullptr: dense caches [B][max_len][Hkv][128]; otherwise
@@ -785,23 +767,10 @@ hipError_t launch_decode(bool bifocal, const uint16_t* q, const uint16_t* kc, co
   hipError_t e = hipSuccess;
   const bool freq = bifocal && freq_og != nullptr;
   if (freq) {
-    FreqRowsArgs f;
-    f.frows = (float2*)((unsigned char*)ws +
-                        round256(decode_workspace_bytes(B, Hq, Hkv, max_len)));
-    f.kv_lens = kv_lens;
-    f.max_len = max_len;
-    f.w_pre = w_pre;
-    f.stride = freq_row_stride(max_len);
     for (int i = 0; i < kHalf; ++i) {
-      f.omega[i] = freq_og[i];
-      f.gamma[i] = freq_og[kHalf + i];
+      a.fomega[i] = freq_og[i];
+      a.fgamma[i] = freq_og[kHalf + i];
     }
-    a.frows = f.frows;
-    a.frow_stride = f.stride;
-    const long long blocks = ((long long)f.stride * kHalf + 255) / 256;
-    if (blocks > 0x7fffffffLL || B > 65535) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(decode_freq_rows_kernel, dim3((unsigned)blocks, B), dim3(256), 0, stream, f);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   // ev0 / ev1 (optional) are recorded on the stream around the split kernel
   if (ev0 != nullptr && (e = hipEventRecord(ev0, stream)) != hipSuccess) return e;
