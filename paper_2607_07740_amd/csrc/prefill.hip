@@ -895,7 +895,7 @@ static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L) {
   const size_t rows = (size_t)B * L * Hq;
   return 3 * rows * kHeadDim * sizeof(float) + round256(3 * rows * sizeof(float)) +
-         image_bytes(B, Hkv, L);
+         image_bytes(B, Hkv, L) + retry_bytes((long long)B * Hkv * L);
 }
 
 // rtable: the remote view's table, nullptr for the aliasing map (then the
@@ -981,7 +981,7 @@ static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream
   if (nwg > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   const dim3 grid((unsigned)nwg), block(kPfThreads);
   PrefillArgs w = a;
-  w.retry_list = nullptr;  // the window passes check every tile
+  w.retry_list = nullptr;  // the band windows A and C check every tile
   if (a.block_table != nullptr) {  // paged caches: the chunk entry points only
     if (mode == kModeFused) return launch_fast_then_checked<kModeFused, true>(a, grid, stream);
     if (mode == kModeVanilla) return launch_fast_then_checked<kModeVanilla, true>(a, grid, stream);
@@ -991,7 +991,7 @@ static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream
     case kModeFused: return launch_fast_then_checked<kModeFused>(a, grid, stream);
     case kModeVanilla: return launch_fast_then_checked<kModeVanilla>(a, grid, stream);
     case kModeWinA: hipLaunchKernelGGL((prefill_kernel<kModeWinA, true>), grid, block, 0, stream, w); break;
-    case kModeWinB: hipLaunchKernelGGL((prefill_kernel<kModeWinB, true>), grid, block, 0, stream, w); break;
+    case kModeWinB: return launch_fast_then_checked<kModeWinB>(a, grid, stream);
     case kModeWinC: hipLaunchKernelGGL((prefill_kernel<kModeWinC, true>), grid, block, 0, stream, w); break;
     default: return hipErrorInvalidValue;
   }
@@ -1040,8 +1040,10 @@ hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const ui
                  round256(3 * rows * sizeof(float));
   PrefillArgs a = {};
   fill_geometry(a, B, Hq, Hkv, L, 0, L, slack);
+  // window B (every causal key, the bulk of the work) runs as the fused call
+  // does: a fast pass, then the checked rerun of the blocks it lists
   hipError_t e = launch_prep(k, v, table, rtable, table16, rtable16, freq_map, B, Hkv, L, L, G,
-                             images, false, a, stream);
+                             images, true, a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
   const int modes[3] = {kModeWinA, kModeWinB, kModeWinC};
