@@ -43,7 +43,7 @@ constexpr int kDecOffPages = kDecOffDummy + 1024;                  // + landing 
 constexpr int kDecPageCap = 2048;  // paged caches: page indices of up to this many steps in LDS
 constexpr int kDecSmem = kDecOffPages + kDecPageCap * 4;
 constexpr int kDecCopies = 5;  // copies per step of wave 0: four K/V (padded to a fixed count) + rows
-constexpr int kStateFloats = 132;  // m, l, 2 pad, O[128]
+constexpr int kStateFloats = 132;  // m, l, the split count (int bits), pad, O[128]
 
 struct DecodeArgs {
   const uint16_t* q;
@@ -153,16 +153,6 @@ __device__ inline SplitWork split_work(const DecodeArgs& a, int bid) {
   w.hgroup = __builtin_amdgcn_readfirstlane(w.hgroup);
   w.split = __builtin_amdgcn_readfirstlane(w.split);
   return w;
-}
-
-// Splits holding the states of sequence b (the same count split_work gave it).
-__device__ inline int split_count(const DecodeArgs& a, int b) {
-  if (!a.balanced)
-    return min(a.n_split, (clamp_len(a.kv_lens[b], a.max_len) + kDecTile - 1) / kDecTile);
-  const int s = lane_steps(a, threadIdx.x & 63);
-  const int u = balanced_unit(a, s);
-  const int sb = __shfl(s, b);
-  return __builtin_amdgcn_readfirstlane(min(a.n_split, (sb + u - 1) / u));
 }
 
 // Rotate 8 (d, d + 64) pairs given in fp32 by the (cos, sin) pairs c4[0..3]
@@ -608,7 +598,10 @@ __global__ __launch_bounds__(kDecThreads, 1) void decode_split_kernel(DecodeArgs
     }
     if (writer) *(f32x4*)(out + 4 + 16 * db + 4 * g4) = o4;
   }
-  if (writer && g4 == 0) *(f32x4*)out = f32x4{m_own, W_own * l_own + W_oth * l_oth, 0.f, 0.f};
+  // the state's third word carries this sequence's split count, so the
+  // reduce need not recompute the plan (slot 0 is written by every call)
+  if (writer && g4 == 0)
+    *(f32x4*)out = f32x4{m_own, W_own * l_own + W_oth * l_oth, __int_as_float(ns), 0.f};
 }
 
 // Final merge over the splits of one head (Eq. (7) weights exp2(m - M)):
@@ -624,14 +617,13 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
   __shared__ float sDen[kRedGroups];
   const int bh = blockIdx.x;
   const int quarter = blockIdx.y;
-  const int b = bh / a.Hq;
   const int tid = threadIdx.x;
   const float* base = a.ws + (size_t)bh * a.n_split * kStateFloats;
   const int c = tid & 7;
   const int grp = tid >> 3;
 
-  // every slot is read without waiting for the split count (which needs
-  // kv_lens); the slots past it hold stale states and are dropped below
+  // every slot is read at once, slot 0's state carrying the sequence's split
+  // count; the slots past it hold stale states and are dropped below
   float m[kRedPerGroup], l[kRedPerGroup];
   f32x4 ov[kRedPerGroup];
 #pragma unroll
@@ -644,7 +636,7 @@ __global__ __launch_bounds__(256) void decode_reduce_kernel(DecodeArgs a, uint16
     l[i] = ml.y;
     ov[i] = *(const f32x4*)(stt + 4 + 32 * quarter + 4 * c);
   }
-  const int ns = split_count(a, b);  // splits with keys
+  const int ns = __float_as_int(base[2]);  // splits with keys, from slot 0's state
 #pragma unroll
   for (int i = 0; i < kRedPerGroup; ++i) {
     if (grp + kRedGroups * i >= ns) {
