@@ -304,7 +304,10 @@ size_t jl_decode_workspace_bytes(int B, int Hq, int Hkv, int max_len, int head_d
  *                                              token already appended
  *   v_cache  bf16 [B, max_len, Hkv, head_dim]
  *   kv_lens  int32 [B] DEVICE array, 1 <= kv_lens[b] <= max_len; positions
- *            at or past kv_lens[b] are never read
+ *            at or past kv_lens[b] are never read.  The host cannot check
+ *            it: a value below 1 is read as 1 and one past max_len as
+ *            max_len, so a bad length gives wrong values, never an
+ *            out-of-bounds read
  *   o        bf16 [B, Hq, head_dim] output (written)
  *   workspace, workspace_bytes: device scratch of at least
  *            jl_decode_workspace_bytes(B, Hq, Hkv, max_len, head_dim) bytes,
@@ -382,6 +385,7 @@ int jl_bifocal_decode_map(const void* q, const void* k_cache, const void* v_cach
  *   block_table      int32 [B, max_pages] DEVICE array: key k of sequence b
  *                    is row k % page_size of page block_table[b][k / page_size]
  *   kv_lens          int32 [B] DEVICE array, 1 <= kv_lens[b] <= max_pages * page_size
+ *                    (clamped into that range as in jl_bifocal_decode)
  * page_size is a power of two, at least 16 (a 16-key step of the kernel never
  * straddles two pages).  Page indices outside [0, n_pages) are clamped into
  * the pool, so a bad table gives wrong values, never an out-of-bounds read.

@@ -109,3 +109,21 @@ def test_decode_batch_split_plans(B):
         want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=w0,
                               bifocal=bif)
         assert_close(to_f64(out), want, what="decode B=%d bifocal=%s" % (B, bif))
+
+
+def test_decode_lengths_outside_range_are_clamped():
+    """kv_lens lives on the device, so the host cannot check it: a length below
+    1 reads as 1 and one past max_len as max_len, bit for bit, with no read
+    outside the cache (NaN tails past every clamped length would show one)."""
+    Hq, Hkv, w_pre, w0, max_len = 8, 2, 256, 64, 1000
+    bad = [0, -7, max_len + 50, 2 ** 31 - 1, 700]
+    good = [1, 1, max_len, max_len, 700]
+    q, kc, vc, _ = synth.decode_inputs(len(bad), Hq, Hkv, max_len, good, seed=17, nan_tail=True)
+    say("decode clamped lens", bad)
+    for bif in (True, False):
+        a = _run(bif, q, kc, vc, bad, w_pre, w0)
+        b = _run(bif, q, kc, vc, good, w_pre, w0)
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+        want, _, _ = O.decode(q, kc, vc, good, theta=1e6, w_pretrained=w_pre, w_local=w0,
+                              bifocal=bif)
+        assert_close(to_f64(a), want, what="clamped lens bifocal=%s" % bif)
