@@ -663,17 +663,18 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
       // raw K(j+2) and its cos/sin row into registers: they land while
       // QK(j+1) and the softmax of j run
       const RotIn rin = rot_load(pend);
-      // The two waves of a SIMD pass the per-tile barrier together, so a
-      // block of VALU work in one wave finds the other at the same point and
-      // the matrix core idles unless each wave feeds it between its own VALU
-      // instructions.  The visit is therefore issued as two interleaved
-      // streams, pinned by scheduling barriers: each MFMA of the QK product
-      // of j+1 is followed by its operand read and one sixteenth of the
-      // softmax of j (two probabilities, and the bf16 pair of the previous
-      // sixteenth, so nothing waits on an exp2 just issued); each MFMA of the
-      // PV product of j by its operand read, one bf16 pair's dot product for
-      // the row sum (kept out of the QK stream, where it holds up the matrix
-      // cores more) and, on four of them, a quarter of the rotation of j+2.
+      // The visit is written as two streams cut by scheduling barriers: each
+      // MFMA of the QK product of j+1 with its operand read and one
+      // sixteenth of the softmax of j (two probabilities, and the bf16 pair
+      // of the previous sixteenth); each MFMA of the PV product of j with its
+      // operand read, one bf16 pair's dot product for the row sum and, on
+      // four of them, a quarter of the rotation of j+2.  The barriers keep
+      // the operand reads and the rotation quarters in place.  The pure
+      // arithmetic is placed before them, by instruction selection: the
+      // exp2 and conversions come together after the QK product's MFMAs and
+      // the row-sum dot products after the PV product.  Forcing the written
+      // interleave with empty asm ties on each result measured 3% slower on
+      // gfx950, and so did leaving the rotation to the compiler as well.
       const unsigned char* kb = kbuf(j + 1);
       auto kop = [&](int m) __attribute__((always_inline)) {
         const int r = 32 * (m & 1) + kr_lane;
