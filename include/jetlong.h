@@ -127,9 +127,11 @@ enum {
  * When L <= w_pretrained (s = 1, G = 1) both maps run the vanilla kernel.
  * The frequency map keeps one library-owned table of cos/sin(p * omega'_i),
  * L x 512 bytes per device, for the last (rope_theta, L, w_pretrained) used;
- * a new configuration builds a new table (waiting for the stream) and keeps
- * the old one until jl_release_caches.  Other arguments, scratch and errors
- * as in jl_bifocal_prefill; remote_map outside {0, 1} -> JL_ERR_INVALID_ARG.
+ * a new configuration waits for the whole device and rebuilds that table in
+ * place (in a new buffer of at least twice the capacity when L does not fit,
+ * the old one freed), then waits for the stream.  jl_release_caches frees it.
+ * Other arguments, scratch and errors as in jl_bifocal_prefill; remote_map
+ * outside {0, 1} -> JL_ERR_INVALID_ARG.
  */
 int jl_bifocal_prefill_map(const void* q, const void* k, const void* v, void* o, float* lse,
                            int B, int Hq, int Hkv, int L, int head_dim, double rope_theta,
@@ -282,7 +284,9 @@ size_t jl_prefill_literal_workspace_bytes(int B, int Hq, int Hkv, int L, int hea
  *     x * B * L * Hq * head_dim, and LSE_X as fp32 [B, Hq, L] at float offset
  *     3 * B * L * Hq * head_dim + x * B * Hq * L.
  * When G == 1 the call runs the vanilla kernel, as jl_bifocal_prefill does,
- * and leaves the workspace unwritten.  No library scratch is used.
+ * with its transposed value tiles in the workspace's tile region; the window
+ * outputs and LSEs are left unwritten.  Either way no library scratch is
+ * used (only the RoPE table cache, as for every entry point).
  */
 int jl_bifocal_prefill_literal(const void* q, const void* k, const void* v, void* o, float* lse,
                                int B, int Hq, int Hkv, int L, int head_dim, double rope_theta,

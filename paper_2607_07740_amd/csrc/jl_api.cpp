@@ -340,8 +340,9 @@ int check_common(int B, int Hq, int Hkv, int head_dim, double theta) {
 }
 
 // literal: run Eq. (7) as three window passes plus a merge, in the caller's
-// workspace (ws, ws_bytes); otherwise the fused or vanilla kernel with the
-// library scratch.
+// workspace (ws, ws_bytes), or at G == 1 the vanilla kernel with its tile
+// images in that workspace's tile region; otherwise the fused or vanilla
+// kernel with the library scratch.
 int prefill_common(bool bifocal, const void* q, const void* k, const void* v, void* o, float* lse,
                    int B, int Hq, int Hkv, int L, int head_dim, double theta, int w_pre, int w0,
                    void* stream, bool literal = false, void* ws = nullptr, size_t ws_bytes = 0,
@@ -406,8 +407,15 @@ int prefill_common(bool bifocal, const void* q, const void* k, const void* v, vo
   }
   std::lock_guard<std::mutex> launch_lock(g_prefill_mu);
   void* scratch = nullptr;
-  st = get_scratch(s, jl::prefill_workspace_bytes(use_bifocal, B, Hkv, L), &scratch);
-  if (st != JL_OK) return st;
+  if (literal) {
+    // the literal workspace ends with the tile images and rerun list that
+    // the vanilla kernel needs (the same layout as the library scratch)
+    const size_t tail = jl::prefill_workspace_bytes(false, B, Hkv, L);
+    scratch = static_cast<char*>(ws) + (jl::literal_workspace_bytes(B, Hq, Hkv, L) - tail);
+  } else {
+    st = get_scratch(s, jl::prefill_workspace_bytes(use_bifocal, B, Hkv, L), &scratch);
+    if (st != JL_OK) return st;
+  }
   hipEvent_t ev0, ev1;
   timing_events(0, &ev0, &ev1);
   hipError_t e = jl::launch_prefill_chunk(use_bifocal, (const uint16_t*)q, (const uint16_t*)k,

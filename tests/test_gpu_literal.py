@@ -144,6 +144,32 @@ def test_literal_within_window_is_vanilla():
     assert torch.equal(out.view(torch.int16), van.view(torch.int16))
 
 
+def test_literal_within_window_allocates_nothing():
+    """G == 1 at the 32K within-window shape: the vanilla kernel the literal
+    entry runs stages its value tiles in the caller's workspace, so the call
+    adds no device memory once the RoPE table covers L (a decode of the same
+    length builds that table first), and it still equals the vanilla call."""
+    B, Hq, Hkv, L = 1, 32, 8, 32768
+    q, k, v = (to_dev(x) for x in synth.prefill_inputs(B, Hq, Hkv, L, 128, seed=8))
+    out = torch.empty_like(q)
+    need = api.prefill_literal_workspace_bytes(B, Hq, Hkv, L)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    dq = q[:, L - 1].contiguous()
+    lens = torch.full((B,), L, dtype=torch.int32, device="cuda")
+    api.release_caches()
+    api.bifocal_decode(dq, k, v, lens, w_pretrained=L, w_local=64)
+    torch.cuda.synchronize()
+    free0, _ = torch.cuda.mem_get_info()
+    say("literal G == 1 at L=%d, free %.1f GB" % (L, free0 / 1e9))
+    api.bifocal_prefill_literal(q, k, v, w_pretrained=L, w_local=64, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info()
+    assert free0 - free1 < (8 << 20), (free0, free1)
+    van = api.rope_attention(q, k, v)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), van.view(torch.int16))
+
+
 def test_literal_rejects_small_workspace():
     B, Hq, Hkv, L = 1, 4, 2, 128
     q, k, v = (to_dev(x) for x in synth.prefill_inputs(B, Hq, Hkv, L, 128, seed=1))
