@@ -41,8 +41,9 @@
  *    The literal and decode entry points use the caller's workspace and
  *    allocate nothing else.  jl_release_caches frees every cache.
  *  - Thread safety: calls may come from several host threads; the library's
- *    only shared state (a per-device cache of cos/sin tables) is guarded by a
- *    mutex.  Calls that share output buffers must be ordered by the caller.
+ *    shared state (the caches above and the debug settings below) is guarded
+ *    by mutexes.  Calls that share output buffers must be ordered by the
+ *    caller.
  *  - Status codes are returned; no exception crosses the ABI and nothing
  *    aborts.  jl_last_error() gives a human-readable detail for the calling
  *    thread's most recent failure.
@@ -469,12 +470,14 @@ int jl_debug_prefill_tiles(int L, int Hq, int Hkv, int w_local, int8_t* classes_
 double jl_debug_prefill_rescale_log2(double log2_bound);
 
 /*
- * Timing hook for benchmarks, process-wide.  which = 0: every later
- * jl_bifocal_prefill / jl_rope_attention call records the HIP event `start`
- * on its stream right before its attention kernel and `stop` right after it,
- * so hipEventElapsedTime(start, stop) is that kernel's duration alone (the
- * value-transpose kernel in front of it stays outside).  which = 1: the same
- * around the split kernel of every decode call (the reduce stays outside).
+ * Timing hook for benchmarks, process-wide.  which = 0: every later prefill
+ * call that runs the fused or vanilla attention kernel (every prefill entry
+ * point but the literal one's three window passes) records the HIP event
+ * `start` on its stream right before that kernel and `stop` right after its
+ * checked rerun, so hipEventElapsedTime(start, stop) is the attention alone
+ * (the value-transpose kernel in front of it stays outside).  which = 1: the
+ * same around the split kernel of every decode call that takes a workspace
+ * (all but jl_bifocal_decode_noalloc; the reduce stays outside).
  * start, stop: hipEvent_t created and owned by the caller; NULL, NULL clears
  * the hook.  JL_ERR_INVALID_ARG for another `which` or when only one event is
  * NULL.  The events must outlive every call that records them.
