@@ -70,3 +70,45 @@ def test_decode_512k_g16():
     vk = synth.bf16_to_f32(vc[0, 4567, 0]).astype(np.float64)
     assert np.abs(want[0, 3] - vk).max() < 1e-6
     assert np.abs(to_f64(out)[0, 3] - vk).max() < 2e-2
+
+
+def test_decode_at_the_maximum_length():
+    """max_len = 2^23, the largest length the decode accepts (G = 256): the
+    query's cos/sin rows reach the last table row and byte offset 2^32 - 512.
+    The fp64 oracle would rotate 2^23 keys per view, so the check is by
+    construction instead: every key is zero but two planted ones, a remote
+    key that lines up with head 0's query only under Eq. (3) with G = 256
+    and a band key that lines up with head 1's under the base rotation.
+    Each needle scores about 34 against 0 for the 2^23 others, so each head's
+    output is its needle's value row to within 1e-8 before bf16 rounding; the
+    vanilla decode, which rotates the remote key to its own position, is not."""
+    B, Hq, Hkv, max_len, w_pre, w0 = 1, 2, 1, 1 << 23, 32768, 4096
+    G = api.group_size(max_len, w_pre)
+    assert G == 256
+    qpos = max_len - 1
+    rng = np.random.default_rng(23)
+    q = synth.bf16_bits(rng.standard_normal((B, Hq, 128), dtype=np.float32))
+    say("building 2^23-key caches")
+    kc = np.zeros((B, max_len, Hkv, 128), dtype=np.uint16)
+    pool = synth.bf16_bits(rng.standard_normal((1 << 16, 128), dtype=np.float32))
+    vc = np.tile(pool, (max_len >> 16, 1)).reshape(B, max_len, Hkv, 128)
+    ks_r, ks_l, gain = 1234567, qpos - 1000, 3.0
+    xq = synth.bf16_to_f32(q[0]).astype(np.float64)
+    kc[0, ks_r, 0] = synth.bf16_bits(
+        (gain * O.rope_rotate(xq[0], qpos // G - ks_r // G, THETA)).astype(np.float32))
+    kc[0, ks_l, 0] = synth.bf16_bits((gain * O.rope_rotate(xq[1], qpos - ks_l, THETA)).astype(np.float32))
+    vc[0, ks_r, 0] = synth.bf16_bits(rng.standard_normal(128, dtype=np.float32))
+    vc[0, ks_l, 0] = synth.bf16_bits(rng.standard_normal(128, dtype=np.float32))
+    qd, kd, vd = to_dev(q), to_dev(kc), to_dev(vc)
+    ld = torch.full((B,), max_len, dtype=torch.int32, device="cuda")
+    say("decode max_len=%d G=%d" % (max_len, G))
+    out = to_f64(api.bifocal_decode(qd, kd, vd, ld, w_pretrained=w_pre, w_local=w0))
+    van = to_f64(api.rope_attention_decode(qd, kd, vd, ld))
+    torch.cuda.synchronize()
+    want = synth.bf16_to_f32(vc[0, [ks_r, ks_l], 0]).astype(np.float64)
+    err = np.abs(out[0] - want)
+    say("needle rows: max err %.2e, mean %.2e; vanilla head 0 off by %.2f" %
+        (err.max(), err.mean(), np.abs(van[0, 0] - want[0]).max()))
+    assert np.isfinite(out).all()
+    assert err.max() < 2e-2 and err.mean() < 1e-3
+    assert np.abs(van[0, 0] - want[0]).max() > 0.5
