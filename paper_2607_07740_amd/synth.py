@@ -22,16 +22,23 @@ BF16_NAN = 0x7FC0
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:
-    """float32 -> bf16 bit patterns (uint16), round to nearest even."""
+    """float32 -> bf16 bit patterns (uint16), round to nearest even.
+
+    The sum u + 0x7FFF + lsb is formed in uint32; where it wraps (NaN
+    patterns only) the kept bits 16..31 are those the exact sum would give,
+    as the result is 16 bits wide either way."""
     x = np.ascontiguousarray(x, dtype=np.float32)
     u = x.view(np.uint32)
     out = np.empty(u.shape, dtype=np.uint16)
     step = 1 << 24  # chunked to bound temporaries on very large inputs
     flat_u, flat_o = u.reshape(-1), out.reshape(-1)
     for s in range(0, flat_u.size, step):
-        c = flat_u[s:s + step].astype(np.uint64)
-        r = ((c >> 16) & 1) + 0x7FFF
-        flat_o[s:s + step] = ((c + r) >> 16).astype(np.uint16)
+        c = flat_u[s:s + step]
+        r = (c >> 16) & 1
+        r += 0x7FFF
+        r += c
+        r >>= 16
+        flat_o[s:s + step] = r
     return out
 
 

@@ -1,6 +1,7 @@
-"""Lengths past the benchmark's 128K: a 256K prefill (G = 8) and a 512K decode
-(G = 16) with few heads, against the fp64 oracle on sampled rows, and with a
-planted remote needle that lines up only under the aliasing map of Eq. (3)."""
+"""Lengths past the benchmark's 128K: 256K and 1M prefills (G = 8, 32) and a
+512K decode (G = 16) with few heads, against the fp64 oracle on sampled rows,
+each with a planted remote needle that lines up only under the aliasing map of
+Eq. (3); and the decode at its largest accepted length, 2^23."""
 import numpy as np
 import pytest
 
@@ -22,12 +23,13 @@ def _needle(q, k, b, h, g, qs, ks, G, gain=4.0):
     k[b, ks, h // g] = synth.bf16_bits((gain * O.rope_rotate(xq, shift, THETA)).astype(np.float32))
 
 
-def test_prefill_256k_g8_sampled_rows_and_needle():
-    B, Hq, Hkv, L, w_pre, w0 = 1, 4, 1, 262144, 32768, 4096
+@pytest.mark.parametrize("L,G_want", [(262144, 8), (1048576, 32)])
+def test_prefill_long_sampled_rows_and_needle(L, G_want):
+    B, Hq, Hkv, w_pre, w0 = 1, 4, 1, 32768, 4096
     G = api.group_size(L, w_pre)
-    assert G == 8
-    say("generating 256K prefill inputs")
-    q, k, v = synth.prefill_inputs(B, Hq, Hkv, L, 128, seed=256)
+    assert G == G_want
+    say("generating %dK prefill inputs" % (L // 1024))
+    q, k, v = synth.prefill_inputs(B, Hq, Hkv, L, 128, seed=L // 1024)
     qs, ks = L - 1, 12345  # a remote needle for head 2
     _needle(q, k, 0, 2, Hq // Hkv, qs, ks, G)
     say("prefill L=%d G=%d" % (L, G))
@@ -39,7 +41,7 @@ def test_prefill_256k_g8_sampled_rows_and_needle():
     rows = rows_for(B, Hq, pos)
     say("oracle on %d rows" % len(rows))
     want, _ = O.prefill_rows(q, k, v, rows, theta=THETA, w_pretrained=w_pre, w_local=w0)
-    assert_close(o[rows[:, 0], rows[:, 2], rows[:, 1]], want, what="prefill 256K G=8")
+    assert_close(o[rows[:, 0], rows[:, 2], rows[:, 1]], want, what="prefill %dK G=%d" % (L // 1024, G))
     # the needle row is the needle's value row: the oracle's exactly, the kernel's too
     vk = synth.bf16_to_f32(v[0, ks, 0]).astype(np.float64)
     got = o[0, qs, 2]
