@@ -231,7 +231,7 @@ def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--prefill", default="qwen3_8b_prefill_128k")
     ap.add_argument("--decode", default="qwen3_4b_decode_128k")
     ap.add_argument("--overhead-reps", type=int, default=3,
