@@ -127,3 +127,20 @@ def test_decode_lengths_outside_range_are_clamped():
         want, _, _ = O.decode(q, kc, vc, good, theta=1e6, w_pretrained=w_pre, w_local=w0,
                               bifocal=bif)
         assert_close(to_f64(a), want, what="clamped lens bifocal=%s" % bif)
+
+
+@pytest.mark.parametrize("Hkv,g", [(3, 2), (6, 1), (6, 4)])
+def test_decode_partial_head_groups(Hkv, g):
+    """A workgroup serves up to 4 kv heads: Hkv = 3 leaves one group of three,
+    Hkv = 6 a full group beside a group of two, whose unused copy slots land
+    in a slot nobody reads.  Ragged lengths with NaN tails, both kernels."""
+    Hq, w_pre, w0, max_len = g * Hkv, 256, 40, 3000
+    lens = [3000, 1, 1777, 257]
+    q, kc, vc, lens = synth.decode_inputs(len(lens), Hq, Hkv, max_len, lens, seed=Hkv * 10 + g,
+                                          nan_tail=True)
+    say("decode partial head groups Hkv=%d g=%d" % (Hkv, g))
+    for bif in (True, False):
+        out = _run(bif, q, kc, vc, lens, w_pre, w0)
+        want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=w0,
+                              bifocal=bif)
+        assert_close(to_f64(out), want, what="Hkv=%d g=%d bifocal=%s" % (Hkv, g, bif))

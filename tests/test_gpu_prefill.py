@@ -65,6 +65,20 @@ def test_ragged_shapes_full_tensor(L, g, w_pre, w0):
         assert torch.equal(out.view(torch.int16), van.view(torch.int16))
 
 
+@pytest.mark.parametrize("B,Hkv,g,L", [(2, 3, 2, 300), (4, 6, 1, 200), (1, 5, 8, 129)])
+def test_kv_group_counts_and_block_orders(B, Hkv, g, L):
+    """B * Hkv kv groups of 6, 24 and 5: the workgroup order differs when the
+    count divides by 8 (each XCD takes whole groups) and when it does not."""
+    w_pre, w0 = 64, 30
+    q, k, v = synth.prefill_inputs(B, g * Hkv, Hkv, L, 128, seed=B * 100 + Hkv, outlier_channels=8)
+    say("prefill B=%d Hkv=%d g=%d L=%d" % (B, Hkv, g, L))
+    for bif in (True, False):
+        out = _run(bif, q, k, v, w_pre, w0)
+        want, _ = (O.prefill(q, k, v, theta=1e6, w_pretrained=w_pre, w_local=w0) if bif
+                   else O.prefill(q, k, v, theta=1e6, bifocal=False))
+        assert_close(to_f64(out), want, what="B=%d Hkv=%d bifocal=%s" % (B, Hkv, bif))
+
+
 @pytest.mark.parametrize("bifocal", [True, False])
 @pytest.mark.parametrize("L,g,w_pre,w0", [(300, 4, 70, 20), (517, 2, 100, 128), (64, 1, 16, 5)])
 def test_rescale_path_on_every_tile(bifocal, L, g, w_pre, w0):
