@@ -144,3 +144,18 @@ def test_decode_partial_head_groups(Hkv, g):
         want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=w0,
                               bifocal=bif)
         assert_close(to_f64(out), want, what="Hkv=%d g=%d bifocal=%s" % (Hkv, g, bif))
+
+
+def test_decode_band_covering_every_key_is_vanilla():
+    """w_local >= kv_len - 1 for every sequence: no key takes the remote view
+    and the bifocal decode gives the vanilla decode's output bit for bit,
+    whatever G each length gives (here 1 to 12)."""
+    Hq, Hkv, w_pre, max_len = 8, 2, 256, 3000
+    lens = [3000, 2999, 257, 1, 1500]
+    q, kc, vc, lens = synth.decode_inputs(len(lens), Hq, Hkv, max_len, lens, seed=31, nan_tail=True)
+    say("decode band over every key")
+    a = _run(True, q, kc, vc, lens, w_pre, max_len - 1)
+    b = _run(False, q, kc, vc, lens, w_pre, 0)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=max_len - 1)
+    assert_close(to_f64(a), want, what="decode band over every key")

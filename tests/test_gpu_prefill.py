@@ -189,3 +189,19 @@ def test_long_8b_128k_sampled_rows():
 
 def test_long_8b_64k_sampled_rows():
     _sampled_parity("qwen3_8b_prefill_64k", 16)
+
+
+@pytest.mark.parametrize("w0", [299, 1 << 30])
+def test_band_covering_every_key_is_vanilla(w0):
+    """w_local >= L - 1 leaves no remote pair (Eq. (1)), so the bifocal call
+    is the base model whatever G is (here G = 5): the fused kernel then visits
+    the vanilla kernel's tiles in its order with its masks, bit for bit."""
+    B, Hkv, g, L, w_pre = 2, 2, 4, 300, 64
+    assert api.group_size(L, w_pre) == 5
+    q, k, v = synth.prefill_inputs(B, g * Hkv, Hkv, L, 128, seed=w0 % 1000, outlier_channels=8)
+    say("prefill band over every key, w0=%d" % w0)
+    out = _run(True, q, k, v, w_pre, w0)
+    van = _run(False, q, k, v, 0, 0)
+    assert torch.equal(out.view(torch.int16), van.view(torch.int16))
+    want, _ = O.prefill(q, k, v, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    assert_close(to_f64(out), want, what="band over every key")
