@@ -159,3 +159,18 @@ def test_decode_band_covering_every_key_is_vanilla():
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
     want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=max_len - 1)
     assert_close(to_f64(a), want, what="decode band over every key")
+
+
+@pytest.mark.parametrize("w_pre,w0", [(1, 0), (1, 5), (7, 0)])
+def test_decode_extreme_windows(w_pre, w0):
+    """w_pretrained = 1 makes G the length itself, so every remote key sits
+    at position f(k) = 0 (no rotation at all); w_local = 0 leaves only the
+    query's own key in the band (Sec. 4's attention-to-self case)."""
+    Hq, Hkv, max_len = 8, 2, 700
+    lens = [700, 1, 2, 65, 333]
+    q, kc, vc, lens = synth.decode_inputs(len(lens), Hq, Hkv, max_len, lens, seed=w_pre * 10 + w0,
+                                          nan_tail=True)
+    say("decode w_pre=%d w0=%d" % (w_pre, w0))
+    out = _run(True, q, kc, vc, lens, w_pre, w0)
+    want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    assert_close(to_f64(out), want, what="decode w_pre=%d w0=%d" % (w_pre, w0))
