@@ -1,5 +1,6 @@
 """Seeded random small configurations against the fp64 oracle: full-tensor
-prefill (with LSE) and a ragged decode batch per configuration, so corner
+prefill (with LSE) and a ragged decode batch per configuration, under the
+Eq. (3) map and the Sec. 4.5 frequency map, so corner
 combinations of length, GQA group, pretraining window and local window that
 the hand-picked cases miss are covered too.  The draw is fixed (seed 2607),
 so every run checks the same configurations."""
@@ -32,18 +33,21 @@ def _configs(n=16, seed=2607):
     return out
 
 
+@pytest.mark.parametrize("remote_map", ["alias", "freq"])
 @pytest.mark.parametrize("i,B,Hkv,g,L,w_pre,w0", _configs())
-def test_random_prefill_and_decode(i, B, Hkv, g, L, w_pre, w0):
+def test_random_prefill_and_decode(i, B, Hkv, g, L, w_pre, w0, remote_map):
     Hq = g * Hkv
     q, k, v = synth.prefill_inputs(B, Hq, Hkv, L, 128, seed=1000 + i, outlier_channels=8)
-    say("random config %d: B=%d Hkv=%d g=%d L=%d w_pre=%d w0=%d G=%d"
-        % (i, B, Hkv, g, L, w_pre, w0, api.group_size(L, w_pre)))
+    say("random config %d (%s): B=%d Hkv=%d g=%d L=%d w_pre=%d w0=%d G=%d"
+        % (i, remote_map, B, Hkv, g, L, w_pre, w0, api.group_size(L, w_pre)))
     qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)
     out = torch.full_like(qd, float("nan"))
     lse = torch.full((B, Hq, L), float("nan"), device="cuda")
-    api.bifocal_prefill(qd, kd, vd, w_pretrained=w_pre, w_local=w0, out=out, lse=lse)
+    api.bifocal_prefill(qd, kd, vd, w_pretrained=w_pre, w_local=w0, out=out, lse=lse,
+                        remote_map=remote_map)
     torch.cuda.synchronize()
-    want, want_lse = O.prefill(q, k, v, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    want, want_lse = O.prefill(q, k, v, theta=1e6, w_pretrained=w_pre, w_local=w0,
+                               remote_map=remote_map)
     assert_close(to_f64(out), want, what="prefill config %d" % i)
     assert_close(lse.cpu().numpy(), want_lse, max_abs=5e-2, mean_abs=5e-3, what="lse")
 
@@ -53,7 +57,8 @@ def test_random_prefill_and_decode(i, B, Hkv, g, L, w_pre, w0):
     lens = np.array([int(rng.integers(1, L + 1)) for _ in range(B)], dtype=np.int32)
     dq = np.stack([q[b, lens[b] - 1] for b in range(B)])
     dout = api.bifocal_decode(to_dev(dq), kd, vd, torch.from_numpy(lens).cuda(),
-                              w_pretrained=w_pre, w_local=w0)
+                              w_pretrained=w_pre, w_local=w0, remote_map=remote_map)
     torch.cuda.synchronize()
-    dwant, _, _ = O.decode(dq, k, v, lens, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    dwant, _, _ = O.decode(dq, k, v, lens, theta=1e6, w_pretrained=w_pre, w_local=w0,
+                           remote_map=remote_map)
     assert_close(to_f64(dout), dwant, what="decode config %d lens %s" % (i, [int(x) for x in lens]))
