@@ -62,3 +62,65 @@ def test_random_prefill_and_decode(i, B, Hkv, g, L, w_pre, w0, remote_map):
     dwant, _, _ = O.decode(dq, k, v, lens, theta=1e6, w_pretrained=w_pre, w_local=w0,
                            remote_map=remote_map)
     assert_close(to_f64(dout), dwant, what="decode config %d lens %s" % (i, [int(x) for x in lens]))
+
+
+@pytest.mark.parametrize("i,B,Hkv,g,L,w_pre,w0", _configs())
+def test_random_chunk_paged_and_packed_entries_agree(i, B, Hkv, g, L, w_pre, w0):
+    """On the same configurations, each serving entry point against the full
+    prefill of the same keys, bit for bit: a chunk of rows P .. L-1 over a
+    NaN-padded cache (G from its length L), the same chunk over shuffled
+    pages, and the batch packed into one varlen call (each sequence its own L)."""
+    Hq = g * Hkv
+    rng = np.random.default_rng(3000 + i)
+    q, k, v = synth.prefill_inputs(B, Hq, Hkv, L, 128, seed=1000 + i, outlier_channels=8)
+    qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)
+    full = api.bifocal_prefill(qd, kd, vd, w_pretrained=w_pre, w_local=w0)
+
+    P = int(rng.integers(0, L))
+    pad = int(rng.integers(0, 100))
+    nan = np.uint16(0x7FC0)
+    kc = np.full((B, L + pad, Hkv, 128), nan, dtype=np.uint16)
+    vc = np.full_like(kc, nan)
+    kc[:, :L], vc[:, :L] = k, v
+    say("random config %d: chunk P=%d of L=%d, pad %d" % (i, P, L, pad))
+    chunk = api.prefill_chunk(to_dev(q[:, P:]), to_dev(kc), to_dev(vc), q_start=P,
+                              w_pretrained=w_pre, w_local=w0)
+    torch.cuda.synchronize()
+    assert torch.equal(chunk.view(torch.int16), full[:, P:].view(torch.int16))
+
+    page = int(rng.choice([64, 128, 256]))
+    per_seq = (L + page - 1) // page
+    n_pages = B * per_seq + 2
+    order = rng.permutation(n_pages)
+    kp = np.full((n_pages, page, Hkv, 128), nan, dtype=np.uint16)
+    vp = np.full_like(kp, nan)
+    table = np.zeros((B, per_seq), dtype=np.int32)
+    for b in range(B):
+        for j in range(per_seq):
+            pg = int(order[b * per_seq + j])
+            table[b, j] = pg
+            lo, hi = j * page, min((j + 1) * page, L)
+            kp[pg, :hi - lo], vp[pg, :hi - lo] = k[b, lo:hi], v[b, lo:hi]
+    say("random config %d: paged chunk, page %d" % (i, page))
+    paged = api.prefill_chunk_paged(to_dev(q[:, P:]), to_dev(kp), to_dev(vp),
+                                    torch.from_numpy(table).cuda(), q_start=P,
+                                    w_pretrained=w_pre, w_local=w0)
+    torch.cuda.synchronize()
+    assert torch.equal(paged.view(torch.int16), chunk.view(torch.int16))
+
+    # the batch packed with a second, shorter copy of each sequence
+    cut = [L] + [int(rng.integers(1, L + 1)) for _ in range(B)]
+    seqs = [(0, cut[0])] + [(b, cut[1 + b]) for b in range(B)]
+    cu = np.cumsum([0] + [n for _, n in seqs]).astype(np.int32)
+    qp = np.concatenate([q[b, :n] for b, n in seqs])
+    kpk = np.concatenate([k[b, :n] for b, n in seqs])
+    vpk = np.concatenate([v[b, :n] for b, n in seqs])
+    say("random config %d: packed lengths %s" % (i, [n for _, n in seqs]))
+    packed = api.prefill_varlen(to_dev(qp), to_dev(kpk), to_dev(vpk), torch.from_numpy(cu).cuda(),
+                                max_seqlen=L, w_pretrained=w_pre, w_local=w0)
+    torch.cuda.synchronize()
+    for s_, (b, n) in enumerate(seqs):
+        alone = api.bifocal_prefill(to_dev(q[b:b + 1, :n]), to_dev(k[b:b + 1, :n]),
+                                    to_dev(v[b:b + 1, :n]), w_pretrained=w_pre, w_local=w0)
+        torch.cuda.synchronize()
+        assert torch.equal(packed[cu[s_]:cu[s_ + 1]].view(torch.int16), alone[0].view(torch.int16))
