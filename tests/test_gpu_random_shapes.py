@@ -124,3 +124,40 @@ def test_random_chunk_paged_and_packed_entries_agree(i, B, Hkv, g, L, w_pre, w0)
                                     to_dev(v[b:b + 1, :n]), w_pretrained=w_pre, w_local=w0)
         torch.cuda.synchronize()
         assert torch.equal(packed[cu[s_]:cu[s_ + 1]].view(torch.int16), alone[0].view(torch.int16))
+
+
+@pytest.mark.parametrize("i,B,Hkv,g,L,w_pre,w0", _configs())
+def test_random_paged_and_noalloc_decode_agree(i, B, Hkv, g, L, w_pre, w0):
+    """On the same configurations, the paged decode (shuffled pages) and the
+    no-alloc decode against the dense decode over the same keys, bit for bit,
+    with ragged lengths; the dense cache is padded to the pool's capacity so
+    all three take the same split plan."""
+    Hq = g * Hkv
+    rng = np.random.default_rng(4000 + i)
+    page = int(rng.choice([16, 32, 64]))
+    per_seq = (L + page - 1) // page
+    max_len = per_seq * page
+    lens = [int(rng.integers(1, L + 1)) for _ in range(B)]
+    q, kc, vc, lens = synth.decode_inputs(B, Hq, Hkv, max_len, lens, seed=5000 + i, nan_tail=True)
+    ld = torch.from_numpy(lens).cuda()
+    say("random config %d: decode lens %s, page %d" % (i, [int(x) for x in lens], page))
+    dense = api.bifocal_decode(to_dev(q), to_dev(kc), to_dev(vc), ld, w_pretrained=w_pre,
+                               w_local=w0)
+    noalloc = api.bifocal_decode_noalloc(to_dev(q), to_dev(kc), to_dev(vc), ld,
+                                         w_pretrained=w_pre, w_local=w0)
+    n_pages = B * per_seq + 3
+    order = rng.permutation(n_pages)
+    nan = np.uint16(0x7FC0)
+    kp = np.full((n_pages, page, Hkv, 128), nan, dtype=np.uint16)
+    vp = np.full_like(kp, nan)
+    table = np.zeros((B, per_seq), dtype=np.int32)
+    for b in range(B):
+        for j in range(per_seq):
+            pg = int(order[b * per_seq + j])
+            table[b, j] = pg
+            kp[pg], vp[pg] = kc[b, j * page:(j + 1) * page], vc[b, j * page:(j + 1) * page]
+    paged = api.decode_paged(to_dev(q), to_dev(kp), to_dev(vp), torch.from_numpy(table).cuda(),
+                             ld, w_pretrained=w_pre, w_local=w0)
+    torch.cuda.synchronize()
+    assert torch.equal(noalloc.view(torch.int16), dense.view(torch.int16))
+    assert torch.equal(paged.view(torch.int16), dense.view(torch.int16))
