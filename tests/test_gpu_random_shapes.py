@@ -161,3 +161,18 @@ def test_random_paged_and_noalloc_decode_agree(i, B, Hkv, g, L, w_pre, w0):
     torch.cuda.synchronize()
     assert torch.equal(noalloc.view(torch.int16), dense.view(torch.int16))
     assert torch.equal(paged.view(torch.int16), dense.view(torch.int16))
+
+
+@pytest.mark.parametrize("i,B,Hkv,g,L,w_pre,w0", _configs())
+def test_random_literal_mode(i, B, Hkv, g, L, w_pre, w0):
+    """The literal Eq. (7) prefill (three window passes and the merge) on the
+    same configurations, against the oracle's output and LSE."""
+    Hq = g * Hkv
+    q, k, v = synth.prefill_inputs(B, Hq, Hkv, L, 128, seed=1000 + i, outlier_channels=8)
+    say("random config %d: literal mode, G=%d" % (i, api.group_size(L, w_pre)))
+    out, lse = api.bifocal_prefill_literal(to_dev(q), to_dev(k), to_dev(v), w_pretrained=w_pre,
+                                           w_local=w0, want_lse=True)
+    torch.cuda.synchronize()
+    want, want_lse = O.prefill(q, k, v, theta=1e6, w_pretrained=w_pre, w_local=w0)
+    assert_close(to_f64(out), want, what="literal config %d" % i)
+    assert_close(lse.cpu().numpy(), want_lse, max_abs=5e-2, mean_abs=5e-3, what="literal lse")
