@@ -128,8 +128,8 @@ def test_random_chunk_paged_and_packed_entries_agree(i, B, Hkv, g, L, w_pre, w0)
 
 @pytest.mark.parametrize("i,B,Hkv,g,L,w_pre,w0", _configs())
 def test_random_paged_and_noalloc_decode_agree(i, B, Hkv, g, L, w_pre, w0):
-    """On the same configurations, the paged decode (shuffled pages) and the
-    no-alloc decode against the dense decode over the same keys, bit for bit,
+    """On the same configurations, the paged decode (shuffled pages, both remote
+    maps) and the no-alloc decode against the dense decode over the same keys, bit for bit,
     with ragged lengths; the dense cache is padded to the pool's capacity so
     all three take the same split plan."""
     Hq = g * Hkv
@@ -158,9 +158,15 @@ def test_random_paged_and_noalloc_decode_agree(i, B, Hkv, g, L, w_pre, w0):
             kp[pg], vp[pg] = kc[b, j * page:(j + 1) * page], vc[b, j * page:(j + 1) * page]
     paged = api.decode_paged(to_dev(q), to_dev(kp), to_dev(vp), torch.from_numpy(table).cuda(),
                              ld, w_pretrained=w_pre, w_local=w0)
+    # the same pages under the frequency map
+    dense_f = api.bifocal_decode(to_dev(q), to_dev(kc), to_dev(vc), ld, w_pretrained=w_pre,
+                                 w_local=w0, remote_map="freq")
+    paged_f = api.decode_paged(to_dev(q), to_dev(kp), to_dev(vp), torch.from_numpy(table).cuda(),
+                               ld, w_pretrained=w_pre, w_local=w0, remote_map="freq")
     torch.cuda.synchronize()
     assert torch.equal(noalloc.view(torch.int16), dense.view(torch.int16))
     assert torch.equal(paged.view(torch.int16), dense.view(torch.int16))
+    assert torch.equal(paged_f.view(torch.int16), dense_f.view(torch.int16))
 
 
 @pytest.mark.parametrize("i,B,Hkv,g,L,w_pre,w0", _configs())
