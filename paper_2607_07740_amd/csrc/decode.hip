@@ -19,9 +19,9 @@
 // once, to the view its distance selects (Eq. (1)), and scored against both
 // column groups; a column keeps only keys of its own view, so every column is
 // the partial softmax state (m, l, O) of one (head, view) pair: the local
-// window state and the remote-only state of Sec. 3.3.  The reduce kernel
-// merges all (split, view) states of a head with the max-shifted,
-// linear-space rule of Eq. (7) in fp32.
+// window state and the remote-only state of Sec. 3.3.  Each split merges its
+// head's two view states with the max-shifted, linear-space rule of Eq. (7)
+// in fp32, and the reduce kernel merges the splits' states the same way.
 #include <mutex>
 
 #include "jl_device.h"

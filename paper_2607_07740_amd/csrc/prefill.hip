@@ -6,11 +6,12 @@
 // Prefill is the inclusion-exclusion combination of attention passes over the
 // two views (Sec. 3.3, Eq. (7)), fused into one kernel.
 //
-// Two launches per call:
+// Launches per call:
 //  1. vt_prep_kernel transposes V into the byte image of each 64-key tile that
 //     the attention kernel reads in the PV product (a call-scoped buffer; the
 //     caller's K and V are only read).
-//  2. prefill_kernel reads raw (pre-RoPE) K tiles from memory straight into
+//  2. prefill_kernel, a fast pass and then a checked rerun of the blocks the
+//     fast pass listed (see the softmax below), reads raw (pre-RoPE) K tiles from memory straight into
 //     registers, 8 keys per wave, with the cos/sin rows of their positions,
 //     and rotates them to the view of the visit: k_loc = R(k) x_k on band
 //     tiles, k_rem = R(f(k)) x_k on remote tiles (Sec. 3.2, Eqs. (4)-(6): the
@@ -72,12 +73,9 @@ constexpr int kKeysPerWave = kPfBK / kPfWaves;
 //              16 lanes reading 16 consecutive keys at one chunk (the QK
 //              operand reads) hit 16 distinct bank groups, and so do 16 lanes
 //              covering chunks 0..7 (or 8..15) of an even and the following
-//              odd key (the rotation's reads and writes).
-//   cos/sin rows of a tile: row i (0..63) at i * 256 holds table row
-//              row0 + i (clamped to the tile's last row) as 64 fp16 pairs;
-//              its 16-byte chunk s (pairs 4s .. 4s+3) sits in slot s ^ (i & 1),
-//              so the rotation's lanes reading two consecutive rows hit
-//              distinct bank groups (lanes on one row read the same bytes).
+//              odd key (the rotation's writes).
+//   (The raw keys and their cos/sin rows go from memory to registers and
+//   never pass through LDS.)
 //   V^T image: d (0..127) at d * 128; slot s of a row holds the 8 keys of
 //              group g = s ^ ((d >> 1) & 7), g = 2 ks + h, in the order
 //              t -> key 16 ks + 8 (t / 4) + 4 h + t % 4 (the k order of the
@@ -890,8 +888,9 @@ size_t prefill_workspace_bytes(bool /*bifocal*/, int B, int Hkv, int L) {
 }
 
 // Literal mode workspace: O_A, O_B, O_C (fp32 [B][L][Hq][128] each), then
-// LSE_A, LSE_B, LSE_C (fp32 [B][Hq][L] each), then the V^T images at the next
-// 256-byte boundary (the window passes run checked, with no rerun list).
+// LSE_A, LSE_B, LSE_C (fp32 [B][Hq][L] each), then at the next 256-byte
+// boundary the V^T images and window B's rerun counter and list, laid out as
+// the library scratch (windows A and C run checked and use no list).
 static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L) {
   const size_t rows = (size_t)B * L * Hq;
@@ -1162,9 +1161,8 @@ static void varlen_sizes(int B, int T, int g, long long* nq, long long* nt) {
   *nt = ((long long)T + kPfBK - 1) / kPfBK + B;
 }
 
-// Scratch of a packed batch: the tile images of nt tiles per kv head (kv head
-// h's at h * nt), then the query-block and tile work lists.
-// Scratch of a packed call: the V^T images, the two work lists, the rerun
+// Scratch of a packed call: the V^T images of nt tiles per kv head (kv head
+// h's at h * nt), the query-block and tile work lists, the rerun counter and
 // list, then (frequency map only) the per-sequence remote tables, fp32 and
 // bf16, one row per token.
 static size_t varlen_lists_end(int B, int T, int Hq, int Hkv) {
