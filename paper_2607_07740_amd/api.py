@@ -141,7 +141,11 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _dev(t, name, dtype=None):
+def _dev(t, name, dtype=None, shape=None, device=None):
+    """Device pointer of a contiguous CUDA tensor.  The library reads and writes
+    through raw pointers, so a caller-supplied output must have exactly the
+    shape the call writes (shape), and every tensor must sit on the query's
+    device (device)."""
     import torch
     if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
         raise TypeError("%s must be a CUDA (HIP) tensor" % name)
@@ -149,7 +153,28 @@ def _dev(t, name, dtype=None):
         raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
     if not t.is_contiguous():
         raise ValueError("%s must be contiguous" % name)
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, the query on %s" % (name, t.device, device))
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _bf16(t, name, q, shape=None):
+    """A bf16 tensor of the call, on q's device."""
+    import torch
+    return _dev(t, name, torch.bfloat16, shape, q.device)
+
+
+def _f32(t, name, q, shape):
+    """An optional fp32 output (None passes a null pointer), on q's device."""
+    import torch
+    return None if t is None else _dev(t, name, torch.float32, shape, q.device)
+
+
+def _i32(t, name, q):
+    import torch
+    return _dev(t, name, torch.int32, None, q.device)
 
 
 def group_size(L: int, w_pretrained: int) -> int:
@@ -167,9 +192,8 @@ def _prefill(bifocal, q, k, v, w_pretrained, w_local, rope_theta, out, lse, want
         out = torch.empty_like(q)
     if lse is None and want_lse:
         lse = torch.empty((B, Hq, L), dtype=torch.float32, device=q.device)
-    args = [_dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
-            _dev(v, "v", torch.bfloat16), _dev(out, "out", torch.bfloat16),
-            _dev(lse, "lse", torch.float32) if lse is not None else None, B, Hq, Hkv, L, D,
+    args = [_bf16(q, "q", q), _bf16(k, "k", q), _bf16(v, "v", q),
+            _bf16(out, "out", q, q.shape), _f32(lse, "lse", q, (B, Hq, L)), B, Hq, Hkv, L, D,
             float(rope_theta)]
     if bifocal and remote_map != "alias":
         _check(lib().jl_bifocal_prefill_map(*args, int(w_pretrained), int(w_local),
@@ -214,9 +238,8 @@ def prefill_chunk(q, k_cache, v_cache, *, q_start: int, w_pretrained: int = 1, w
     want_lse = want_lse or lse is not None
     if lse is None and want_lse:
         lse = torch.empty((B, Hq, n), dtype=torch.float32, device=q.device)
-    args = [_dev(q, "q", torch.bfloat16), _dev(k_cache, "k_cache", torch.bfloat16),
-            _dev(v_cache, "v_cache", torch.bfloat16), _dev(out, "out", torch.bfloat16),
-            _dev(lse, "lse", torch.float32) if lse is not None else None, B, Hq, Hkv,
+    args = [_bf16(q, "q", q), _bf16(k_cache, "k_cache", q), _bf16(v_cache, "v_cache", q),
+            _bf16(out, "out", q, q.shape), _f32(lse, "lse", q, (B, Hq, n)), B, Hq, Hkv,
             int(q_start), n, max_len, D, float(rope_theta)]
     if bifocal:
         _check(lib().jl_bifocal_prefill_chunk(*args, int(w_pretrained), int(w_local),
@@ -246,11 +269,9 @@ def prefill_chunk_paged(q, k_pages, v_pages, block_table, *, q_start: int,
     want_lse = want_lse or lse is not None
     if lse is None and want_lse:
         lse = torch.empty((B, Hq, n), dtype=torch.float32, device=q.device)
-    args = [_dev(q, "q", torch.bfloat16), _dev(k_pages, "k_pages", torch.bfloat16),
-            _dev(v_pages, "v_pages", torch.bfloat16),
-            _dev(block_table, "block_table", torch.int32), max_pages, page_size, n_pages,
-            _dev(out, "out", torch.bfloat16),
-            _dev(lse, "lse", torch.float32) if lse is not None else None, B, Hq, Hkv,
+    args = [_bf16(q, "q", q), _bf16(k_pages, "k_pages", q), _bf16(v_pages, "v_pages", q),
+            _i32(block_table, "block_table", q), max_pages, page_size, n_pages,
+            _bf16(out, "out", q, q.shape), _f32(lse, "lse", q, (B, Hq, n)), B, Hq, Hkv,
             int(q_start), n, D, float(rope_theta)]
     if bifocal:
         _check(lib().jl_bifocal_prefill_chunk_paged(*args, int(w_pretrained), int(w_local),
@@ -281,10 +302,9 @@ def prefill_varlen(q, k, v, cu_seqlens, *, max_seqlen: int, w_pretrained: int = 
     want_lse = want_lse or lse is not None
     if lse is None and want_lse:
         lse = torch.empty((Hq, T), dtype=torch.float32, device=q.device)
-    args = [_dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
-            _dev(v, "v", torch.bfloat16), _dev(out, "out", torch.bfloat16),
-            _dev(lse, "lse", torch.float32) if lse is not None else None,
-            _dev(cu_seqlens, "cu_seqlens", torch.int32), B, T, int(max_seqlen), Hq, Hkv, D,
+    args = [_bf16(q, "q", q), _bf16(k, "k", q), _bf16(v, "v", q),
+            _bf16(out, "out", q, q.shape), _f32(lse, "lse", q, (Hq, T)),
+            _i32(cu_seqlens, "cu_seqlens", q), B, T, int(max_seqlen), Hq, Hkv, D,
             float(rope_theta)]
     if bifocal and remote_map != "alias":
         _check(lib().jl_bifocal_prefill_varlen_map(*args, int(w_pretrained), int(w_local),
@@ -325,10 +345,9 @@ def bifocal_prefill_literal(q, k, v, *, w_pretrained: int, w_local: int, rope_th
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
     _check(lib().jl_bifocal_prefill_literal(
-        _dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
-        _dev(v, "v", torch.bfloat16), _dev(out, "out", torch.bfloat16),
-        _dev(lse, "lse", torch.float32) if lse is not None else None, B, Hq, Hkv, L, D,
-        float(rope_theta), int(w_pretrained), int(w_local), _dev(workspace, "workspace"),
+        _bf16(q, "q", q), _bf16(k, "k", q), _bf16(v, "v", q), _bf16(out, "out", q, q.shape),
+        _f32(lse, "lse", q, (B, Hq, L)), B, Hq, Hkv, L, D, float(rope_theta), int(w_pretrained),
+        int(w_local), _dev(workspace, "workspace", device=q.device),
         workspace.numel() * workspace.element_size(), _stream(stream)))
     return (out, lse) if want_lse else out
 
@@ -359,10 +378,11 @@ def _decode(bifocal, q, k_cache, v_cache, kv_lens, w_pretrained, w_local, rope_t
     need = decode_workspace_bytes(B, Hq, Hkv, max_len, D)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
-    args = [_dev(q, "q", torch.bfloat16), _dev(k_cache, "k_cache", torch.bfloat16),
-            _dev(v_cache, "v_cache", torch.bfloat16), _dev(kv_lens, "kv_lens", torch.int32),
-            max_len, _dev(out, "out", torch.bfloat16), B, Hq, Hkv, D, float(rope_theta)]
-    ws = [_dev(workspace, "workspace"), workspace.numel() * workspace.element_size()]
+    args = [_bf16(q, "q", q), _bf16(k_cache, "k_cache", q), _bf16(v_cache, "v_cache", q),
+            _i32(kv_lens, "kv_lens", q), max_len, _bf16(out, "out", q, q.shape), B, Hq, Hkv, D,
+            float(rope_theta)]
+    ws = [_dev(workspace, "workspace", device=q.device),
+          workspace.numel() * workspace.element_size()]
     if bifocal:
         _check(lib().jl_bifocal_decode(*args, int(w_pretrained), int(w_local), *ws,
                                        _stream(stream)))
@@ -385,9 +405,9 @@ def bifocal_decode_noalloc(q, k_cache, v_cache, kv_lens, *, w_pretrained: int, w
     if out is None:
         out = torch.empty_like(q)
     _check(lib().jl_bifocal_decode_noalloc(
-        _dev(q, "q", torch.bfloat16), _dev(k_cache, "k_cache", torch.bfloat16),
-        _dev(v_cache, "v_cache", torch.bfloat16), _dev(kv_lens, "kv_lens", torch.int32),
-        max_len, _dev(out, "out", torch.bfloat16), B, Hq, Hkv, D, float(rope_theta),
+        _bf16(q, "q", q), _bf16(k_cache, "k_cache", q), _bf16(v_cache, "v_cache", q),
+        _i32(kv_lens, "kv_lens", q), max_len, _bf16(out, "out", q, q.shape), B, Hq, Hkv, D,
+        float(rope_theta),
         int(w_pretrained), int(w_local), _stream(stream)))
     return out
 
@@ -415,10 +435,10 @@ def bifocal_decode(q, k_cache, v_cache, kv_lens, *, w_pretrained: int, w_local: 
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
     _check(lib().jl_bifocal_decode_map(
-        _dev(q, "q", torch.bfloat16), _dev(k_cache, "k_cache", torch.bfloat16),
-        _dev(v_cache, "v_cache", torch.bfloat16), _dev(kv_lens, "kv_lens", torch.int32), max_len,
-        _dev(out, "out", torch.bfloat16), B, Hq, Hkv, D, float(rope_theta), int(w_pretrained),
-        int(w_local), REMOTE_MAPS[remote_map], _dev(workspace, "workspace"),
+        _bf16(q, "q", q), _bf16(k_cache, "k_cache", q), _bf16(v_cache, "v_cache", q),
+        _i32(kv_lens, "kv_lens", q), max_len, _bf16(out, "out", q, q.shape), B, Hq, Hkv, D,
+        float(rope_theta), int(w_pretrained), int(w_local), REMOTE_MAPS[remote_map],
+        _dev(workspace, "workspace", device=q.device),
         workspace.numel() * workspace.element_size(), _stream(stream)))
     return out
 
@@ -462,11 +482,12 @@ def decode_paged(q, k_pages, v_pages, block_table, kv_lens, *, w_pretrained: int
         need = decode_workspace_bytes(B, Hq, Hkv, max_pages * page_size, D)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
-    args = [_dev(q, "q", torch.bfloat16), _dev(k_pages, "k_pages", torch.bfloat16),
-            _dev(v_pages, "v_pages", torch.bfloat16), _dev(block_table, "block_table", torch.int32),
-            max_pages, page_size, n_pages, _dev(kv_lens, "kv_lens", torch.int32),
-            _dev(out, "out", torch.bfloat16), B, Hq, Hkv, D, float(rope_theta)]
-    ws = [_dev(workspace, "workspace"), workspace.numel() * workspace.element_size()]
+    args = [_bf16(q, "q", q), _bf16(k_pages, "k_pages", q), _bf16(v_pages, "v_pages", q),
+            _i32(block_table, "block_table", q), max_pages, page_size, n_pages,
+            _i32(kv_lens, "kv_lens", q), _bf16(out, "out", q, q.shape), B, Hq, Hkv, D,
+            float(rope_theta)]
+    ws = [_dev(workspace, "workspace", device=q.device),
+          workspace.numel() * workspace.element_size()]
     if bifocal and remote_map != "alias":
         _check(lib().jl_bifocal_decode_paged_map(*args, int(w_pretrained), int(w_local),
                                                  REMOTE_MAPS[remote_map], *ws, _stream(stream)))
