@@ -256,8 +256,9 @@ int jl_rope_attention(const void* q, const void* k, const void* v, void* o, floa
  * Bytes of device workspace jl_bifocal_prefill_literal needs for this shape:
  * 3 * B * L * Hq * head_dim * 4 (the window outputs) + the window LSEs
  * (3 * B * Hq * L * 4, rounded up to 256) + B * Hkv * ceil(L / 64) * 16 KB
- * (transposed value tiles) + 256 + 4 * B * Hkv * L (window B's list of query
- * blocks for the checked rerun).  Returns 0 for invalid arguments.
+ * (transposed value tiles) + 256 + 4 * B * Hkv * L (the window passes'
+ * counters and list of query blocks for the checked rerun).  Returns 0 for
+ * invalid arguments.
  */
 size_t jl_prefill_literal_workspace_bytes(int B, int Hq, int Hkv, int L, int head_dim);
 
@@ -265,8 +266,8 @@ size_t jl_prefill_literal_workspace_bytes(int B, int Hq, int Hkv, int L, int hea
  * Bifocal prefill with Eq. (7) of Sec. 3.3 taken literally: the three
  * attention calls A (band q - k <= w_local, base rotation), B (all causal
  * keys, remote rotation) and C (band, remote rotation) run as three calls
- * of the attention kernel (window B, the bulk of the work, as the fused call
- * runs: a fast pass, then a checked rerun of the blocks it lists), each
+ * of the attention kernel (each as the fused call runs: a fast pass, then a
+ * checked rerun of the blocks it lists), each
  * writing its normalised output O_X and its natural-log LSE_X, and a fourth
  * kernel merges them per row with
  *   M = max(LSE_A, LSE_B, LSE_C), W_X = exp(LSE_X - M),

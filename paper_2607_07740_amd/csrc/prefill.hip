@@ -65,6 +65,7 @@ constexpr int kRotOff = 0, kVtOff = 2 * kTileBytes;
 constexpr int kSmemBytes = 4 * kTileBytes;  // 64 KB
 constexpr int kPfCopyBytes = kTileBytes / kPfWaves;  // each wave's share of a tile copy: 8 keys
 constexpr int kKeysPerWave = kPfBK / kPfWaves;
+constexpr int kRetryCounters = 3;  // rerun counters at the head of the rerun area
 
 // LDS layouts.
 //   rotated K tile: key r (0..63) at r * 256; its 16-byte
@@ -113,8 +114,10 @@ __device__ inline size_t paged_row(int page, int n_pages, int page_shift, int k0
 // packed batch.  Keys past the sequence's length are written as zeros.
 __global__ __launch_bounds__(256) void vt_prep_kernel(PrepArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t sv[kPfBK * kHeadDim];
-  if (a.retry_count != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
-    *a.retry_count = 0;
+  // the rerun counters: one per attention pass that follows (the literal
+  // mode's three window passes use three)
+  if (a.retry_count != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < kRetryCounters)
+    a.retry_count[threadIdx.x] = 0;
   int tile, L;
   size_t seq_row, img;
   const int kvh_v = blockIdx.y;
@@ -321,8 +324,7 @@ __device__ inline void load_q_operand(const uint16_t* qrow, int half, const floa
 // any tile's probability sum exceeded 2^slack, and at the end whether a row's
 // total fell below 2^-slack.  A block with either writes nothing and lists
 // itself; the SAFE launch that follows reruns only the listed blocks with the
-// per-tile check, which moves the reference as needed.  Window modes always
-// run SAFE.
+// per-tile check, which moves the reference as needed.  Every mode runs so.
 template <int MODE, bool SAFE, bool PAGED = false>
 __global__ __launch_bounds__(kPfThreads, 2) void prefill_kernel(PrefillArgs a) {
   constexpr bool CHECK_LATE = !SAFE;
@@ -889,8 +891,8 @@ size_t prefill_workspace_bytes(bool /*bifocal*/, int B, int Hkv, int L) {
 
 // Literal mode workspace: O_A, O_B, O_C (fp32 [B][L][Hq][128] each), then
 // LSE_A, LSE_B, LSE_C (fp32 [B][Hq][L] each), then at the next 256-byte
-// boundary the V^T images and window B's rerun counter and list, laid out as
-// the library scratch (windows A and C run checked and use no list).
+// boundary the V^T images and the window passes' rerun counters and list,
+// laid out as the library scratch.
 static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t literal_workspace_bytes(int B, int Hq, int Hkv, int L) {
   const size_t rows = (size_t)B * L * Hq;
@@ -979,9 +981,7 @@ static hipError_t launch_fast_then_checked(const PrefillArgs& a, dim3 grid, hipS
 static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream) {
   const long long nwg = (long long)a.n_qblocks * a.B * a.Hkv;
   if (nwg > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  const dim3 grid((unsigned)nwg), block(kPfThreads);
-  PrefillArgs w = a;
-  w.retry_list = nullptr;  // the band windows A and C check every tile
+  const dim3 grid((unsigned)nwg);
   if (a.block_table != nullptr) {  // paged caches: the chunk entry points only
     if (mode == kModeFused) return launch_fast_then_checked<kModeFused, true>(a, grid, stream);
     if (mode == kModeVanilla) return launch_fast_then_checked<kModeVanilla, true>(a, grid, stream);
@@ -990,12 +990,11 @@ static hipError_t launch_attn(int mode, const PrefillArgs& a, hipStream_t stream
   switch (mode) {
     case kModeFused: return launch_fast_then_checked<kModeFused>(a, grid, stream);
     case kModeVanilla: return launch_fast_then_checked<kModeVanilla>(a, grid, stream);
-    case kModeWinA: hipLaunchKernelGGL((prefill_kernel<kModeWinA, true>), grid, block, 0, stream, w); break;
+    case kModeWinA: return launch_fast_then_checked<kModeWinA>(a, grid, stream);
     case kModeWinB: return launch_fast_then_checked<kModeWinB>(a, grid, stream);
-    case kModeWinC: hipLaunchKernelGGL((prefill_kernel<kModeWinC, true>), grid, block, 0, stream, w); break;
+    case kModeWinC: return launch_fast_then_checked<kModeWinC>(a, grid, stream);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 // Queries at positions q_start .. q_start + Lq - 1 (q, o: [B][Lq][Hq][128],
@@ -1040,17 +1039,21 @@ hipError_t launch_prefill_literal(const uint16_t* q, const uint16_t* k, const ui
                  round256(3 * rows * sizeof(float));
   PrefillArgs a = {};
   fill_geometry(a, B, Hq, Hkv, L, 0, L, slack);
-  // window B (every causal key, the bulk of the work) runs as the fused call
-  // does: a fast pass, then the checked rerun of the blocks it lists
+  // each window runs as the fused call does: a fast pass, then the checked
+  // rerun of the blocks it lists.  The passes count their blocks in counters
+  // of their own (all zeroed by the prep kernel) and share the list, which
+  // each pass's rerun has read before the next pass writes it (one stream).
   hipError_t e = launch_prep(k, v, table, rtable, table16, rtable16, freq_map, B, Hkv, L, L, G,
                              images, true, a, stream);
   if (e != hipSuccess) return e;
   a.q = q;
+  int* const counters = a.retry_count;
   const int modes[3] = {kModeWinA, kModeWinB, kModeWinC};
   for (int x = 0; x < 3; ++x) {
     a.o32 = o3 + (size_t)x * rows * kHeadDim;
     a.lse = lse3 + (size_t)x * rows;
     a.w0 = modes[x] == kModeWinB ? INT_MAX : w0;
+    a.retry_count = counters + x;
     e = launch_attn(modes[x], a, stream);
     if (e != hipSuccess) return e;
   }

@@ -311,7 +311,7 @@ def test_literal_workspace_size_and_rejections():
     o_bytes = 3 * B * L * Hq * 128 * 4
     lse_bytes = -(-3 * B * Hq * L * 4 // 256) * 256
     img = B * Hkv * (-(-L // 64)) * 16384  # V^T tile images only: K is read raw
-    retry = 256 + 4 * B * Hkv * L  # window B's list of blocks for the checked rerun
+    retry = 256 + 4 * B * Hkv * L  # the windows' counters and list of blocks for the checked rerun
     assert n == o_bytes + lse_bytes + img + retry
     assert api.prefill_literal_workspace_bytes(B, 7, Hkv, L) == 0
     assert api.prefill_literal_workspace_bytes(B, Hq, Hkv, L, 64) == 0
