@@ -36,3 +36,29 @@ def test_bench_main_keeps_decode_and_varlen_lengths_apart():
     assert "config_block(wp, wd, dlens," in main
     assert "(dq, dk, dv, dlens, wd)" in main
     assert "\n        lens = " not in main and "\n    lens = " not in main
+
+
+def test_traffic_is_reported_only_for_the_profiled_kernel_source(tmp_path, monkeypatch):
+    """bench.py reads the HBM traffic from the committed counter summary only
+    while that summary's source hash matches the kernel sources it runs."""
+    bench = _bench()
+    good = tmp_path / "good.txt"
+    good.write_text("# comment: ignored\nkernel_source_sha256: %s\nhbm_bytes_per_launch: 1.5e+10\n"
+                    % bench._kernel_hash())
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(good))
+    assert bench._traffic_from_profile() == 1.5e10
+    stale = tmp_path / "stale.txt"
+    stale.write_text("kernel_source_sha256: %s\nhbm_bytes_per_launch: 1.5e+10\n" % ("0" * 64))
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(stale))
+    assert bench._traffic_from_profile() is None
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "missing.txt"))
+    assert bench._traffic_from_profile() is None
+
+
+def test_more_than_one_gpu_is_refused():
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0
+    assert "--gpus 1" in r.stderr
