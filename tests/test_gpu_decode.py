@@ -157,6 +157,8 @@ def test_decode_band_covering_every_key_is_vanilla():
     a = _run(True, q, kc, vc, lens, w_pre, max_len - 1)
     b = _run(False, q, kc, vc, lens, w_pre, 0)
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    c = _run(True, q, kc, vc, lens, w_pre, 2 ** 31 - 1)  # the largest w_local
+    assert torch.equal(c.view(torch.int16), b.view(torch.int16))
     want, _, _ = O.decode(q, kc, vc, lens, theta=1e6, w_pretrained=w_pre, w_local=max_len - 1)
     assert_close(to_f64(a), want, what="decode band over every key")
 

@@ -191,7 +191,7 @@ def test_long_8b_64k_sampled_rows():
     _sampled_parity("qwen3_8b_prefill_64k", 16)
 
 
-@pytest.mark.parametrize("w0", [299, 1 << 30])
+@pytest.mark.parametrize("w0", [299, 1 << 30, 2 ** 31 - 1])
 def test_band_covering_every_key_is_vanilla(w0):
     """w_local >= L - 1 leaves no remote pair (Eq. (1)), so the bifocal call
     is the base model whatever G is (here G = 5): the fused kernel then visits
